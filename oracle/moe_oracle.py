@@ -1,0 +1,255 @@
+"""fp64 CPU oracle of one fused MoE layer -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this module.  The product path (the HIP library and
+its Python binding) never imports, calls or links it, and it never imports the
+product: the two sides share nothing but the seeded input data of
+``synth.moe_inputs``.
+
+What it computes is the paper's MoE skeleton, MoE Gate -> Fused MoE -> Weight
+Sum (Fig. 1; Fig. 3 and Sec. 5.1), with the numeric semantics of every
+quantised format spelled out (e4m3 format, scale granularity, zero point,
+layout; Sec. 6.2 and the "FP8 representation" row of Table 3).  The paper
+states no formula for the layer, so every step below is the plain definition
+of the operation, written out in float64 with library primitives (sort,
+bincount, matmul, exp) and no blocking or fusion:
+
+  gate      key_e = l_e (+ b_e)            softmax scoring
+            key_e = sigmoid(l_e) + b_e      sigmoid scoring (b: selection only)
+            top-k by key, descending, equal keys -> lower expert index first;
+            weights: softmax over the selected logits (renormalised) or the
+            full softmax; sigmoid scores over their selected sum
+            (renormalised) or raw; all times routed_scale.
+  permute   segment per expert (ascending e), each padded to a multiple of
+            block_m, flat ids t*k+j ascending inside a segment, pads = T*k.
+  experts   a = SiLU(x W1[e,:I]^T) * (x W1[e,I:]^T);  y = a W2[e]^T
+            with SiLU(g) = g / (1 + exp(-g)).
+  combine   out[t] = sum_j w[t,j] * y[t,j].
+
+Quantisation points the kernels take are mirrored (``mirror=True``):
+  * bf16 / int4 weights: the intermediate ``a`` is rounded to fp32, then to
+    bf16 (round to nearest even) before the second product;
+  * fp8: the hidden rows and the intermediate ``a`` are each quantised per
+    (row, 128-column group): s = fp32(max(amax, 1e-10) / 448) with an IEEE
+    fp32 divide, q = e4m3fn(RNE(fp32(x / s))) saturated to +-448, and the
+    product then uses q * s.
+With ``mirror=False`` the layer is evaluated on the unquantised operands.
+
+Every function here is pinned by the CPU tests (tests/test_oracle_*.py)
+against closed forms, brute force, invariants and an independent library
+implementation; nothing here is "parity unpinned".
+"""
+from __future__ import annotations
+
+import numpy as np
+
+E4M3_MAX = 448.0
+QGROUP = 128  # quantisation group along K (activations, int4 weights, fp8 blocks)
+
+
+# ============================================================ storage decoding
+def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns (uint16) -> exact float64 values."""
+    b = np.asarray(bits).astype(np.uint32) << np.uint32(16)
+    return b.view(np.float32).astype(np.float64)
+
+
+def f32_to_bf16_rne(x: np.ndarray) -> np.ndarray:
+    """fp32 values -> bf16 bit patterns, round to nearest, ties to even
+    (finite inputs).  Integer arithmetic on the fp32 bit pattern."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    lsb = (u >> np.uint64(16)) & np.uint64(1)
+    r = (u + np.uint64(0x7FFF) + lsb) >> np.uint64(16)
+    return r.astype(np.uint16)
+
+
+def e4m3_decode(codes: np.ndarray) -> np.ndarray:
+    """OCP fp8 e4m3fn codes -> float64.  Layout S.EEEE.MMM, exponent bias 7,
+    no infinities, S.1111.111 is NaN, E=0 encodes subnormals M * 2^-9."""
+    c = np.asarray(codes).astype(np.int64)
+    sign = np.where(c & 0x80, -1.0, 1.0)
+    e = (c >> 3) & 0xF
+    m = c & 0x7
+    val = np.where(e == 0, m * 2.0 ** -9, (1.0 + m / 8.0) * np.ldexp(1.0, e - 7))
+    val = np.where((e == 15) & (m == 7), np.nan, val)
+    return sign * val
+
+
+def e4m3_encode(x: np.ndarray) -> np.ndarray:
+    """Finite values -> e4m3fn codes: magnitude saturated to 448, then rounded
+    to the nearest representable value, ties to even mantissa."""
+    x = np.asarray(x, dtype=np.float64)
+    neg = np.signbit(x)
+    a = np.minimum(np.abs(x), E4M3_MAX)
+    _, ex = np.frexp(a)                      # a = f * 2^ex, f in [0.5, 1)
+    e = np.maximum(ex - 1, -6)               # binade of a; subnormals share 2^-6's step
+    step = np.ldexp(1.0, e - 3)              # 3 mantissa bits
+    r = np.rint(a / step) * step             # exact scaling, ties to even
+    # split r back into fields
+    _, ex2 = np.frexp(r)
+    e2 = ex2 - 1
+    is_norm = r >= 2.0 ** -6
+    exp_field = np.where(is_norm, e2 + 7, 0)
+    mant = np.where(is_norm, np.rint((r / np.ldexp(1.0, e2) - 1.0) * 8.0), np.rint(r / 2.0 ** -9))
+    exp_field = np.where(r == 0, 0, exp_field)
+    mant = np.where(r == 0, 0, mant)
+    code = (neg.astype(np.int64) << 7) | (exp_field.astype(np.int64) << 3) | mant.astype(np.int64)
+    return code.astype(np.uint8)
+
+
+def int4_unpack(words: np.ndarray) -> np.ndarray:
+    """int32 words [..., K/8] -> signed nibbles int8 [..., K]; element 8w+j is
+    bits [4j, 4j+4) of word w, two's complement."""
+    w = np.asarray(words).view(np.uint32)
+    out = np.empty(w.shape[:-1] + (w.shape[-1] * 8,), dtype=np.int8)
+    for j in range(8):
+        nib = ((w >> np.uint32(4 * j)) & np.uint32(0xF)).astype(np.int8)
+        out[..., j::8] = np.where(nib >= 8, nib - 16, nib)
+    return out
+
+
+def dequant_weight(wfmt: str, w: np.ndarray, scale) -> np.ndarray:
+    """One expert's stored weight [N, K] (+ scales) -> exact float64 values."""
+    if wfmt == "bf16":
+        return bf16_to_f64(w)
+    if wfmt == "fp8":
+        q = e4m3_decode(w)
+        s = np.asarray(scale, dtype=np.float64)            # [N/128, K/128]
+        return q * np.repeat(np.repeat(s, QGROUP, axis=0), QGROUP, axis=1)
+    if wfmt == "int4":
+        q = int4_unpack(w).astype(np.float64)              # [N, K]
+        s = bf16_to_f64(scale)                              # [N, K/128]
+        return q * np.repeat(s, QGROUP, axis=1)
+    raise ValueError(f"unknown weight format {wfmt!r}")
+
+
+# ============================================================ the layer
+def gate(logits, sel_bias, top_k, mode="softmax", renormalize=True, routed_scale=1.0):
+    """MoE Gate (Fig. 1): returns expert ids int32 [T,k] in descending-key
+    order (equal keys -> lower index first) and float64 weights [T,k]."""
+    lg = np.asarray(logits, dtype=np.float32).astype(np.float64)
+    T, E = lg.shape
+    if not 1 <= top_k <= E:
+        raise ValueError("top_k must be in [1, E]")
+    bias = np.zeros(E) if sel_bias is None else np.asarray(sel_bias, np.float32).astype(np.float64)
+    if mode == "softmax":
+        key = lg + bias[None, :]
+    elif mode == "sigmoid":
+        score = 1.0 / (1.0 + np.exp(-lg))
+        key = score + bias[None, :]
+    else:
+        raise ValueError(f"unknown scoring mode {mode!r}")
+    order = np.argsort(-key, axis=1, kind="stable")         # stable: ties keep index order
+    ids = order[:, :top_k].astype(np.int32)
+    if mode == "softmax":
+        sel = np.take_along_axis(lg, ids, axis=1)
+        if renormalize:
+            z = np.exp(sel - sel.max(axis=1, keepdims=True))
+            w = z / z.sum(axis=1, keepdims=True)
+        else:
+            m = lg.max(axis=1, keepdims=True)
+            w = np.exp(sel - m) / np.exp(lg - m).sum(axis=1, keepdims=True)
+    else:
+        sel = np.take_along_axis(score, ids, axis=1)
+        w = sel / sel.sum(axis=1, keepdims=True) if renormalize else sel
+    return ids, w * float(routed_scale)
+
+
+def permute_capacity(T, top_k, E, block_m):
+    return T * top_k + E * (block_m - 1)
+
+
+def permute(ids, E, block_m=1):
+    """Token -> expert permutation.  Returns expert_offsets [E+1],
+    sorted_ids [cap] (flat ids t*k+j, pads = T*k) and inv_pos [T*k]."""
+    flat = np.asarray(ids).reshape(-1).astype(np.int64)
+    n = flat.size
+    counts = np.bincount(flat, minlength=E)
+    padded = (counts + block_m - 1) // block_m * block_m
+    offsets = np.concatenate([[0], np.cumsum(padded)]).astype(np.int32)
+    cap = n + E * (block_m - 1)
+    sorted_ids = np.full(cap, n, dtype=np.int32)
+    inv_pos = np.empty(n, dtype=np.int32)
+    order = np.argsort(flat, kind="stable")                 # by expert, flat id ascending
+    start = 0
+    for e in range(E):
+        seg = order[start:start + counts[e]]
+        sorted_ids[offsets[e]:offsets[e] + counts[e]] = seg
+        inv_pos[seg] = offsets[e] + np.arange(counts[e])
+        start += counts[e]
+    return offsets, sorted_ids, inv_pos
+
+
+def act_quant_fp8(x32: np.ndarray):
+    """Per (row, 128-column group) e4m3 quantisation of fp32 rows [M, K]:
+    returns codes uint8 [M, K] and fp32 scales [M, K/128]."""
+    x = np.ascontiguousarray(x32, dtype=np.float32)
+    M, K = x.shape
+    g = x.reshape(M, K // QGROUP, QGROUP)
+    amax = np.abs(g).max(axis=2)
+    s = (np.maximum(amax, np.float32(1e-10)) / np.float32(E4M3_MAX)).astype(np.float32)
+    y = (g / s[:, :, None]).astype(np.float32)              # IEEE fp32 divide
+    return e4m3_encode(y).reshape(M, K), s
+
+
+def act_dequant_fp8(codes, scales):
+    M, K = codes.shape
+    return e4m3_decode(codes) * np.repeat(np.asarray(scales, np.float64), QGROUP, axis=1)
+
+
+def _round_intermediate(a: np.ndarray, wfmt: str) -> np.ndarray:
+    a32 = a.astype(np.float32)
+    if wfmt == "fp8":
+        return act_dequant_fp8(*act_quant_fp8(a32))
+    return bf16_to_f64(f32_to_bf16_rne(a32))
+
+
+def swiglu_expert(x, w1, w2, wfmt="bf16", mirror=True):
+    """One expert on rows x [M,H]: returns (a [M,I], y [M,H]) in float64."""
+    I = w1.shape[0] // 2
+    g = x @ w1[:I].T
+    u = x @ w1[I:].T
+    with np.errstate(over="ignore"):
+        a = g / (1.0 + np.exp(-g)) * u
+    if mirror:
+        a = _round_intermediate(a, wfmt)
+    return a, a @ w2.T
+
+
+def activation_operand(hidden_bits, wfmt="bf16", mirror=True):
+    """The first product's left operand for hidden rows (bf16 bits [M,H])."""
+    x = bf16_to_f64(hidden_bits)
+    if wfmt == "fp8" and mirror:
+        return act_dequant_fp8(*act_quant_fp8(x.astype(np.float32)))
+    return x
+
+
+def forward(cfg, inputs, mirror=True, tokens=None, want_rows=False):
+    """The whole layer.  ``tokens``: optional subset of token indices, in
+    which case ``out`` has one row per listed token (gate and experts run for
+    those tokens only).  Returns a dict with ids, w, out and, if
+    ``want_rows``, the per-routed-row intermediates ``a`` and ``y`` indexed by
+    (token slot, j)."""
+    T, k = cfg.T, cfg.top_k
+    tok = np.arange(T) if tokens is None else np.asarray(tokens, dtype=np.int64)
+    ids, w = gate(inputs["logits"][tok], inputs.get("sel_bias"), k, cfg.mode,
+                  cfg.renormalize, cfg.routed_scale)
+    x = activation_operand(inputs["hidden"][tok], cfg.wfmt, mirror)
+    n = tok.size
+    y = np.zeros((n * k, cfg.H))
+    a_rows = np.zeros((n * k, cfg.I)) if want_rows else None
+    flat = ids.reshape(-1)
+    for e in np.unique(flat):
+        rows = np.nonzero(flat == e)[0]                     # flat slots t*k+j, ascending
+        w1 = dequant_weight(cfg.wfmt, inputs["w1"][e], None if inputs["w1_scale"] is None else inputs["w1_scale"][e])
+        w2 = dequant_weight(cfg.wfmt, inputs["w2"][e], None if inputs["w2_scale"] is None else inputs["w2_scale"][e])
+        a, ye = swiglu_expert(x[rows // k], w1, w2, cfg.wfmt, mirror)
+        y[rows] = ye
+        if want_rows:
+            a_rows[rows] = a
+        del w1, w2
+    out = (w[:, :, None] * y.reshape(n, k, cfg.H)).sum(axis=1)
+    res = {"ids": ids, "w": w, "out": out}
+    if want_rows:
+        res["a"], res["y"] = a_rows, y
+    return res

@@ -1,0 +1,10 @@
+"""Seeded synthetic inputs for the fused MoE layer (data only, no layer arithmetic)."""
+from .moe_inputs import (  # noqa: F401
+    MoeConfig,
+    CONFIGS,
+    config,
+    tiny_config,
+    make_inputs,
+    make_routing_inputs,
+    make_expert_weights,
+)

@@ -1,0 +1,148 @@
+"""Pins of the oracle's storage codecs (bf16, OCP e4m3fn, packed int4) and of
+its weight dequantisation, against published tables, hand-derived rounding
+cases and an independent implementation (torch's CPU casts)."""
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import moe_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rows(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if line:
+                yield line.split()
+
+
+def test_e4m3_decode_matches_ocp_table():
+    for code, val, *_ in _rows("e4m3_ocp_table.txt"):
+        got = O.e4m3_decode(np.array([int(code, 16)]))[0]
+        if val == "nan":
+            assert math.isnan(got), code
+        else:
+            assert got == float(val) and math.copysign(1, got) == math.copysign(1, float(val)), code
+
+
+def test_e4m3_decode_all_codes_vs_torch():
+    codes = np.arange(256, dtype=np.uint8)
+    ours = O.e4m3_decode(codes)
+    ref = torch.from_numpy(codes).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(ours), nan)
+    assert np.array_equal(ours[~nan], ref[~nan])
+    assert nan.sum() == 2  # only S.1111.111
+
+
+def test_e4m3_encode_hand_rounding_cases():
+    for x, code, *_ in _rows("e4m3_rounding.txt"):
+        assert O.e4m3_encode(np.array([float(x)]))[0] == int(code, 16), x
+
+
+def test_e4m3_encode_roundtrip_every_finite_code():
+    codes = np.array([c for c in range(256) if (c & 0x7F) != 0x7F], dtype=np.uint8)
+    vals = O.e4m3_decode(codes)
+    assert np.array_equal(O.e4m3_encode(vals), codes)
+
+
+def test_e4m3_encode_dense_sweep_vs_torch():
+    rng = np.random.default_rng(0)
+    # every fp32 value on a fine grid across all binades, plus exact midpoints
+    grid = O.e4m3_decode(np.arange(0, 0x7F, dtype=np.uint8))
+    mids = (grid[:-1] + grid[1:]) / 2
+    x = np.concatenate([
+        np.ldexp(rng.uniform(1, 2, 200000), rng.integers(-12, 9, 200000)),
+        rng.uniform(0, 448, 200000), mids, grid,
+    ]).astype(np.float32)
+    x = np.concatenate([x, -x])
+    x = x[np.abs(x) <= 448]
+    ours = O.e4m3_encode(x)
+    ref = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    assert np.array_equal(ours, ref)
+
+
+def test_bf16_rne_hand_cases():
+    for xin, want, *_ in _rows("bf16_rounding.txt"):
+        x = np.array([int(xin, 16)], dtype=np.uint32).view(np.float32)
+        assert O.f32_to_bf16_rne(x)[0] == int(want, 16), xin
+
+
+def test_bf16_rne_sweep_vs_torch_and_exact_decode():
+    rng = np.random.default_rng(1)
+    bits = rng.integers(0, 2 ** 32, 400000, dtype=np.uint64).astype(np.uint32)
+    x = bits.view(np.float32)
+    x = x[np.isfinite(x)]
+    ours = O.f32_to_bf16_rne(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(ours, ref)
+    # decode is exact: every bf16 value is an fp32 value with 16 zero low bits
+    dec = O.bf16_to_f64(ours)
+    assert np.array_equal(dec.astype(np.float32).view(np.uint32) & 0xFFFF, np.zeros_like(ours, dtype=np.uint32))
+
+
+def test_int4_unpack_hand_cases():
+    for word, *elems in _rows("int4_packing.txt"):
+        w = np.array([int(word, 16)], dtype=np.uint32).view(np.int32)
+        assert O.int4_unpack(w).tolist() == [int(e) for e in elems], word
+
+
+def test_int4_pack_unpack_roundtrip():
+    rng = np.random.default_rng(2)
+    q = rng.integers(-8, 8, (5, 64)).astype(np.int64)
+    words = np.zeros((5, 8), dtype=np.uint32)
+    for j in range(8):
+        words |= (q[:, j::8] & 0xF).astype(np.uint32) << np.uint32(4 * j)
+    assert np.array_equal(O.int4_unpack(words.view(np.int32)), q)
+
+
+def test_fp8_block_dequant_scale_orientation():
+    # [N=256, K=384] all codes 1.0; block scales differ along both axes
+    w = np.full((256, 384), 0x38, dtype=np.uint8)
+    s = np.array([[1, 2, 3], [10, 20, 30]], dtype=np.float32)  # [N/128, K/128]
+    d = O.dequant_weight("fp8", w, s)
+    assert d[0, 0] == 1 and d[0, 200] == 2 and d[0, 300] == 3
+    assert d[200, 0] == 10 and d[200, 383] == 30 and d[127, 255] == 2 and d[128, 255] == 20
+
+
+def test_int4_group_dequant():
+    # [N=2, K=256]: element (n,k) = q * s[n, k // 128]
+    q = np.zeros((2, 256), dtype=np.int64)
+    q[0, 3], q[1, 130], q[1, 255] = -8, 7, -1
+    words = np.zeros((2, 32), dtype=np.uint32)
+    for j in range(8):
+        words |= (q[:, j::8] & 0xF).astype(np.uint32) << np.uint32(4 * j)
+    s = O.f32_to_bf16_rne(np.array([[0.5, 2.0], [0.25, 3.0]], dtype=np.float32))
+    d = O.dequant_weight("int4", words.view(np.int32), s)
+    assert d[0, 3] == -4.0 and d[1, 130] == 21.0 and d[1, 255] == -3.0
+    assert np.count_nonzero(d) == 3
+
+
+def test_act_quant_worked_groups():
+    x = np.zeros((3, 256), dtype=np.float32)
+    # group (0,0): amax = 448 -> scale exactly 1, on-grid values stay exact
+    x[0, :4] = [448.0, -1.0, 0.015625, 240.0]
+    # group (0,1): all zero -> scale 1e-10/448, codes 0
+    # group (1,0): amax 1 -> the max element hits the top code 0x7E
+    x[1, 5] = 1.0
+    x[1, 6] = -0.5
+    # group (2,1): halfway case after scaling by s = 2 (amax 896)
+    x[2, 128] = 896.0
+    x[2, 129] = 2.0 * 1.0625     # -> 1.0625 -> ties to 1.0
+    codes, s = O.act_quant_fp8(x)
+    assert s[0, 0] == 1.0 and s[2, 1] == 2.0
+    assert s[0, 1] == np.float32(np.float32(1e-10) / np.float32(448.0))
+    assert codes[0, :4].tolist() == [0x7E, 0xB8, 0x08, 0x77]
+    assert np.all(codes[0, 128:] == 0)
+    assert codes[1, 5] == 0x7E
+    assert codes[2, 128] == 0x7E and codes[2, 129] == 0x38
+    dq = O.act_dequant_fp8(codes, s)
+    assert dq[0, 0] == 448.0 and dq[2, 129] == 2.0
+    # every element is within half a grid step (relative 1/16) of its input
+    nz = x != 0
+    assert np.all(np.abs(dq[nz] - x[nz]) <= np.abs(x[nz]) / 16 + 1e-12)

@@ -1,0 +1,156 @@
+"""Pins of the oracle's whole layer: a hand-worked example, the dense SwiGLU
+special case against torch, identical-expert and token-order invariants, and a
+per-token brute force over every expert on tiny shapes."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import moe_oracle as O
+
+
+def _bits(x):
+    return O.f32_to_bf16_rne(np.asarray(x, dtype=np.float32))
+
+
+def _sig(x):
+    return 1 / (1 + math.exp(-x))
+
+
+def test_worked_two_expert_example():
+    """H=2, I=1, E=2.  Gate rows [0,I) of W1 and up rows [I,2I) are asymmetric,
+    so a gate/up swap, a transposed W2 or a dropped SiLU all change the result."""
+    cfg = synth.MoeConfig("worked", T=2, H=2, E=2, I=1, top_k=1)
+    inputs = {
+        "hidden": _bits([[1.0, 2.0], [0.5, -1.0]]),
+        "logits": np.array([[1.0, 0.0], [0.0, 1.0]], np.float32),
+        "sel_bias": None,
+        "w1": _bits([[[1.0, 0.0], [0.0, 1.0]], [[0.0, -1.0], [2.0, 0.0]]]),
+        "w2": _bits([[[1.0], [-2.0]], [[3.0], [0.5]]]),
+        "w1_scale": None, "w2_scale": None,
+    }
+    r = O.forward(cfg, inputs, mirror=False)
+    s1 = _sig(1.0)
+    # token 0 -> expert 0: g = 1, u = 2, a = 2*sigmoid(1); y = [a, -2a]
+    # token 1 -> expert 1: g = 1, u = 1, a = sigmoid(1);  y = [3a, a/2]
+    want = np.array([[2 * s1, -4 * s1], [3 * s1, 0.5 * s1]])
+    assert r["ids"].tolist() == [[0], [1]]
+    assert np.allclose(r["out"], want, rtol=0, atol=1e-15)
+    # top-2: token 0 mixes both experts with weights sigmoid(1), sigmoid(-1)
+    cfg2 = synth.MoeConfig("worked2", T=2, H=2, E=2, I=1, top_k=2)
+    r2 = O.forward(cfg2, inputs, mirror=False)
+    x0 = np.array([1.0, 2.0])
+    a1 = (lambda g, u: g * _sig(g) * u)(-2.0, 2.0)          # expert 1 on token 0
+    y1 = np.array([3 * a1, 0.5 * a1])
+    y0 = np.array([2 * s1, -4 * s1])
+    assert np.allclose(r2["out"][0], s1 * y0 + _sig(-1.0) * y1, rtol=0, atol=1e-15)
+    del x0
+
+
+def _dense_torch(x, w1, w2, round_intermediate=False):
+    x, w1, w2 = (torch.from_numpy(np.asarray(v, np.float64)) for v in (x, w1, w2))
+    I = w1.shape[0] // 2
+    a = torch.nn.functional.silu(x @ w1[:I].T) * (x @ w1[I:].T)
+    if round_intermediate:
+        a = a.to(torch.float32).to(torch.bfloat16).to(torch.float64)
+    return (a @ w2.T).numpy()
+
+
+@pytest.mark.parametrize("mirror", [False, True])
+def test_single_expert_top1_is_dense_swiglu(mirror):
+    cfg = synth.MoeConfig("dense", T=33, H=256, E=1, I=128, top_k=1, seed=11)
+    inp = synth.make_inputs(cfg)
+    r = O.forward(cfg, inp, mirror=mirror)
+    x = O.bf16_to_f64(inp["hidden"])
+    ref = _dense_torch(x, O.bf16_to_f64(inp["w1"][0]), O.bf16_to_f64(inp["w2"][0]), mirror)
+    rms = np.sqrt((ref ** 2).mean())
+    # unmirrored: identical math; mirrored: a bf16 tie may round the other way
+    tol = 1e-12 if not mirror else 2 ** -8
+    assert np.max(np.abs(r["out"] - ref)) <= tol * rms
+    assert np.all(r["w"] == 1.0)
+
+
+@pytest.mark.parametrize("n", [1, 4, 5])
+def test_identical_experts_any_routing(n):
+    cfg = synth.tiny_config(n)
+    inp = synth.make_inputs(cfg, identical_experts=True)
+    r = O.forward(cfg, inp, mirror=False)
+    w1 = O.dequant_weight(cfg.wfmt, inp["w1"][0], None if inp["w1_scale"] is None else inp["w1_scale"][0])
+    w2 = O.dequant_weight(cfg.wfmt, inp["w2"][0], None if inp["w2_scale"] is None else inp["w2_scale"][0])
+    ref = cfg.routed_scale * _dense_torch(O.bf16_to_f64(inp["hidden"]), w1, w2)
+    assert np.max(np.abs(r["out"] - ref)) <= 1e-12 * np.sqrt((ref ** 2).mean())
+
+
+@pytest.mark.parametrize("n", [1, 4, 5])
+def test_token_order_invariance(n):
+    cfg = synth.tiny_config(n)
+    inp = synth.make_inputs(cfg)
+    perm = np.random.default_rng(7).permutation(cfg.T)
+    inp2 = dict(inp, hidden=inp["hidden"][perm], logits=inp["logits"][perm])
+    r1 = O.forward(cfg, inp)
+    r2 = O.forward(cfg, inp2)
+    assert np.array_equal(r2["ids"], r1["ids"][perm])
+    rms = np.sqrt((r1["out"] ** 2).mean())
+    assert np.max(np.abs(r2["out"] - r1["out"][perm])) <= 1e-12 * rms
+
+
+def _brute_layer(cfg, inp, mirror):
+    """Per token: evaluate EVERY expert on the token, then pick the top-k by a
+    scan and weight-sum them in slot order.  Shares only the codecs."""
+    outs = []
+    lg = inp["logits"].astype(np.float64)
+    b = np.zeros(cfg.E) if inp["sel_bias"] is None else inp["sel_bias"].astype(np.float64)
+    ws = [(O.dequant_weight(cfg.wfmt, inp["w1"][e], None if inp["w1_scale"] is None else inp["w1_scale"][e]),
+           O.dequant_weight(cfg.wfmt, inp["w2"][e], None if inp["w2_scale"] is None else inp["w2_scale"][e]))
+          for e in range(cfg.E)]
+    for t in range(cfg.T):
+        x = O.activation_operand(inp["hidden"][t:t + 1], cfg.wfmt, mirror)[0]
+        ys = []
+        for w1, w2 in ws:
+            g = np.array([np.dot(w1[i], x) for i in range(cfg.I)])
+            u = np.array([np.dot(w1[cfg.I + i], x) for i in range(cfg.I)])
+            a = g * (1 / (1 + np.exp(-g))) * u
+            if mirror:
+                a = O._round_intermediate(a[None, :], cfg.wfmt)[0]
+            ys.append(np.array([np.dot(w2[h], a) for h in range(cfg.H)]))
+        if cfg.mode == "softmax":
+            key = lg[t] + b
+        else:
+            sc = 1 / (1 + np.exp(-lg[t]))
+            key = sc + b
+        chosen = []
+        for _ in range(cfg.top_k):
+            best = max((e for e in range(cfg.E) if e not in chosen), key=lambda e: (key[e], -e))
+            chosen.append(best)
+        if cfg.mode == "softmax":
+            z = np.exp(np.array([lg[t][e] for e in chosen]) - max(lg[t][e] for e in chosen))
+            w = z / z.sum()
+        else:
+            s = np.array([sc[e] for e in chosen])
+            w = s / s.sum()
+        w = w * cfg.routed_scale
+        outs.append(sum(w[j] * ys[chosen[j]] for j in range(cfg.top_k)))
+    return np.array(outs)
+
+
+@pytest.mark.parametrize("n", [1, 4, 5])
+@pytest.mark.parametrize("mirror", [False, True])
+def test_brute_force_tiny(n, mirror):
+    cfg = synth.tiny_config(n, T=9, H=256, I=128, E=6, top_k=3)
+    inp = synth.make_inputs(cfg)
+    r = O.forward(cfg, inp, mirror=mirror)
+    ref = _brute_layer(cfg, inp, mirror)
+    rms = np.sqrt((ref ** 2).mean())
+    assert np.max(np.abs(r["out"] - ref)) <= 1e-12 * rms
+
+
+def test_token_subset_matches_full():
+    cfg = synth.tiny_config(4)
+    inp = synth.make_inputs(cfg)
+    full = O.forward(cfg, inp)
+    tok = np.array([5, 0, cfg.T - 1, 17])
+    sub = O.forward(cfg, inp, tokens=tok)
+    assert np.array_equal(sub["ids"], full["ids"][tok])
+    assert np.allclose(sub["out"], full["out"][tok], rtol=0, atol=1e-12)
