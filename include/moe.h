@@ -1,0 +1,200 @@
+/*
+ * moe.h -- C ABI of the fused Mixture-of-Experts layer for AMD MI355X (gfx950).
+ *
+ * The layer is the paper's MoE skeleton, MoE Gate -> Fused MoE -> Weight Sum
+ * (Fig. 1; Fig. 3 and Sec. 5.1), for one GPU:
+ *
+ *   gate     router logits [T,E] -> top-k expert ids and weights per token
+ *   permute  token -> expert grouping (histogram, padded prefix scan, stable
+ *            scatter)
+ *   experts  per expert e and routed row x:  a = SiLU(x W1[e,:I]^T) * (x W1[e,I:]^T),
+ *            y = a W2[e]^T, SiLU(g) = g / (1 + exp(-g))
+ *   combine  out[t] = sum_j w[t,j] * y[t,j]            ("Weight Sum")
+ *
+ * Quantised weight formats carry their full numeric semantics in the format
+ * tag (e4m3 flavour, scale granularity, zero point, layout), as Sec. 6.2 and
+ * the "FP8 representation" row of Table 3 ask of quantisation dispatch.
+ *
+ * Conventions for every entry point:
+ *   - Pointers marked "device" are HIP device (or managed) memory owned by the
+ *     caller; the library never allocates, frees or retains them, and keeps no
+ *     state between calls.  All arrays are dense, row-major, contiguous.
+ *   - bf16 values are passed as their uint16_t bit patterns.
+ *   - Work is enqueued on `stream` and never synchronised; results are
+ *     available when the stream has drained.  Nothing is copied to the host.
+ *   - Arguments are validated on the host before anything is enqueued; on any
+ *     error nothing is enqueued and outputs are untouched.
+ *   - Calls on one stream are ordered; concurrent calls that share output or
+ *     workspace buffers race.
+ *   - Inputs must be finite; NaN/Inf inputs give unspecified results.
+ */
+#ifndef MOE_H
+#define MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MOE_OK = 0,
+  MOE_ERR_NULL = 1,        /* a required pointer is NULL                         */
+  MOE_ERR_SHAPE = 2,       /* a size is out of range or inconsistent             */
+  MOE_ERR_UNSUPPORTED = 3, /* valid request this library does not implement      */
+  MOE_ERR_ALIGN = 4,       /* a device pointer is not 16-byte aligned            */
+  MOE_ERR_WORKSPACE = 5,   /* workspace smaller than moe_workspace_bytes()       */
+  MOE_ERR_HIP = 6          /* a kernel launch failed (hipGetLastError)           */
+} moe_status;
+
+/* Router scoring (MoE Gate, Fig. 1). */
+typedef enum {
+  /* key_e = logit_e (+ sel_bias_e); weights = softmax over the selected
+     logits (renormalize=1) or the softmax over all E logits (renormalize=0). */
+  MOE_SCORE_SOFTMAX = 0,
+  /* s_e = 1/(1+exp(-logit_e)); key_e = s_e + sel_bias_e (selection only);
+     weights = s_j / sum_selected s (renormalize=1) or s_j (renormalize=0). */
+  MOE_SCORE_SIGMOID = 1
+} moe_score;
+
+/* Expert weight storage.  N x K below is [2I x H] for W1 and [H x I] for W2. */
+typedef enum {
+  /* bf16 bits, w[e][n][k] (uint16_t).  Needs H, I multiples of 128. */
+  MOE_W_BF16 = 0,
+  /* OCP fp8 e4m3fn codes (bias 7, max 448, no Inf, S.1111.111 = NaN),
+     w[e][n][k] (uint8_t); fp32 scale per 128x128 block of [N,K]:
+     scale[e][n/128][k/128]; value = decode(q) * scale.  Activations are then
+     quantised in-layer to e4m3 with an fp32 scale per (row, 128 columns):
+     s = max(amax, 1e-10) / 448 (IEEE fp32 divide), q = RNE(x / s) saturated
+     to +-448; the SwiGLU intermediate is quantised the same way. */
+  MOE_W_FP8E4M3_B128 = 1,
+  /* signed two's-complement int4, zero point 0, 8 per int32 along K: element
+     k = 8w+j sits in bits [4j,4j+4) of word w (low nibble first):
+     w[e][n][K/8] (int32_t); bf16 scale per 128 along K: scale[e][n][k/128];
+     value = q * scale. */
+  MOE_W_INT4_G128 = 2
+} moe_wfmt;
+
+typedef enum { MOE_OUT_F32 = 0, MOE_OUT_BF16 = 1 } moe_ofmt;
+
+/* Limits checked on the host. */
+#define MOE_MAX_EXPERTS 1024
+#define MOE_MAX_TOPK 32
+
+/*
+ * MoE Gate (Fig. 1): top-k expert selection per token.
+ *   logits    device fp32 [T,E]
+ *   sel_bias  device fp32 [E] or NULL (= zeros); enters the selection key only
+ *   T >= 0, 1 <= E <= MOE_MAX_EXPERTS, 1 <= top_k <= min(E, MOE_MAX_TOPK)
+ *   mode      moe_score; renormalize 0/1; routed_scale multiplies every weight
+ *   topk_ids  device int32 [T,top_k]: experts in descending key order; equal
+ *             keys -> lower expert index first.  Keys are compared in fp64
+ *             (the fp32 logit, or fp64 sigmoid + bias).
+ *   topk_w    device fp32 [T,top_k]: weights, computed in fp64, rounded once.
+ * Errors: MOE_ERR_NULL, MOE_ERR_SHAPE, MOE_ERR_ALIGN (logits/outputs need
+ * 4-byte alignment only), MOE_ERR_HIP.  T == 0 is a no-op.
+ */
+moe_status moe_gate_topk(const float* logits, const float* sel_bias, int T, int E, int top_k,
+                         int mode, int renormalize, float routed_scale, int32_t* topk_ids,
+                         float* topk_w, hipStream_t stream);
+
+/* Rows needed by moe_permute's sorted_ids: T*top_k + E*(block_m-1).  Host-only. */
+size_t moe_permute_capacity(int T, int top_k, int E, int block_m);
+
+/* Device scratch moe_permute needs (bytes).  Host-only, pure. */
+size_t moe_permute_workspace_bytes(int T, int top_k, int E);
+
+/*
+ * Permute / align: groups the T*top_k routed rows by expert.
+ *   topk_ids        device int32 [T,top_k], each in [0,E)
+ *   block_m         1..1024: every expert segment is padded to a multiple
+ *   expert_offsets  device int32 [E+1]: off[0]=0,
+ *                   off[e+1] = off[e] + roundup(count_e, block_m)
+ *   sorted_ids      device int32 [cap], cap >= moe_permute_capacity(): inside
+ *                   segment e the flat ids t*top_k+j of rows routed to e in
+ *                   ascending order, then pads; every slot from the pads of
+ *                   each segment up to cap holds the pad id T*top_k
+ *   inv_pos         device int32 [T*top_k]: position of flat id f in sorted_ids
+ *   ws, ws_bytes    device scratch of >= moe_permute_workspace_bytes()
+ * Deterministic: bit-identical on every run.
+ * Errors: MOE_ERR_NULL, MOE_ERR_SHAPE (cap too small, block_m out of range),
+ * MOE_ERR_WORKSPACE, MOE_ERR_HIP.  T == 0 writes offsets (all 0) and pads.
+ */
+moe_status moe_permute(const int32_t* topk_ids, int T, int top_k, int E, int block_m,
+                       int32_t* expert_offsets, int32_t* sorted_ids, int32_t* inv_pos, int cap,
+                       void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Activation quantisation for the fp8 format (done inside moe_forward; exposed
+ * for unit checks): per (row, 128-column group) of bf16 x [M,K]:
+ *   s = max(amax, 1e-10) / 448 (fp32, IEEE divide), q = e4m3fn(RNE(x / s))
+ *   saturated to +-448.
+ *   x  device bf16 bits [M,K]; q device uint8 [M,K]; s device fp32 [M,K/128]
+ * Needs K % 128 == 0 and 16-byte aligned pointers.
+ */
+moe_status moe_act_quant_fp8(const uint16_t* x, int M, int K, uint8_t* q, float* s,
+                             hipStream_t stream);
+
+/* The whole layer. */
+typedef struct moe_args {
+  int32_t T, H, E, I, top_k;
+  int32_t score_mode;       /* moe_score                                     */
+  int32_t renormalize;      /* 0 / 1                                          */
+  float routed_scale;       /* multiplies every routing weight               */
+  int32_t wfmt;             /* moe_wfmt                                       */
+  int32_t ofmt;             /* moe_ofmt                                       */
+  const float* sel_bias;    /* device fp32 [E] or NULL                        */
+  const uint16_t* hidden;   /* device bf16 [T,H]                              */
+  const float* logits;      /* device fp32 [T,E]                              */
+  const void* w1;           /* device, [E,2I,H] in the wfmt storage (gate rows [0,I), up rows [I,2I)) */
+  const void* w2;           /* device, [E,H,I] in the wfmt storage            */
+  const void* w1_scale;     /* device, per wfmt (NULL for bf16)               */
+  const void* w2_scale;     /* device, per wfmt (NULL for bf16)               */
+  void* out;                /* device [T,H], fp32 or bf16 per ofmt            */
+  int32_t* topk_ids_out;    /* optional device int32 [T,top_k] copy, or NULL  */
+  float* topk_w_out;        /* optional device fp32 [T,top_k] copy, or NULL   */
+} moe_args;
+
+/* Workspace bytes moe_forward needs for these sizes/format.  Host-only, pure. */
+size_t moe_workspace_bytes(const moe_args* a);
+
+/* Where moe_forward keeps its intermediates inside the workspace (byte
+   offsets; for inspection by tests and profilers).  -1 = not used. */
+typedef struct moe_ws_layout {
+  int64_t topk_ids, topk_w;          /* int32 / fp32 [T*top_k]                   */
+  int64_t expert_offsets;            /* int32 [E+1]                              */
+  int64_t sorted_ids, inv_pos;       /* int32 [cap], int32 [T*top_k]             */
+  int64_t act_q, act_s;              /* fp8: uint8 [T,H], fp32 [T,H/128]         */
+  int64_t inter, inter_s;            /* bf16 [cap,I] (fp8: uint8 [cap,I], fp32 [cap,I/128]) */
+  int64_t y;                         /* [cap,H] rows in sorted order: fp32 for bf16
+                                        weights, bf16 for fp8 / int4; pad rows unspecified */
+  int64_t permute_ws;                /* moe_permute scratch                      */
+  int32_t block_m, cap;              /* padding granule and sorted_ids length   */
+  int64_t total;                     /* == moe_workspace_bytes                  */
+} moe_ws_layout;
+
+moe_status moe_workspace_layout(const moe_args* a, moe_ws_layout* layout);
+
+/*
+ * Fused MoE layer: gate -> permute -> [fp8 activation quantisation] ->
+ * grouped GEMM1 with fused SiLU*up epilogue -> grouped GEMM2 -> combine, all
+ * enqueued on `stream`; no host synchronisation, no allocation.
+ * Requirements: T >= 0; 1 <= E <= MOE_MAX_EXPERTS; 1 <= top_k <= min(E,
+ * MOE_MAX_TOPK); H and I multiples of 128; every device pointer 16-byte
+ * aligned; ws_bytes >= moe_workspace_bytes(a); sel_bias only with a format
+ * that reads it (both scoring modes do).  Padding rows of the intermediates
+ * are unspecified.  T == 0 is a no-op.
+ * Errors: MOE_ERR_NULL, MOE_ERR_SHAPE, MOE_ERR_UNSUPPORTED, MOE_ERR_ALIGN,
+ * MOE_ERR_WORKSPACE, MOE_ERR_HIP.
+ */
+moe_status moe_forward(const moe_args* a, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Static, NUL-terminated name of a status code. */
+const char* moe_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOE_H */

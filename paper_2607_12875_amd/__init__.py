@@ -1,0 +1,12 @@
+"""Fused Mixture-of-Experts layer for AMD MI355X (gfx950).
+
+MoE Gate -> Fused MoE -> Weight Sum (the paper's MoE skeleton, Fig. 1 and
+Fig. 3) as hand-written HIP kernels behind the C ABI of include/moe.h; this
+package is the thin Python binding over that library (``_binding``) and its
+build script (``build``).
+"""
+from ._binding import (  # noqa: F401
+    LIB_PATH, MoeArgs, MoeError, lib, make_args, moe_act_quant_fp8, moe_forward,
+    moe_forward_args, moe_gate_topk, moe_permute, moe_permute_capacity,
+    moe_permute_workspace_bytes, moe_workspace_bytes, moe_workspace_layout,
+)

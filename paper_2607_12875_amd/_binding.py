@@ -1,0 +1,212 @@
+"""Thin ctypes binding of ``libmoe_mi355x.so`` (declared in include/moe.h).
+
+Argument marshalling only: every step of the layer runs in the library's HIP
+kernels.  torch supplies device memory and the current HIP stream.  There is no
+fallback of any kind: a missing library or a non-OK status raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmoe_mi355x.so")
+
+MOE_OK = 0
+MOE_ERR_NULL, MOE_ERR_SHAPE, MOE_ERR_UNSUPPORTED, MOE_ERR_ALIGN, MOE_ERR_WORKSPACE, MOE_ERR_HIP = range(1, 7)
+STATUS_NAMES = {0: "MOE_OK", 1: "MOE_ERR_NULL", 2: "MOE_ERR_SHAPE", 3: "MOE_ERR_UNSUPPORTED",
+                4: "MOE_ERR_ALIGN", 5: "MOE_ERR_WORKSPACE", 6: "MOE_ERR_HIP"}
+SCORE = {"softmax": 0, "sigmoid": 1}
+WFMT = {"bf16": 0, "fp8": 1, "int4": 2}
+OFMT = {"f32": 0, "bf16": 1}
+
+EXPORTED = ("moe_status_str", "moe_permute_capacity", "moe_permute_workspace_bytes",
+            "moe_gate_topk", "moe_permute", "moe_act_quant_fp8", "moe_workspace_bytes",
+            "moe_workspace_layout", "moe_forward")
+
+
+class MoeError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {STATUS_NAMES.get(status, status)}")
+        self.status = status
+
+
+class MoeArgs(ctypes.Structure):
+    _fields_ = [
+        ("T", ctypes.c_int32), ("H", ctypes.c_int32), ("E", ctypes.c_int32),
+        ("I", ctypes.c_int32), ("top_k", ctypes.c_int32),
+        ("score_mode", ctypes.c_int32), ("renormalize", ctypes.c_int32),
+        ("routed_scale", ctypes.c_float), ("wfmt", ctypes.c_int32), ("ofmt", ctypes.c_int32),
+        ("sel_bias", ctypes.c_void_p), ("hidden", ctypes.c_void_p), ("logits", ctypes.c_void_p),
+        ("w1", ctypes.c_void_p), ("w2", ctypes.c_void_p),
+        ("w1_scale", ctypes.c_void_p), ("w2_scale", ctypes.c_void_p),
+        ("out", ctypes.c_void_p), ("topk_ids_out", ctypes.c_void_p), ("topk_w_out", ctypes.c_void_p),
+    ]
+
+
+class MoeWsLayout(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in (
+        "topk_ids", "topk_w", "expert_offsets", "sorted_ids", "inv_pos", "act_q", "act_s",
+        "inter", "inter_s", "y", "permute_ws")] + [
+        ("block_m", ctypes.c_int32), ("cap", ctypes.c_int32), ("total", ctypes.c_int64)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load the library once; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_2607_12875_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, f32, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+        L.moe_status_str.restype = ctypes.c_char_p
+        L.moe_status_str.argtypes = [i32]
+        L.moe_permute_capacity.restype = sz
+        L.moe_permute_capacity.argtypes = [i32, i32, i32, i32]
+        L.moe_permute_workspace_bytes.restype = sz
+        L.moe_permute_workspace_bytes.argtypes = [i32, i32, i32]
+        L.moe_gate_topk.restype = i32
+        L.moe_gate_topk.argtypes = [vp, vp, i32, i32, i32, i32, i32, f32, vp, vp, vp]
+        L.moe_permute.restype = i32
+        L.moe_permute.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, i32, vp, sz, vp]
+        L.moe_act_quant_fp8.restype = i32
+        L.moe_act_quant_fp8.argtypes = [vp, i32, i32, vp, vp, vp]
+        L.moe_workspace_bytes.restype = sz
+        L.moe_workspace_bytes.argtypes = [ctypes.POINTER(MoeArgs)]
+        L.moe_workspace_layout.restype = i32
+        L.moe_workspace_layout.argtypes = [ctypes.POINTER(MoeArgs), ctypes.POINTER(MoeWsLayout)]
+        L.moe_forward.restype = i32
+        L.moe_forward.argtypes = [ctypes.POINTER(MoeArgs), vp, sz, vp]
+        _lib = L
+    return _lib
+
+
+def _check(status: int, where: str):
+    if status != MOE_OK:
+        raise MoeError(status, where)
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev(*ts):
+    for t in ts:
+        if t is not None and (not t.is_cuda or not t.is_contiguous()):
+            raise ValueError("tensors must be contiguous device tensors")
+
+
+# ------------------------------------------------------------------ entry points
+def moe_permute_capacity(T: int, top_k: int, E: int, block_m: int) -> int:
+    return lib().moe_permute_capacity(T, top_k, E, block_m)
+
+
+def moe_permute_workspace_bytes(T: int, top_k: int, E: int) -> int:
+    return lib().moe_permute_workspace_bytes(T, top_k, E)
+
+
+def moe_gate_topk(logits, top_k, mode="softmax", renormalize=True, routed_scale=1.0,
+                  sel_bias=None, topk_ids=None, topk_w=None, stream=None):
+    """MoE Gate: returns (topk_ids int32 [T,k], topk_w fp32 [T,k])."""
+    _dev(logits, sel_bias)
+    T, E = logits.shape
+    if topk_ids is None:
+        topk_ids = torch.empty((T, top_k), dtype=torch.int32, device=logits.device)
+    if topk_w is None:
+        topk_w = torch.empty((T, top_k), dtype=torch.float32, device=logits.device)
+    _check(lib().moe_gate_topk(_ptr(logits), _ptr(sel_bias), T, E, top_k, SCORE[mode],
+                               int(renormalize), float(routed_scale), _ptr(topk_ids),
+                               _ptr(topk_w), _stream(stream)), "moe_gate_topk")
+    return topk_ids, topk_w
+
+
+def moe_permute(topk_ids, E: int, block_m: int, stream=None):
+    """Permute/align: returns (expert_offsets [E+1], sorted_ids [cap], inv_pos [T*k])."""
+    _dev(topk_ids)
+    T, k = topk_ids.shape
+    dev = topk_ids.device
+    cap = moe_permute_capacity(T, k, E, block_m)
+    offsets = torch.empty(E + 1, dtype=torch.int32, device=dev)
+    sorted_ids = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+    inv_pos = torch.empty(max(T * k, 1), dtype=torch.int32, device=dev)
+    nws = moe_permute_workspace_bytes(T, k, E)
+    ws = torch.empty(max(nws, 16), dtype=torch.uint8, device=dev)
+    _check(lib().moe_permute(_ptr(topk_ids), T, k, E, block_m, _ptr(offsets), _ptr(sorted_ids),
+                             _ptr(inv_pos), cap, _ptr(ws), nws, _stream(stream)), "moe_permute")
+    return offsets, sorted_ids[:cap], inv_pos[:T * k]
+
+
+def moe_act_quant_fp8(x, stream=None):
+    """Per (row, 128-column) e4m3 quantisation of bf16 x [M,K] -> (codes uint8, scales fp32)."""
+    _dev(x)
+    M, K = x.shape
+    q = torch.empty((M, K), dtype=torch.uint8, device=x.device)
+    s = torch.empty((M, max(K // 128, 1)), dtype=torch.float32, device=x.device)
+    _check(lib().moe_act_quant_fp8(_ptr(x), M, K, _ptr(q), _ptr(s), _stream(stream)),
+           "moe_act_quant_fp8")
+    return q, s
+
+
+def make_args(T, H, E, I, top_k, *, mode="softmax", renormalize=True, routed_scale=1.0,
+              wfmt="bf16", out_dtype="f32", hidden=None, logits=None, w1=None, w2=None,
+              w1_scale=None, w2_scale=None, sel_bias=None, out=None, topk_ids_out=None,
+              topk_w_out=None) -> MoeArgs:
+    return MoeArgs(T, H, E, I, top_k, SCORE[mode], int(renormalize), float(routed_scale),
+                   WFMT[wfmt], OFMT[out_dtype], _ptr(sel_bias), _ptr(hidden), _ptr(logits),
+                   _ptr(w1), _ptr(w2), _ptr(w1_scale), _ptr(w2_scale), _ptr(out),
+                   _ptr(topk_ids_out), _ptr(topk_w_out))
+
+
+def moe_workspace_bytes(args: MoeArgs) -> int:
+    return lib().moe_workspace_bytes(ctypes.byref(args))
+
+
+def moe_workspace_layout(args: MoeArgs) -> dict:
+    L = MoeWsLayout()
+    _check(lib().moe_workspace_layout(ctypes.byref(args), ctypes.byref(L)), "moe_workspace_layout")
+    return {name: getattr(L, name) for name, _ in MoeWsLayout._fields_}
+
+
+def moe_forward_args(args: MoeArgs, workspace, stream=None):
+    """Run the layer on a prepared MoeArgs with a caller-owned uint8 workspace."""
+    _check(lib().moe_forward(ctypes.byref(args), _ptr(workspace), workspace.numel(),
+                             _stream(stream)), "moe_forward")
+
+
+def moe_forward(hidden, logits, w1, w2, top_k, *, mode="softmax", renormalize=True,
+                routed_scale=1.0, wfmt="bf16", sel_bias=None, w1_scale=None, w2_scale=None,
+                out_dtype="f32", out=None, workspace=None, topk_ids_out=None, topk_w_out=None,
+                stream=None):
+    """The whole layer on device tensors; returns (out [T,H], workspace).
+
+    hidden bf16 [T,H]; logits fp32 [T,E]; weights in the wfmt storage:
+    bf16 [E,2I,H] / [E,H,I]; fp8 uint8 codes with fp32 block scales
+    [E,2I/128,H/128] / [E,H/128,I/128]; int4 int32 [E,2I,H/8] / [E,H,I/8] with
+    bf16 scales [E,2I,H/128] / [E,H,I/128]."""
+    _dev(hidden, logits, w1, w2, sel_bias, w1_scale, w2_scale, out, topk_ids_out, topk_w_out)
+    T, H = hidden.shape
+    E = logits.shape[1]
+    I = w2.shape[2] * (8 if wfmt == "int4" else 1)
+    if out is None:
+        out = torch.empty((T, H), dtype=torch.float32 if out_dtype == "f32" else torch.bfloat16,
+                          device=hidden.device)
+    args = make_args(T, H, E, I, top_k, mode=mode, renormalize=renormalize,
+                     routed_scale=routed_scale, wfmt=wfmt, out_dtype=out_dtype, hidden=hidden,
+                     logits=logits, w1=w1, w2=w2, w1_scale=w1_scale, w2_scale=w2_scale,
+                     sel_bias=sel_bias, out=out, topk_ids_out=topk_ids_out, topk_w_out=topk_w_out)
+    need = moe_workspace_bytes(args)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=hidden.device)
+    moe_forward_args(args, workspace, stream)
+    return out, workspace

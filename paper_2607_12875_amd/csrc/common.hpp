@@ -1,0 +1,84 @@
+// Shared device helpers for the gfx950 (CDNA4) MoE kernels: vector types,
+// bf16 / e4m3 conversions, MFMA wrappers and wavefront reductions.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace moe {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// Round-to-nearest-even fp32 -> bf16 (v_cvt_pk_bf16_f32 on gfx950).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+}
+
+// Two fp32 -> two OCP e4m3fn codes in the low 16 bits (round to nearest even;
+// callers saturate to +-448 first).
+__device__ __forceinline__ uint32_t f32x2_to_e4m3(float a, float b) {
+  return static_cast<uint32_t>(__builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false)) & 0xFFFFu;
+}
+
+__device__ __forceinline__ float sat_e4m3(float x) {
+  return fminf(fmaxf(x, -448.0f), 448.0f);
+}
+
+// D(16x16, fp32) += A(16x32, bf16) * B(32x16, bf16).
+// Lane l holds A row (l % 16), B column (l % 16), eight consecutive k of the
+// k-group (l / 16); D rows 4*(l/16) + i, column l % 16.
+__device__ __forceinline__ f32x4 mfma16x16x32(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// D(32x32, fp32) += A(32x16, bf16) * B(16x32, bf16).
+// Lane l holds A row (l % 32), B column (l % 32), eight consecutive k of the
+// k-group (l / 32); D element v: row 8*(v/4) + 4*(l/32) + v%4, column l % 32.
+__device__ __forceinline__ f32x16 mfma32x32x16(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// D(16x16, fp32) += A(16x128, e4m3) * B(128x16, e4m3); lane l holds 32
+// consecutive k of k-group (l / 16) for row / column (l % 16).
+__device__ __forceinline__ f32x4 mfma16x16x128_fp8(const i32x8& a, const i32x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+
+// D(32x32, fp32) += A(32x64, e4m3) * B(64x32, e4m3); lane l holds 32
+// consecutive k of k-group (l / 32) for row / column (l % 32).
+__device__ __forceinline__ f32x16 mfma32x32x64_fp8(const i32x8& a, const i32x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ float silu_mul(float g, float u) {
+  return g / (1.0f + __expf(-g)) * u;
+}
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+
+// Index e with off[e] <= p < off[e+1] (off non-decreasing, off[0] = 0 <= p < off[E]).
+__device__ __forceinline__ int find_segment(const int32_t* __restrict__ off, int E, int p) {
+  int lo = 0, hi = E;  // invariant: off[lo] <= p < off[hi]
+  while (hi - lo > 1) {
+    int mid = (lo + hi) >> 1;
+    if (off[mid] <= p) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+}  // namespace moe

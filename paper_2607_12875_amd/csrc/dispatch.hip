@@ -1,0 +1,29 @@
+// Per-format dispatch of the grouped expert GEMMs.
+#include "launch.hpp"
+
+namespace moe {
+
+int gemm_block_m_bf16(int T, int top_k, int E);
+hipError_t launch_gemms_bf16(const GroupedGemm& g, hipStream_t s);
+int gemm_block_m_fp8(int T, int top_k, int E);
+hipError_t launch_gemms_fp8(const GroupedGemm& g, hipStream_t s);
+int gemm_block_m_int4(int T, int top_k, int E);
+hipError_t launch_gemms_int4(const GroupedGemm& g, hipStream_t s);
+
+int gemm_block_m(int wfmt, int T, int top_k, int E) {
+  switch (wfmt) {
+    case 1: return gemm_block_m_fp8(T, top_k, E);
+    case 2: return gemm_block_m_int4(T, top_k, E);
+    default: return gemm_block_m_bf16(T, top_k, E);
+  }
+}
+
+hipError_t launch_expert_gemms(int wfmt, const GroupedGemm& g, hipStream_t s) {
+  switch (wfmt) {
+    case 1: return launch_gemms_fp8(g, s);
+    case 2: return launch_gemms_int4(g, s);
+    default: return launch_gemms_bf16(g, s);
+  }
+}
+
+}  // namespace moe

@@ -1,0 +1,53 @@
+// Internal launchers of the MoE kernels (host side).  Shapes are validated by
+// the C ABI layer (moe_api.hip) before any of these is called.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+namespace moe {
+
+hipError_t launch_gate_topk(const float* logits, const float* bias, int T, int E, int k, int mode,
+                            int renorm, float scale, int32_t* ids, float* w, int32_t* ids2,
+                            float* w2, hipStream_t s);
+
+int permute_chunk(int E);
+size_t permute_workspace_bytes(int T, int k, int E);
+hipError_t launch_permute(const int32_t* ids, int T, int k, int E, int block_m, int32_t* offsets,
+                          int32_t* sorted_ids, int32_t* inv_pos, int cap, void* ws,
+                          hipStream_t s);
+
+// y: [cap, H] rows in sorted order, fp32 (y_f32) or bf16.
+hipError_t launch_combine(const void* y, bool y_f32, const float* w, const int32_t* inv_pos, int T,
+                          int H, int k, bool out_bf16, void* out, hipStream_t s);
+
+hipError_t launch_act_quant(const uint16_t* x, int M, int K, uint8_t* q, float* s, hipStream_t st);
+
+// Grouped expert GEMMs.  Rows are the permuted routed rows (sorted order),
+// grouped by expert in segments padded to a multiple of the kernel's row tile;
+// `offsets` is the permute's expert_offsets[E+1], `max_rows` the capacity.
+struct GroupedGemm {
+  // first product: A rows are hidden[sorted_ids[p] / top_k] (pads read row 0)
+  const void* x;              // bf16 hidden [T,H] (fp8: e4m3 codes [T,H])
+  const float* x_scale;       // fp8 only: [T, H/128]
+  const int32_t* sorted_ids;  // [cap]
+  const int32_t* offsets;     // [E+1]
+  int T, H, E, I, top_k, n_routed, max_rows;
+  const void* w1;             // [E, 2I, H] in storage format
+  const void* w1_scale;
+  const void* w2;             // [E, H, I]
+  const void* w2_scale;
+  void* inter;                // [cap, I] bf16 (fp8: e4m3 codes)
+  float* inter_scale;         // fp8 only: [cap, I/128]
+  void* y;                    // [cap, H]: fp32 for bf16 weights, bf16 otherwise
+};
+
+// y is kept in fp32 for bf16 weights (their 2e-2 output tolerance has no room
+// for a bf16 rounding of every routed row) and in bf16 for fp8 / int4.
+inline bool y_is_f32(int wfmt) { return wfmt == 0; }
+
+// Row tile (padding granule) the kernels for this format/shape use.
+int gemm_block_m(int wfmt, int T, int top_k, int E);
+hipError_t launch_expert_gemms(int wfmt, const GroupedGemm& g, hipStream_t s);
+
+}  // namespace moe

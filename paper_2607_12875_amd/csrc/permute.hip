@@ -1,0 +1,153 @@
+// Permute / align: group the T*k routed rows by expert (the data movement
+// inside the paper's "Fused MoE" node, Fig. 1 / Fig. 3).
+//
+// Flat ids f = t*k + j are cut into chunks of C consecutive ids, one
+// workgroup per chunk.
+//   count pass   per chunk, an LDS-atomic histogram over experts -> counts[c][e]
+//   scatter pass every chunk block rebuilds the global layout it needs:
+//                totals per expert, segment sizes padded to block_m, an
+//                exclusive scan over experts (wave scan + LDS), and the base of
+//                its own chunk inside each segment (counts of earlier chunks).
+//                The stable rank of each id inside its chunk comes from an LDS
+//                bitmap: bit i of row e is set when chunk element i routes to
+//                e; rank = popcount of the bits below i.  No ordering depends
+//                on atomics, so the result is bit-identical on every run.
+// With a single chunk the count pass is skipped and totals come from the
+// bitmap itself.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace moe {
+
+constexpr int kPermThreads = 1024;
+constexpr int kBitmapWords = 8192;  // 32 KiB of LDS: E * C/32 words
+
+int permute_chunk(int E) { return E <= 256 ? 1024 : (E <= 512 ? 512 : 256); }
+
+__global__ __launch_bounds__(kPermThreads) void permute_count_kernel(
+    const int32_t* __restrict__ ids, int n, int E, int C, int32_t* __restrict__ counts) {
+  __shared__ int hist[1024];
+  for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
+  __syncthreads();
+  const int f = blockIdx.x * C + threadIdx.x;
+  if (threadIdx.x < C && f < n) {
+    const int e = ids[f];
+    if (e >= 0 && e < E) atomicAdd(&hist[e], 1);
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < E; e += blockDim.x) counts[blockIdx.x * E + e] = hist[e];
+}
+
+// Inclusive scan of one int per thread across the block (blockDim = 1024).
+__device__ __forceinline__ int block_inclusive_scan(int v, int* wave_tot) {
+  const int lane = lane_id(), wv = threadIdx.x >> 6;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int o = __shfl_up(v, off);
+    if (lane >= off) v += o;
+  }
+  if (lane == 63) wave_tot[wv] = v;
+  __syncthreads();
+  if (wv == 0) {
+    int t = lane < (kPermThreads / 64) ? wave_tot[lane] : 0;
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+      const int o = __shfl_up(t, off);
+      if (lane >= off) t += o;
+    }
+    if (lane < (kPermThreads / 64)) wave_tot[lane] = t;
+  }
+  __syncthreads();
+  if (wv > 0) v += wave_tot[wv - 1];
+  return v;
+}
+
+__global__ __launch_bounds__(kPermThreads) void permute_scatter_kernel(
+    const int32_t* __restrict__ ids, int n, int E, int C, int block_m, int nchunks,
+    const int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
+    int32_t* __restrict__ sorted_ids, int32_t* __restrict__ inv_pos, int cap) {
+  __shared__ uint32_t bitmap[kBitmapWords];
+  __shared__ int base[1024];
+  __shared__ int wave_tot[16];
+  __shared__ int total_padded;
+  const int W = C / 32;  // bitmap words per expert
+  const int tid = threadIdx.x;
+  const int c = blockIdx.x;
+
+  for (int i = tid; i < E * W; i += kPermThreads) bitmap[i] = 0;
+  __syncthreads();
+  const int f = c * C + tid;
+  int my_e = -1;
+  if (tid < C && f < n) {
+    my_e = ids[f];
+    if (my_e >= 0 && my_e < E) atomicOr(&bitmap[my_e * W + (tid >> 5)], 1u << (tid & 31));
+    else my_e = -1;
+  }
+  __syncthreads();
+
+  // per-expert totals and the count of this expert in earlier chunks
+  int tot = 0, pre = 0;
+  if (tid < E) {
+    if (counts == nullptr) {
+      for (int w = 0; w < W; ++w) tot += __popc(bitmap[tid * W + w]);
+    } else {
+      for (int cc = 0; cc < nchunks; ++cc) {
+        const int v = counts[cc * E + tid];
+        tot += v;
+        if (cc < c) pre += v;
+      }
+    }
+  }
+  const int padded = (tot + block_m - 1) / block_m * block_m;
+  const int incl = block_inclusive_scan(tid < E ? padded : 0, wave_tot);
+  const int seg0 = incl - padded;  // exclusive offset of expert tid
+  if (tid < E) base[tid] = seg0 + pre;
+  if (tid == E - 1) total_padded = incl;
+  if (c == 0 && tid < E) {
+    offsets[tid] = seg0;
+    for (int p = seg0 + tot; p < seg0 + padded; ++p) sorted_ids[p] = n;
+    if (tid == E - 1) offsets[E] = incl;
+  }
+  __syncthreads();
+  if (c == 0)  // pads after the last segment, up to the capacity
+    for (int p = total_padded + tid; p < cap; p += kPermThreads) sorted_ids[p] = n;
+
+  if (my_e >= 0) {
+    const uint32_t* row = bitmap + my_e * W;
+    const int wi = tid >> 5;
+    int rank = __popc(row[wi] & ((1u << (tid & 31)) - 1u));
+    for (int w = 0; w < wi; ++w) rank += __popc(row[w]);
+    const int pos = base[my_e] + rank;
+    sorted_ids[pos] = f;
+    inv_pos[f] = pos;
+  } else if (tid < C && f < n) {
+    inv_pos[f] = -1;
+  }
+}
+
+size_t permute_workspace_bytes(int T, int k, int E) {
+  const long n = static_cast<long>(T) * k;
+  const int C = permute_chunk(E);
+  const long nchunks = (n + C - 1) / C;
+  if (nchunks <= 1) return 0;
+  return static_cast<size_t>((nchunks * E * 4 + 255) / 256 * 256);
+}
+
+hipError_t launch_permute(const int32_t* ids, int T, int k, int E, int block_m, int32_t* offsets,
+                          int32_t* sorted_ids, int32_t* inv_pos, int cap, void* ws,
+                          hipStream_t s) {
+  const int n = T * k;
+  const int C = permute_chunk(E);
+  const int nchunks = n == 0 ? 1 : (n + C - 1) / C;
+  int32_t* counts = nullptr;
+  if (nchunks > 1) {
+    counts = static_cast<int32_t*>(ws);
+    hipLaunchKernelGGL(permute_count_kernel, dim3(nchunks), dim3(kPermThreads), 0, s, ids, n, E,
+                       C, counts);
+  }
+  hipLaunchKernelGGL(permute_scatter_kernel, dim3(nchunks), dim3(kPermThreads), 0, s, ids, n, E,
+                     C, block_m, nchunks, counts, offsets, sorted_ids, inv_pos, cap);
+  return hipGetLastError();
+}
+
+}  // namespace moe

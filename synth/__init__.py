@@ -6,5 +6,6 @@ from .moe_inputs import (  # noqa: F401
     tiny_config,
     make_inputs,
     make_routing_inputs,
+    to_device,
     make_expert_weights,
 )

@@ -241,3 +241,20 @@ def make_inputs(cfg: MoeConfig, threads=None, identical_experts=False) -> dict:
     out = make_routing_inputs(cfg, threads)
     out.update(make_expert_weights(cfg, threads=threads, identical_experts=identical_experts))
     return out
+
+
+# ---------------------------------------------------------------- device upload
+def to_device(inputs: dict, device="cuda") -> dict:
+    """Numpy inputs -> torch tensors on ``device`` in the library's dtypes:
+    bf16 bits as torch.bfloat16, fp8 codes as uint8, int4 words as int32,
+    fp32 scales as float32, bf16 scales as torch.bfloat16."""
+    out = {}
+    for k, v in inputs.items():
+        if v is None:
+            out[k] = None
+            continue
+        t = torch.from_numpy(np.ascontiguousarray(v))
+        if v.dtype == np.uint16:
+            t = t.view(torch.int16).view(torch.bfloat16)
+        out[k] = t.to(device)
+    return out

@@ -1,0 +1,106 @@
+"""The C ABI without a GPU: the library loads, exports every function
+include/moe.h declares, and rejects bad arguments on the host before any HIP
+call (the only failures a test can force without a device)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_12875_amd as moe
+from paper_2607_12875_amd import _binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x10000  # a 16-byte aligned non-null address; never dereferenced on these paths
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "moe.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return set(re.findall(r"\b(moe_[a-z0-9_]+)\s*\(", src))
+
+
+def test_every_declared_symbol_is_exported():
+    L = moe.lib()
+    declared = _declared()
+    assert declared == set(B.EXPORTED)
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def test_status_strings():
+    L = moe.lib()
+    for code, name in B.STATUS_NAMES.items():
+        assert L.moe_status_str(code).decode() == name
+    assert L.moe_status_str(99).decode() == "MOE_ERR_UNKNOWN"
+
+
+def _args(**kw):
+    base = dict(T=64, H=256, E=8, I=128, top_k=2)
+    base.update({k: kw.pop(k) for k in list(kw) if k in base})
+    a = B.make_args(**base, **{k: v for k, v in kw.items() if k in ("mode", "wfmt", "out_dtype", "renormalize")})
+    for k in ("hidden", "logits", "w1", "w2", "w1_scale", "w2_scale", "out"):
+        setattr(a, k, kw.get(k, FAKE))
+    return a
+
+
+def _fwd(a, ws=FAKE, nbytes=1 << 40):
+    return moe.lib().moe_forward(ctypes.byref(a), ws, nbytes, None)
+
+
+def test_forward_argument_validation():
+    assert _fwd(_args(top_k=9)) == B.MOE_ERR_SHAPE
+    assert _fwd(_args(top_k=0)) == 2
+    assert _fwd(_args(E=0)) == 2
+    assert _fwd(_args(E=2000, top_k=2)) == 2
+    assert _fwd(_args(H=200)) == 2
+    assert _fwd(_args(I=100)) == 2
+    assert _fwd(_args(T=-1)) == 2
+    assert _fwd(_args(hidden=None)) == 1
+    assert _fwd(_args(out=None)) == 1
+    assert _fwd(_args(wfmt="fp8", w1_scale=None)) == 1
+    assert _fwd(_args(hidden=FAKE + 8)) == 4
+    assert _fwd(_args(), ws=None) == 5
+    a = _args()
+    need = moe.moe_workspace_bytes(a)
+    assert need > 0
+    assert _fwd(a, nbytes=need - 1) == 5
+    a.score_mode = 7
+    assert _fwd(a) == 3
+    a = _args()
+    a.wfmt = 9
+    assert _fwd(a) == 3
+    # T == 0 is a no-op that touches no device memory
+    assert _fwd(_args(T=0, hidden=None, logits=None, w1=None, w2=None, out=None), ws=None, nbytes=0) == 0
+
+
+def test_gate_and_permute_validation():
+    L = moe.lib()
+    assert L.moe_gate_topk(FAKE, None, 4, 8, 9, 0, 1, 1.0, FAKE, FAKE, None) == 2
+    assert L.moe_gate_topk(None, None, 4, 8, 2, 0, 1, 1.0, FAKE, FAKE, None) == 1
+    assert L.moe_gate_topk(FAKE, None, 4, 8, 2, 5, 1, 1.0, FAKE, FAKE, None) == 3
+    assert L.moe_gate_topk(FAKE + 2, None, 4, 8, 2, 0, 1, 1.0, FAKE, FAKE, None) == 4
+    assert L.moe_gate_topk(None, None, 0, 8, 2, 0, 1, 1.0, None, None, None) == 0
+    cap = moe.moe_permute_capacity(10, 2, 8, 16)
+    assert cap == 10 * 2 + 8 * 15
+    assert L.moe_permute(FAKE, 10, 2, 8, 16, FAKE, FAKE, FAKE, cap - 1, None, 0, None) == 2
+    assert L.moe_permute(FAKE, 10, 2, 8, 0, FAKE, FAKE, FAKE, cap, None, 0, None) == 2
+    assert L.moe_permute(FAKE, 10, 2, 8, 16, None, FAKE, FAKE, cap, None, 0, None) == 1
+    big = moe.moe_permute_workspace_bytes(100000, 8, 256)
+    assert big > 0 and moe.moe_permute_workspace_bytes(10, 2, 8) == 0
+    cap = moe.moe_permute_capacity(100000, 8, 256, 1)
+    assert L.moe_permute(FAKE, 100000, 8, 256, 1, FAKE, FAKE, FAKE, cap, None, 0, None) == 5
+    assert L.moe_act_quant_fp8(FAKE, 4, 100, FAKE, FAKE, None) == 2
+    assert L.moe_act_quant_fp8(FAKE + 4, 4, 128, FAKE, FAKE, None) == 4
+
+
+def test_workspace_layout_is_consistent():
+    for wfmt, (T, H, E, I, k) in [("bf16", (16, 4096, 64, 1408, 6)), ("bf16", (4096, 4096, 64, 1408, 6)),
+                                  ("fp8", (8192, 7168, 256, 2048, 8)), ("int4", (512, 4096, 128, 1536, 8))]:
+        a = B.make_args(T, H, E, I, k, wfmt=wfmt)
+        L = moe.moe_workspace_layout(a)
+        assert L["total"] == moe.moe_workspace_bytes(a)
+        assert L["cap"] == T * k + E * (L["block_m"] - 1)
+        offs = sorted(v for n, v in L.items() if n not in ("block_m", "cap", "total") and v >= 0)
+        assert offs[0] == 0 and all(o % 256 == 0 for o in offs) and offs[-1] <= L["total"]
+        assert (L["act_q"] >= 0) == (wfmt == "fp8")

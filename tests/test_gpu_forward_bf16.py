@@ -1,0 +1,81 @@
+"""GPU parity of the whole layer with bf16 experts against the fp64 oracle
+(quantisation points mirrored): bit-exact routing and permutation, and
+max|out - oracle| <= 2e-2 * rms(oracle out)."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import moe_oracle as O
+from tests.gpu_util import TOL, rel_err, require_gpu, run_forward, ws_view
+import torch
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return require_gpu()
+
+
+def _check(cfg, inp=None, out_dtype="f32"):
+    print(f"forward parity {cfg}", flush=True)
+    inp = synth.make_inputs(cfg) if inp is None else inp
+    out, ws, L, _ = run_forward(cfg, inp, out_dtype)
+    ref = O.forward(cfg, inp)
+    n = cfg.T * cfg.top_k
+    ids = ws_view(ws, L, "topk_ids", torch.int32, n).reshape(cfg.T, cfg.top_k)
+    assert np.array_equal(ids, ref["ids"])
+    ro, rs, ri = O.permute(ref["ids"], cfg.E, L["block_m"])
+    assert np.array_equal(ws_view(ws, L, "expert_offsets", torch.int32, cfg.E + 1), ro)
+    assert np.array_equal(ws_view(ws, L, "sorted_ids", torch.int32, L["cap"]), rs)
+    assert np.array_equal(ws_view(ws, L, "inv_pos", torch.int32, n), ri)
+    err = rel_err(out, ref["out"])
+    print(f"  max|err|/rms = {err:.3e} (block_m={L['block_m']})", flush=True)
+    rms = np.sqrt((ref["out"] ** 2).mean())
+    # a bf16 output adds its own rounding: at most 2^-9 of each element
+    slack = 0.0 if out_dtype == "f32" else 2 ** -9 * np.abs(ref["out"]).max() / rms
+    assert err <= TOL[cfg.wfmt] + slack
+    return out, ref
+
+
+def test_tiny_config_full_size(dev):
+    _check(synth.config(1))
+
+
+@pytest.mark.parametrize("T", [1, 7, 77, 300])
+def test_small_shapes_skinny_and_tiled(dev, T):
+    # E=4, k=2: T=300 gives 150 rows per expert (tiled kernels), small T the skinny ones
+    _check(synth.tiny_config(1, T=T, H=384, I=256, E=4, top_k=2))
+
+
+def test_many_experts_ragged(dev):
+    _check(synth.tiny_config(1, T=201, H=512, I=384, E=40, top_k=5))
+
+
+def test_bf16_output_format(dev):
+    _check(synth.tiny_config(1, T=50), out_dtype="bf16")
+
+
+def test_decode_config_full_size(dev):
+    _check(synth.config(2))
+
+
+def test_prefill_config_full_size(dev):
+    _check(synth.config(3))
+
+
+def test_run_twice_bit_identical(dev):
+    cfg = synth.tiny_config(1, T=300, E=4, top_k=2)
+    inp = synth.make_inputs(cfg)
+    a, ws, _, _ = run_forward(cfg, inp)
+    b, _, _, _ = run_forward(cfg, inp, workspace=ws)
+    assert np.array_equal(a, b)
+
+
+def test_token_order_permutes_output(dev):
+    cfg = synth.tiny_config(1, T=120, E=8, top_k=3)
+    inp = synth.make_inputs(cfg)
+    perm = np.random.default_rng(1).permutation(cfg.T)
+    a, _, _, _ = run_forward(cfg, inp)
+    b, _, _, _ = run_forward(cfg, dict(inp, hidden=inp["hidden"][perm], logits=inp["logits"][perm]))
+    assert np.array_equal(b, a[perm])

@@ -1,0 +1,97 @@
+"""GPU parity of the MoE Gate and permute kernels against the oracle:
+bit-exact ids (incl. order), offsets, sorted ids and inverse positions;
+routing weights within 1e-6 relative."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_12875_amd as moe
+import synth
+from oracle import moe_oracle as O
+from tests.gpu_util import require_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return require_gpu()
+
+
+def _gate(dev, logits, bias, k, mode, renorm, scale):
+    lg = torch.from_numpy(np.ascontiguousarray(logits)).to(dev)
+    b = None if bias is None else torch.from_numpy(bias).to(dev)
+    ids, w = moe.moe_gate_topk(lg, k, mode, renorm, scale, sel_bias=b)
+    torch.cuda.synchronize()
+    return ids.cpu().numpy(), w.cpu().numpy()
+
+
+def _check_gate(dev, logits, bias, k, mode="softmax", renorm=True, scale=1.0):
+    ids, w = _gate(dev, logits, bias, k, mode, renorm, scale)
+    rid, rw = O.gate(logits, bias, k, mode, renorm, scale)
+    assert np.array_equal(ids, rid), np.argwhere(ids != rid)[:5]
+    assert np.all(np.abs(w - rw) <= 1e-6 * np.abs(rw))
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 4, 5])
+def test_gate_full_size_configs(dev, n):
+    cfg = synth.config(n)
+    print(f"gate parity cfg{n}", flush=True)
+    r = synth.make_routing_inputs(cfg)
+    _check_gate(dev, r["logits"], r["sel_bias"], cfg.top_k, cfg.mode, cfg.renormalize, cfg.routed_scale)
+
+
+@pytest.mark.parametrize("E,k", [(1, 1), (16, 5), (100, 7), (1024, 32), (257, 8)])
+@pytest.mark.parametrize("mode", ["softmax", "sigmoid"])
+@pytest.mark.parametrize("renorm", [True, False])
+def test_gate_shapes_and_modes(dev, E, k, mode, renorm):
+    rng = np.random.default_rng(E * 31 + k)
+    lg = rng.standard_normal((333, E)).astype(np.float32)
+    b = rng.standard_normal(E).astype(np.float32) * 0.3 if E % 2 else None
+    _check_gate(dev, lg, b, k, mode, renorm, 1.7)
+
+
+def test_gate_integer_ties(dev):
+    lg = np.random.default_rng(3).integers(-2, 3, (1000, 64)).astype(np.float32)
+    _check_gate(dev, lg, None, 6)
+    _check_gate(dev, np.zeros((5, 256), np.float32), np.zeros(256, np.float32), 8, "sigmoid", True, 2.5)
+
+
+def _check_permute(dev, ids, E, block_m):
+    t = torch.from_numpy(np.ascontiguousarray(ids, dtype=np.int32)).to(dev)
+    off, sid, inv = moe.moe_permute(t, E, block_m)
+    torch.cuda.synchronize()
+    ro, rs, ri = O.permute(ids, E, block_m)
+    assert np.array_equal(off.cpu().numpy(), ro)
+    assert np.array_equal(sid.cpu().numpy(), rs)
+    assert np.array_equal(inv.cpu().numpy(), ri)
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("block_m", [1, 16, 128])
+def test_permute_full_size_configs(dev, n, block_m):
+    cfg = synth.config(n)
+    print(f"permute parity cfg{n} block_m={block_m}", flush=True)
+    r = synth.make_routing_inputs(cfg)
+    ids, _ = O.gate(r["logits"], r["sel_bias"], cfg.top_k, cfg.mode)
+    _check_permute(dev, ids, cfg.E, block_m)
+
+
+def test_permute_edge_cases(dev):
+    _check_permute(dev, np.zeros((0, 3), np.int32), 7, 16)                # empty
+    _check_permute(dev, np.full((3000, 1), 5, np.int32), 8, 64)           # one expert takes all
+    _check_permute(dev, np.zeros((1, 1), np.int32), 1, 1)                 # single row
+    rng = np.random.default_rng(9)
+    ids = np.stack([rng.permutation(1000)[:8] for _ in range(700)]).astype(np.int32)
+    _check_permute(dev, ids, 1000, 32)                                    # E=1000, 256-id chunks
+    ids = np.stack([rng.permutation(300)[:4] for _ in range(2000)]).astype(np.int32)
+    _check_permute(dev, ids, 300, 8)                                      # 512-id chunks
+
+
+def test_permute_deterministic(dev):
+    r = synth.make_routing_inputs(synth.config(4))
+    ids, _ = O.gate(r["logits"], r["sel_bias"], 8, "sigmoid")
+    t = torch.from_numpy(ids).to(dev)
+    a = [x.cpu().numpy() for x in moe.moe_permute(t, 256, 128)]
+    b = [x.cpu().numpy() for x in moe.moe_permute(t, 256, 128)]
+    assert all(np.array_equal(x, y) for x, y in zip(a, b))
