@@ -191,6 +191,18 @@ moe_status moe_workspace_layout(const moe_args* a, moe_ws_layout* layout);
  */
 moe_status moe_forward(const moe_args* a, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/*
+ * moe_forward with per-stage timing: the same launches on the same stream,
+ * with events[i] recorded before stage i and events[MOE_NUM_STAGES] after the
+ * last stage.  Stages: 0 gate, 1 permute, 2 fp8 activation quantisation
+ * (empty for bf16 / int4), 3 GEMM1 + SiLU*up, 4 GEMM2, 5 combine.
+ *   events  host array of MOE_NUM_STAGES + 1 caller-created hipEvent_t
+ * Errors: those of moe_forward; MOE_ERR_NULL for a NULL event.
+ */
+#define MOE_NUM_STAGES 6
+moe_status moe_forward_profiled(const moe_args* a, void* ws, size_t ws_bytes,
+                                hipEvent_t* events, hipStream_t stream);
+
 /* Static, NUL-terminated name of a status code. */
 const char* moe_status_str(int status);
 

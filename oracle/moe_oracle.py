@@ -63,16 +63,24 @@ def f32_to_bf16_rne(x: np.ndarray) -> np.ndarray:
     return r.astype(np.uint16)
 
 
-def e4m3_decode(codes: np.ndarray) -> np.ndarray:
-    """OCP fp8 e4m3fn codes -> float64.  Layout S.EEEE.MMM, exponent bias 7,
-    no infinities, S.1111.111 is NaN, E=0 encodes subnormals M * 2^-9."""
-    c = np.asarray(codes).astype(np.int64)
+def _e4m3_value(c: np.ndarray) -> np.ndarray:
+    """Closed form of OCP fp8 e4m3fn: layout S.EEEE.MMM, exponent bias 7, no
+    infinities, S.1111.111 is NaN, E=0 encodes subnormals M * 2^-9."""
+    c = c.astype(np.int64)
     sign = np.where(c & 0x80, -1.0, 1.0)
     e = (c >> 3) & 0xF
     m = c & 0x7
     val = np.where(e == 0, m * 2.0 ** -9, (1.0 + m / 8.0) * np.ldexp(1.0, e - 7))
     val = np.where((e == 15) & (m == 7), np.nan, val)
     return sign * val
+
+
+_E4M3_TABLE = _e4m3_value(np.arange(256))  # the closed form at every code
+
+
+def e4m3_decode(codes: np.ndarray) -> np.ndarray:
+    """OCP fp8 e4m3fn codes -> float64 (the closed form, tabulated per code)."""
+    return _E4M3_TABLE[np.asarray(codes).astype(np.uint8)]
 
 
 def e4m3_encode(x: np.ndarray) -> np.ndarray:
@@ -97,15 +105,23 @@ def e4m3_encode(x: np.ndarray) -> np.ndarray:
     return code.astype(np.uint8)
 
 
+def _nibble_pair(b: np.ndarray) -> np.ndarray:
+    """Byte -> its (low, high) nibbles as two's complement int4 values."""
+    lo, hi = b & 0xF, (b >> 4) & 0xF
+    return np.stack([np.where(lo >= 8, lo - 16, lo), np.where(hi >= 8, hi - 16, hi)], axis=-1)
+
+
+_NIBBLES = _nibble_pair(np.arange(256)).astype(np.int8)  # [256, 2]
+_NIBBLES_LE16 = np.ascontiguousarray(_NIBBLES).view("<i2").reshape(256)  # (lo, hi) packed per byte value
+
+
 def int4_unpack(words: np.ndarray) -> np.ndarray:
     """int32 words [..., K/8] -> signed nibbles int8 [..., K]; element 8w+j is
-    bits [4j, 4j+4) of word w, two's complement."""
-    w = np.asarray(words).view(np.uint32)
-    out = np.empty(w.shape[:-1] + (w.shape[-1] * 8,), dtype=np.int8)
-    for j in range(8):
-        nib = ((w >> np.uint32(4 * j)) & np.uint32(0xF)).astype(np.int8)
-        out[..., j::8] = np.where(nib >= 8, nib - 16, nib)
-    return out
+    bits [4j, 4j+4) of word w, two's complement.  Byte b of a (little-endian)
+    word holds elements 2b (low nibble) and 2b+1 (high nibble)."""
+    w = np.ascontiguousarray(words).astype("<u4", copy=False)
+    by = w.view(np.uint8)                                   # [..., K/2]
+    return _NIBBLES_LE16[by].view(np.int8).reshape(w.shape[:-1] + (w.shape[-1] * 8,))
 
 
 def dequant_weight(wfmt: str, w: np.ndarray, scale) -> np.ndarray:
@@ -113,13 +129,15 @@ def dequant_weight(wfmt: str, w: np.ndarray, scale) -> np.ndarray:
     if wfmt == "bf16":
         return bf16_to_f64(w)
     if wfmt == "fp8":
-        q = e4m3_decode(w)
+        q = e4m3_decode(w)                                  # [N, K]
+        N, K = q.shape
         s = np.asarray(scale, dtype=np.float64)            # [N/128, K/128]
-        return q * np.repeat(np.repeat(s, QGROUP, axis=0), QGROUP, axis=1)
+        return (q.reshape(N // QGROUP, QGROUP, K // QGROUP, QGROUP) * s[:, None, :, None]).reshape(N, K)
     if wfmt == "int4":
         q = int4_unpack(w).astype(np.float64)              # [N, K]
+        N, K = q.shape
         s = bf16_to_f64(scale)                              # [N, K/128]
-        return q * np.repeat(s, QGROUP, axis=1)
+        return (q.reshape(N, K // QGROUP, QGROUP) * s[:, :, None]).reshape(N, K)
     raise ValueError(f"unknown weight format {wfmt!r}")
 
 
@@ -194,7 +212,8 @@ def act_quant_fp8(x32: np.ndarray):
 
 def act_dequant_fp8(codes, scales):
     M, K = codes.shape
-    return e4m3_decode(codes) * np.repeat(np.asarray(scales, np.float64), QGROUP, axis=1)
+    s = np.asarray(scales, np.float64)
+    return (e4m3_decode(codes).reshape(M, K // QGROUP, QGROUP) * s[:, :, None]).reshape(M, K)
 
 
 def _round_intermediate(a: np.ndarray, wfmt: str) -> np.ndarray:

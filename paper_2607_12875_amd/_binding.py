@@ -24,7 +24,9 @@ OFMT = {"f32": 0, "bf16": 1}
 
 EXPORTED = ("moe_status_str", "moe_permute_capacity", "moe_permute_workspace_bytes",
             "moe_gate_topk", "moe_permute", "moe_act_quant_fp8", "moe_workspace_bytes",
-            "moe_workspace_layout", "moe_forward")
+            "moe_workspace_layout", "moe_forward", "moe_forward_profiled")
+NUM_STAGES = 6
+STAGES = ("gate", "permute", "act_quant", "gemm1", "gemm2", "combine")
 
 
 class MoeError(RuntimeError):
@@ -83,6 +85,9 @@ def lib() -> ctypes.CDLL:
         L.moe_workspace_layout.argtypes = [ctypes.POINTER(MoeArgs), ctypes.POINTER(MoeWsLayout)]
         L.moe_forward.restype = i32
         L.moe_forward.argtypes = [ctypes.POINTER(MoeArgs), vp, sz, vp]
+        L.moe_forward_profiled.restype = i32
+        L.moe_forward_profiled.argtypes = [ctypes.POINTER(MoeArgs), vp, sz,
+                                           ctypes.POINTER(ctypes.c_void_p), vp]
         _lib = L
     return _lib
 
@@ -182,6 +187,13 @@ def moe_forward_args(args: MoeArgs, workspace, stream=None):
     """Run the layer on a prepared MoeArgs with a caller-owned uint8 workspace."""
     _check(lib().moe_forward(ctypes.byref(args), _ptr(workspace), workspace.numel(),
                              _stream(stream)), "moe_forward")
+
+
+def moe_forward_profiled(args: MoeArgs, workspace, events, stream=None):
+    """moe_forward with hipEvent_t handles (ints) recorded around each stage."""
+    arr = (ctypes.c_void_p * (NUM_STAGES + 1))(*events)
+    _check(lib().moe_forward_profiled(ctypes.byref(args), _ptr(workspace), workspace.numel(),
+                                      arr, _stream(stream)), "moe_forward_profiled")
 
 
 def moe_forward(hidden, logits, w1, w2, top_k, *, mode="softmax", renormalize=True,

@@ -4,11 +4,14 @@
 namespace moe {
 
 int gemm_block_m_bf16(int T, int top_k, int E);
-hipError_t launch_gemms_bf16(const GroupedGemm& g, hipStream_t s);
+hipError_t launch_gemm1_bf16(const GroupedGemm& g, hipStream_t s);
+hipError_t launch_gemm2_bf16(const GroupedGemm& g, hipStream_t s);
 int gemm_block_m_fp8(int T, int top_k, int E);
-hipError_t launch_gemms_fp8(const GroupedGemm& g, hipStream_t s);
+hipError_t launch_gemm1_fp8(const GroupedGemm& g, hipStream_t s);
+hipError_t launch_gemm2_fp8(const GroupedGemm& g, hipStream_t s);
 int gemm_block_m_int4(int T, int top_k, int E);
-hipError_t launch_gemms_int4(const GroupedGemm& g, hipStream_t s);
+hipError_t launch_gemm1_int4(const GroupedGemm& g, hipStream_t s);
+hipError_t launch_gemm2_int4(const GroupedGemm& g, hipStream_t s);
 
 int gemm_block_m(int wfmt, int T, int top_k, int E) {
   switch (wfmt) {
@@ -18,11 +21,19 @@ int gemm_block_m(int wfmt, int T, int top_k, int E) {
   }
 }
 
-hipError_t launch_expert_gemms(int wfmt, const GroupedGemm& g, hipStream_t s) {
+hipError_t launch_gemm1(int wfmt, const GroupedGemm& g, hipStream_t s) {
   switch (wfmt) {
-    case 1: return launch_gemms_fp8(g, s);
-    case 2: return launch_gemms_int4(g, s);
-    default: return launch_gemms_bf16(g, s);
+    case 1: return launch_gemm1_fp8(g, s);
+    case 2: return launch_gemm1_int4(g, s);
+    default: return launch_gemm1_bf16(g, s);
+  }
+}
+
+hipError_t launch_gemm2(int wfmt, const GroupedGemm& g, hipStream_t s) {
+  switch (wfmt) {
+    case 1: return launch_gemm2_fp8(g, s);
+    case 2: return launch_gemm2_int4(g, s);
+    default: return launch_gemm2_bf16(g, s);
   }
 }
 

@@ -4,11 +4,8 @@
 //   GEMM2  y = a W2[e]^T
 // Weights are [N,K] with K contiguous, so both products read B rows along K.
 //
-// Two kernel families:
-//  * tiled  (rows per expert >> 16): BM x BN output tile per workgroup, BK=64
-//    slices of A and B staged through LDS (double buffered, 16-byte chunks
-//    XOR-swizzled by row so the MFMA fragment reads are bank-conflict free),
-//    v_mfma_f32_32x32x16_bf16 with fp32 accumulation.
+// Two kernel families: the LDS-tiled persistent kernel shared with the other
+// formats (gemm_tiled.hip) when experts hold many rows, and here
 //  * skinny (decode: a few rows per expert): 16-row tile, the K range split
 //    over the four waves, weight fragments streamed from HBM straight into
 //    registers (no reuse to stage for), v_mfma_f32_16x16x32_bf16, partial sums
@@ -19,135 +16,6 @@
 #include "launch.hpp"
 
 namespace moe {
-
-// ----------------------------------------------------------------- tiled
-template <int BM, int BN, int WM, int WN, bool GEMM1>
-__global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_tiled(GroupedGemm g) {
-  constexpr int NT = WM * WN * 64;
-  constexpr int BK = 64;
-  constexpr int NB = GEMM1 ? 2 * BN : BN;   // B tile rows (gate + up for GEMM1)
-  constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
-  constexpr int A_CH = BM * 8 / NT, B_CH = NB * 8 / NT;  // 16-byte chunks per thread
-  static_assert(A_CH * NT == BM * 8 && B_CH * NT == NB * 8, "tile/thread mismatch");
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * BK];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][NB * BK];
-
-  const int m0 = blockIdx.x * BM;
-  if (m0 >= g.offsets[g.E]) return;
-  const int e = find_segment(g.offsets, g.E, m0);
-  const int n0 = blockIdx.y * BN;
-  const int K = GEMM1 ? g.H : g.I;
-  const int tid = threadIdx.x, lane = lane_id(), wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-
-  // global row pointers of this thread's A and B chunks
-  const uint16_t* a_ptr[A_CH];
-  const uint16_t* b_ptr[B_CH];
-  int a_lds[A_CH], b_lds[B_CH];
-#pragma unroll
-  for (int i = 0; i < A_CH; ++i) {
-    const int q = tid + i * NT, r = q >> 3, c = q & 7;
-    const uint16_t* row;
-    if (GEMM1) {
-      const int sid = g.sorted_ids[m0 + r];
-      const int tok = sid < g.n_routed ? sid / g.top_k : 0;
-      row = static_cast<const uint16_t*>(g.x) + static_cast<size_t>(tok) * g.H;
-    } else {
-      row = static_cast<const uint16_t*>(g.inter) + static_cast<size_t>(m0 + r) * g.I;
-    }
-    a_ptr[i] = row + c * 8;
-    a_lds[i] = r * BK + ((c ^ (r & 7)) << 3);
-  }
-  const uint16_t* wbase = static_cast<const uint16_t*>(GEMM1 ? g.w1 : g.w2) +
-                          static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) * K;
-#pragma unroll
-  for (int i = 0; i < B_CH; ++i) {
-    const int q = tid + i * NT, r = q >> 3, c = q & 7;
-    int n;
-    if (GEMM1) n = r < BN ? n0 + r : g.I + n0 + (r - BN);
-    else n = n0 + r;
-    b_ptr[i] = wbase + static_cast<size_t>(n) * K + c * 8;
-    b_lds[i] = r * BK + ((c ^ (r & 7)) << 3);
-  }
-
-  f32x16 acc[TM][TN], acc_u[TM][GEMM1 ? TN : 1];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      acc[i][j] = f32x16{};
-      if (GEMM1) acc_u[i][j] = f32x16{};
-    }
-
-  uint4 ra[A_CH], rb[B_CH];
-  auto load = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < A_CH; ++i) ra[i] = *reinterpret_cast<const uint4*>(a_ptr[i] + k0);
-#pragma unroll
-    for (int i = 0; i < B_CH; ++i) rb[i] = *reinterpret_cast<const uint4*>(b_ptr[i] + k0);
-  };
-  auto store = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < A_CH; ++i) *reinterpret_cast<uint4*>(&As[buf][a_lds[i]]) = ra[i];
-#pragma unroll
-    for (int i = 0; i < B_CH; ++i) *reinterpret_cast<uint4*>(&Bs[buf][b_lds[i]]) = rb[i];
-  };
-
-  const int nk = K / BK;
-  load(0);
-  store(0);
-  __syncthreads();
-  const int l32 = lane & 31, kg = lane >> 5;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) load((kt + 1) * BK);
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      const int ch = 2 * kk + kg;
-      bf16x8 a[TM], b[TN], bu[GEMM1 ? TN : 1];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int r = wm * (BM / WM) + i * 32 + l32;
-        a[i] = as_bf16x8(*reinterpret_cast<const uint4*>(&As[buf][r * BK + ((ch ^ (r & 7)) << 3)]));
-      }
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int r = wn * (BN / WN) + j * 32 + l32;
-        b[j] = as_bf16x8(*reinterpret_cast<const uint4*>(&Bs[buf][r * BK + ((ch ^ (r & 7)) << 3)]));
-        if (GEMM1) {
-          const int ru = BN + r;
-          bu[j] = as_bf16x8(*reinterpret_cast<const uint4*>(&Bs[buf][ru * BK + ((ch ^ (ru & 7)) << 3)]));
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          acc[i][j] = mfma32x32x16(a[i], b[j], acc[i][j]);
-          if (GEMM1) acc_u[i][j] = mfma32x32x16(a[i], bu[j], acc_u[i][j]);
-        }
-    }
-    if (kt + 1 < nk) store(buf ^ 1);
-    __syncthreads();
-  }
-
-  // epilogue: D element v of a 32x32 tile is (row 8*(v/4) + 4*(lane/32) + v%4, col lane%32)
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = m0 + wm * (BM / WM) + i * 32 + 8 * (v >> 2) + 4 * kg + (v & 3);
-        const int col = n0 + wn * (BN / WN) + j * 32 + l32;
-        if (GEMM1) {
-          static_cast<uint16_t*>(g.inter)[static_cast<size_t>(row) * g.I + col] =
-              f32_to_bf16(silu_mul(acc[i][j][v], acc_u[i][j][v]));
-        } else if (g.sorted_ids[row] < g.n_routed) {  // pad rows are never read
-          static_cast<float*>(g.y)[static_cast<size_t>(row) * g.H + col] = acc[i][j][v];
-        }
-      }
-}
 
 // ----------------------------------------------------------------- skinny
 // NSUB 16-column weight subtiles per workgroup (GEMM1: NSUB/2 gate + NSUB/2
@@ -250,19 +118,22 @@ bool bf16_use_skinny(int T, int top_k, int E) {
   return static_cast<long>(T) * top_k <= 32L * E;  // <= 32 rows per expert on average
 }
 
-hipError_t launch_gemms_bf16(const GroupedGemm& g, hipStream_t s) {
+hipError_t launch_gemm1_bf16(const GroupedGemm& g, hipStream_t s) {
   if (bf16_use_skinny(g.T, g.top_k, g.E)) {
-    constexpr int BM = 16;
-    const dim3 grid1(g.max_rows / BM, g.I / 32), grid2(g.max_rows / BM, g.H / 64);
-    hipLaunchKernelGGL((gemm_bf16_skinny<4, 4, true>), grid1, dim3(256), 0, s, g);
-    hipLaunchKernelGGL((gemm_bf16_skinny<4, 4, false>), grid2, dim3(256), 0, s, g);
-  } else {
-    constexpr int BM = 128;
-    const dim3 grid1(g.max_rows / BM, g.I / 64), grid2(g.max_rows / BM, g.H / 128);
-    hipLaunchKernelGGL((gemm_bf16_tiled<BM, 64, 2, 2, true>), grid1, dim3(256), 0, s, g);
-    hipLaunchKernelGGL((gemm_bf16_tiled<BM, 128, 2, 2, false>), grid2, dim3(256), 0, s, g);
+    const dim3 grid(g.max_rows / 16, g.I / 32);
+    hipLaunchKernelGGL((gemm_bf16_skinny<4, 4, true>), grid, dim3(256), 0, s, g);
+    return hipGetLastError();
   }
-  return hipGetLastError();
+  return launch_gemm1_bf16_tiled(g, s);
+}
+
+hipError_t launch_gemm2_bf16(const GroupedGemm& g, hipStream_t s) {
+  if (bf16_use_skinny(g.T, g.top_k, g.E)) {
+    const dim3 grid(g.max_rows / 16, g.H / 64);
+    hipLaunchKernelGGL((gemm_bf16_skinny<4, 4, false>), grid, dim3(256), 0, s, g);
+    return hipGetLastError();
+  }
+  return launch_gemm2_bf16_tiled(g, s);
 }
 
 int gemm_block_m_bf16(int T, int top_k, int E) { return bf16_use_skinny(T, top_k, E) ? 16 : 128; }

@@ -44,10 +44,13 @@ struct GroupedGemm {
 
 // y is kept in fp32 for bf16 weights (their 2e-2 output tolerance has no room
 // for a bf16 rounding of every routed row) and in bf16 for fp8 / int4.
-inline bool y_is_f32(int wfmt) { return wfmt == 0; }
+__host__ __device__ constexpr bool y_is_f32(int wfmt) { return wfmt == 0; }
 
 // Row tile (padding granule) the kernels for this format/shape use.
 int gemm_block_m(int wfmt, int T, int top_k, int E);
-hipError_t launch_expert_gemms(int wfmt, const GroupedGemm& g, hipStream_t s);
+hipError_t launch_gemm1_bf16_tiled(const GroupedGemm& g, hipStream_t s);
+hipError_t launch_gemm2_bf16_tiled(const GroupedGemm& g, hipStream_t s);
+hipError_t launch_gemm1(int wfmt, const GroupedGemm& g, hipStream_t s);  // + SiLU*up epilogue
+hipError_t launch_gemm2(int wfmt, const GroupedGemm& g, hipStream_t s);
 
 }  // namespace moe

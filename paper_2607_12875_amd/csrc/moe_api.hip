@@ -180,13 +180,24 @@ moe_status moe_workspace_layout(const moe_args* a, moe_ws_layout* layout) {
   return MOE_OK;
 }
 
-moe_status moe_forward(const moe_args* a, void* ws, size_t ws_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// The launch sequence.  With `events` non-null, events[i] is recorded on the
+// stream before stage i (gate, permute, activation quantisation, GEMM1, GEMM2,
+// combine) and events[MOE_NUM_STAGES] after the last; the work is the same.
+moe_status run_layer(const moe_args* a, void* ws, size_t ws_bytes, hipEvent_t* events,
+                     hipStream_t stream) {
   moe_status st = check_args(a);
   if (st != MOE_OK) return st;
   if (a->T == 0) return MOE_OK;
   const moe_ws_layout L = make_layout(a);
   if (!ws || ws_bytes < static_cast<size_t>(L.total)) return MOE_ERR_WORKSPACE;
   if (!aligned16(ws)) return MOE_ERR_ALIGN;
+  auto mark = [&](int i) {
+    return events ? hipEventRecord(events[i], stream) == hipSuccess : true;
+  };
 
   int32_t* ids = at<int32_t>(ws, L.topk_ids);
   float* wts = at<float>(ws, L.topk_w);
@@ -194,10 +205,12 @@ moe_status moe_forward(const moe_args* a, void* ws, size_t ws_bytes, hipStream_t
   int32_t* sorted = at<int32_t>(ws, L.sorted_ids);
   int32_t* inv = at<int32_t>(ws, L.inv_pos);
 
+  if (!mark(0)) return MOE_ERR_HIP;
   if (moe::launch_gate_topk(a->logits, a->sel_bias, a->T, a->E, a->top_k, a->score_mode,
                             a->renormalize, a->routed_scale, ids, wts, a->topk_ids_out,
                             a->topk_w_out, stream) != hipSuccess)
     return MOE_ERR_HIP;
+  if (!mark(1)) return MOE_ERR_HIP;
   if (moe::launch_permute(ids, a->T, a->top_k, a->E, L.block_m, offs, sorted, inv, L.cap,
                           at<void>(ws, L.permute_ws), stream) != hipSuccess)
     return MOE_ERR_HIP;
@@ -205,6 +218,7 @@ moe_status moe_forward(const moe_args* a, void* ws, size_t ws_bytes, hipStream_t
   moe::GroupedGemm g;
   g.x = a->hidden;
   g.x_scale = nullptr;
+  if (!mark(2)) return MOE_ERR_HIP;
   if (a->wfmt == MOE_W_FP8E4M3_B128) {
     uint8_t* q = at<uint8_t>(ws, L.act_q);
     float* s = at<float>(ws, L.act_s);
@@ -228,11 +242,32 @@ moe_status moe_forward(const moe_args* a, void* ws, size_t ws_bytes, hipStream_t
   g.inter = at<void>(ws, L.inter);
   g.inter_scale = L.inter_s >= 0 ? at<float>(ws, L.inter_s) : nullptr;
   g.y = at<void>(ws, L.y);
-  if (moe::launch_expert_gemms(a->wfmt, g, stream) != hipSuccess) return MOE_ERR_HIP;
-  if (moe::launch_combine(g.y, moe::y_is_f32(a->wfmt), wts, inv, a->T, a->H, a->top_k, a->ofmt == MOE_OUT_BF16, a->out,
-                          stream) != hipSuccess)
+  if (!mark(3)) return MOE_ERR_HIP;
+  if (moe::launch_gemm1(a->wfmt, g, stream) != hipSuccess) return MOE_ERR_HIP;
+  if (!mark(4)) return MOE_ERR_HIP;
+  if (moe::launch_gemm2(a->wfmt, g, stream) != hipSuccess) return MOE_ERR_HIP;
+  if (!mark(5)) return MOE_ERR_HIP;
+  if (moe::launch_combine(g.y, moe::y_is_f32(a->wfmt), wts, inv, a->T, a->H, a->top_k,
+                          a->ofmt == MOE_OUT_BF16, a->out, stream) != hipSuccess)
     return MOE_ERR_HIP;
+  if (!mark(6)) return MOE_ERR_HIP;
   return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+moe_status moe_forward(const moe_args* a, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return run_layer(a, ws, ws_bytes, nullptr, stream);
+}
+
+moe_status moe_forward_profiled(const moe_args* a, void* ws, size_t ws_bytes,
+                                hipEvent_t* events, hipStream_t stream) {
+  if (!events) return MOE_ERR_NULL;
+  for (int i = 0; i <= MOE_NUM_STAGES; ++i)
+    if (!events[i]) return MOE_ERR_NULL;
+  return run_layer(a, ws, ws_bytes, events, stream);
 }
 
 }  // extern "C"
