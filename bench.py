@@ -128,6 +128,38 @@ def cpu_baseline(cfg, inputs, budget_s: float):
             "sample": sample, "seconds_per_layer_sample": dt}
 
 
+def gemm1_kernel_match(name: str) -> bool:
+    """True for the GEMM1 (+SiLU*up) kernel of any format / variant."""
+    return ("gemm_bf16_skinny<" in name and "true>" in name) or \
+           ("moe_gemm_tiled<" in name and ", true," in name)
+
+
+def traffic_summary(fetch_csv, write_csv, calib_fetch_csv, calib_write_csv, calib_mib):
+    """HBM bytes per GEMM1 launch from rocprofv3 FETCH_SIZE / WRITE_SIZE
+    counter CSVs (KiB per dispatch), each scaled by what the same counter
+    reads for a plain device copy of calib_mib MiB."""
+    import csv
+
+    def per_kernel(path, match):
+        vals = [float(r["Counter_Value"]) for r in csv.DictReader(open(path)) if match(r["Kernel_Name"])]
+        return sum(vals) / len(vals), len(vals)
+
+    copy = lambda n: "copyBuffer" in n  # noqa: E731
+    nbytes = calib_mib * 1024 * 1024
+    f_copy, _ = per_kernel(calib_fetch_csv, copy)
+    w_copy, _ = per_kernel(calib_write_csv, copy)
+    f_g1, n1 = per_kernel(fetch_csv, gemm1_kernel_match)
+    w_g1, n2 = per_kernel(write_csv, gemm1_kernel_match)
+    f_scale, w_scale = nbytes / (f_copy * 1024), nbytes / (w_copy * 1024)
+    fetch, write = f_g1 * 1024 * f_scale, w_g1 * 1024 * w_scale
+    return {"kernel": "gemm1 (+SiLU*up)", "fetch_size_kib_raw": f_g1, "write_size_kib_raw": w_g1,
+            "dispatches": [n1, n2], "copy_calibration_mib": calib_mib,
+            "copy_fetch_kib_raw": f_copy, "copy_write_kib_raw": w_copy,
+            "fetch_scale": f_scale, "write_scale": w_scale,
+            "hbm_fetch_bytes_per_launch": fetch, "hbm_write_bytes_per_launch": write,
+            "hbm_bytes_per_launch": fetch + write, "kernel_source_hash": kernel_source_hash()}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -136,7 +168,16 @@ def main():
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="host-time budget of the oracle baseline (0 disables it)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB five times (the reference "
+                         "kernel that scales HBM counter readings), then exit")
+    ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
+                    help="host only: print the GEMM1 HBM-traffic record from rocprofv3 counter CSVs "
+                         "(the copy ones from --copy-calibration 1024) and exit")
     args = ap.parse_args()
+    if args.traffic_summary:
+        print(json.dumps(traffic_summary(*args.traffic_summary, 1024), indent=1))
+        return
     if args.gpus != 1:
         print("bench.py: this build runs the MoE layer on one GPU only; multi-GPU "
               "sharding is a design note, not implemented (use --gpus 1).", file=sys.stderr)
@@ -149,6 +190,15 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 5}))
+        return
     moe.lib()
     cfg = synth.config(args.config)
     t0 = time.perf_counter()

@@ -59,7 +59,7 @@ __device__ __forceinline__ bf16x8 dequant_int4x8(uint32_t w, float s) {
 }
 
 template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM>
-__global__ __launch_bounds__(256, 1) void moe_gemm_tiled(GroupedGemm g) {
+__global__ __launch_bounds__(256) void moe_gemm_tiled(GroupedGemm g) {
   static_assert(WM * WN == 4, "four waves");
   constexpr int KE = FmtTraits<FMT>::KE;  // K elements per step
   constexpr int KB = 128;                 // A bytes per row per step
@@ -382,10 +382,15 @@ int cu_count() {
   return n;
 }
 
-// Persistent grid: one workgroup per CU (multiple of the XCD count), never
-// more than the largest possible number of tiles.
-dim3 persistent_grid(long max_tiles) {
-  long n = cu_count();
+// Persistent grid: as many workgroups as fit on the device at once (a
+// multiple of the XCD count), never more than the largest possible number of
+// tiles.
+template <class Kernel>
+dim3 persistent_grid(Kernel k, long max_tiles) {
+  int per_cu = 1;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, 256, 0) != hipSuccess || per_cu < 1)
+    per_cu = 1;
+  long n = static_cast<long>(cu_count()) * per_cu;
   n = (n + kXcds - 1) / kXcds * kXcds;
   const long cap = (max_tiles + kXcds - 1) / kXcds * kXcds;
   return dim3(static_cast<unsigned>(std::max<long>(kXcds, std::min(n, cap))));
@@ -395,8 +400,8 @@ template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM>
 hipError_t launch_tiled(const GroupedGemm& g, hipStream_t s) {
   constexpr int NC = GEMM1 ? BNW / 2 : BNW;
   const long mt = g.max_rows / BM, nt = (GEMM1 ? g.I : g.H) / NC;
-  hipLaunchKernelGGL((moe_gemm_tiled<FMT, GEMM1, BM, BNW, WM, WN, GM>), persistent_grid(mt * nt),
-                     dim3(256), 0, s, g);
+  auto kern = moe_gemm_tiled<FMT, GEMM1, BM, BNW, WM, WN, GM>;
+  hipLaunchKernelGGL(kern, persistent_grid(kern, mt * nt), dim3(256), 0, s, g);
   return hipGetLastError();
 }
 

@@ -42,9 +42,11 @@ struct GroupedGemm {
   void* y;                    // [cap, H]: fp32 for bf16 weights, bf16 otherwise
 };
 
-// y is kept in fp32 for bf16 weights (their 2e-2 output tolerance has no room
-// for a bf16 rounding of every routed row) and in bf16 for fp8 / int4.
-__host__ __device__ constexpr bool y_is_f32(int wfmt) { return wfmt == 0; }
+// y is kept in fp32 for bf16 and int4 weights (a bf16 rounding of every
+// routed row would take most of the bf16 2e-2 output tolerance) and in bf16
+// for fp8, whose 1.9 GB fp32 round trip at 8192 tokens would cost more than
+// the whole error budget it buys back.
+__host__ __device__ constexpr bool y_is_f32(int wfmt) { return wfmt != 1; }
 
 // Row tile (padding granule) the kernels for this format/shape use.
 int gemm_block_m(int wfmt, int T, int top_k, int E);
