@@ -7,7 +7,7 @@
 // Two kernel families: the LDS-tiled persistent kernel shared with the other
 // formats (gemm_tiled.hip) when experts hold many rows, and here
 //  * skinny (decode: a few rows per expert): 16-row tile, the K range split
-//    over the four waves, weight fragments streamed from HBM straight into
+//    over the four waves on 128-byte line boundaries, weight fragments streamed from HBM straight into
 //    registers (no reuse to stage for), v_mfma_f32_16x16x32_bf16, partial sums
 //    reduced through LDS.
 // Segments are padded to the row tile, so every tile belongs to one expert;
@@ -26,10 +26,13 @@ __global__ __launch_bounds__(256) void gemm_bf16_skinny(GroupedGemm g) {
   constexpr int BN = GEMM1 ? NSUB / 2 * 16 : NSUB * 16;  // output columns
   __shared__ f32x4 red[3][NSUB][64];
 
-  const int m0 = blockIdx.x * BM;
+  // column tiles vary fastest in dispatch order: the workgroups of one row
+  // tile (one expert) run together, and the empty row tiles past the last
+  // segment come last
+  const int m0 = blockIdx.y * BM;
   if (m0 >= g.offsets[g.E]) return;
   const int e = find_segment(g.offsets, g.E, m0);
-  const int n0 = blockIdx.y * BN;
+  const int n0 = blockIdx.x * BN;
   const int K = GEMM1 ? g.H : g.I;
   const int lane = lane_id(), wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kg = lane >> 4;
@@ -56,28 +59,47 @@ __global__ __launch_bounds__(256) void gemm_bf16_skinny(GroupedGemm g) {
   f32x4 acc[NSUB];
 #pragma unroll
   for (int s = 0; s < NSUB; ++s) acc[s] = f32x4{};
-  const int kper = K / 4;
-  const int kbeg = wave * kper, kend = kbeg + kper;
+  // K split over the four waves on 64-element (128-byte line) boundaries, so
+  // no cache line is fetched by two waves: wave w takes nl/4 lines, plus one
+  // of the nl%4 remainder lines for the first waves.
+  const int nl = K / 64, lb = nl / 4, lr = nl % 4;
+  const int kbeg = 64 * (wave * lb + min(wave, lr));
+  const int kend = kbeg + 64 * (lb + (wave < lr ? 1 : 0));
+  // Main loop, software pipelined: UNROLL k-steps of 32 form one stage; the
+  // loads of stage i+1 are issued before the MFMAs of stage i, so every lane
+  // keeps NSUB*UNROLL weight loads in flight while it computes.
+  const int nst = (kend - kbeg) / (32 * UNROLL);
   int k = kbeg + kg * 8;
-  // main loop: UNROLL k-steps of 32 per iteration, all loads issued first
-  for (; k + (UNROLL - 1) * 32 < kend; k += UNROLL * 32) {
-    uint4 av[UNROLL], bv[UNROLL][NSUB];
-#pragma unroll
-    for (int u = 0; u < UNROLL; ++u) {
-#pragma unroll
-      for (int s = 0; s < NSUB; ++s) bv[u][s] = *reinterpret_cast<const uint4*>(brow[s] + k + u * 32);
-      av[u] = *reinterpret_cast<const uint4*>(arow + k + u * 32);
-    }
-#pragma unroll
-    for (int u = 0; u < UNROLL; ++u)
-#pragma unroll
-      for (int s = 0; s < NSUB; ++s) acc[s] = mfma16x16x32(as_bf16x8(av[u]), as_bf16x8(bv[u][s]), acc[s]);
+  u32x4 a0[UNROLL], b0[UNROLL][NSUB], a1[UNROLL], b1[UNROLL][NSUB];
+#define MOE_SKINNY_LOAD(A, Bv, k_)                                                           \
+  do {                                                                                       \
+    _Pragma("unroll") for (int u = 0; u < UNROLL; ++u) {                                     \
+      _Pragma("unroll") for (int s = 0; s < NSUB; ++s) Bv[u][s] = ld16(brow[s] + (k_) + u * 32); \
+      A[u] = ld16(arow + (k_) + u * 32);                                                     \
+    }                                                                                        \
+  } while (0)
+#define MOE_SKINNY_MMA(A, Bv)                                                                \
+  do {                                                                                       \
+    _Pragma("unroll") for (int u = 0; u < UNROLL; ++u)                                       \
+        _Pragma("unroll") for (int s = 0; s < NSUB; ++s)                                     \
+            acc[s] = mfma16x16x32(as_bf16x8(A[u]), as_bf16x8(Bv[u][s]), acc[s]);             \
+  } while (0)
+  if (nst > 0) MOE_SKINNY_LOAD(a0, b0, k);
+  for (int i = 0; i < nst; i += 2) {
+    if (i + 1 < nst) MOE_SKINNY_LOAD(a1, b1, k + 32 * UNROLL);
+    MOE_SKINNY_MMA(a0, b0);
+    if (i + 2 < nst) MOE_SKINNY_LOAD(a0, b0, k + 64 * UNROLL);
+    if (i + 1 < nst) MOE_SKINNY_MMA(a1, b1);
+    k += 64 * UNROLL;
   }
+#undef MOE_SKINNY_LOAD
+#undef MOE_SKINNY_MMA
+  k = kbeg + kg * 8 + nst * 32 * UNROLL;
   for (; k < kend; k += 32) {
-    const uint4 av = *reinterpret_cast<const uint4*>(arow + k);
+    const u32x4 av = ld16(arow + k);
 #pragma unroll
     for (int s = 0; s < NSUB; ++s)
-      acc[s] = mfma16x16x32(as_bf16x8(av), as_bf16x8(*reinterpret_cast<const uint4*>(brow[s] + k)), acc[s]);
+      acc[s] = mfma16x16x32(as_bf16x8(av), as_bf16x8(ld16(brow[s] + k)), acc[s]);
   }
 
   if (wave > 0) {
@@ -118,10 +140,26 @@ bool bf16_use_skinny(int T, int top_k, int E) {
   return static_cast<long>(T) * top_k <= 32L * E;  // <= 32 rows per expert on average
 }
 
+// Decode tile knobs: weight subtiles of 16 rows per workgroup and k-steps of
+// 32 loaded ahead per lane (NSUB * UNROLL 16-byte loads in flight per lane).
+#ifndef MOE_SKINNY1_NSUB
+#define MOE_SKINNY1_NSUB 4
+#endif
+#ifndef MOE_SKINNY1_UNROLL
+#define MOE_SKINNY1_UNROLL 2
+#endif
+#ifndef MOE_SKINNY2_NSUB
+#define MOE_SKINNY2_NSUB 4
+#endif
+#ifndef MOE_SKINNY2_UNROLL
+#define MOE_SKINNY2_UNROLL 2
+#endif
+
 hipError_t launch_gemm1_bf16(const GroupedGemm& g, hipStream_t s) {
   if (bf16_use_skinny(g.T, g.top_k, g.E)) {
-    const dim3 grid(g.max_rows / 16, g.I / 32);
-    hipLaunchKernelGGL((gemm_bf16_skinny<4, 4, true>), grid, dim3(256), 0, s, g);
+    constexpr int NS = MOE_SKINNY1_NSUB;
+    const dim3 grid(g.I / (NS / 2 * 16), g.max_rows / 16);
+    hipLaunchKernelGGL((gemm_bf16_skinny<NS, MOE_SKINNY1_UNROLL, true>), grid, dim3(256), 0, s, g);
     return hipGetLastError();
   }
   return launch_gemm1_bf16_tiled(g, s);
@@ -129,8 +167,9 @@ hipError_t launch_gemm1_bf16(const GroupedGemm& g, hipStream_t s) {
 
 hipError_t launch_gemm2_bf16(const GroupedGemm& g, hipStream_t s) {
   if (bf16_use_skinny(g.T, g.top_k, g.E)) {
-    const dim3 grid(g.max_rows / 16, g.H / 64);
-    hipLaunchKernelGGL((gemm_bf16_skinny<4, 4, false>), grid, dim3(256), 0, s, g);
+    constexpr int NS = MOE_SKINNY2_NSUB;
+    const dim3 grid(g.H / (NS * 16), g.max_rows / 16);
+    hipLaunchKernelGGL((gemm_bf16_skinny<NS, MOE_SKINNY2_UNROLL, false>), grid, dim3(256), 0, s, g);
     return hipGetLastError();
   }
   return launch_gemm2_bf16_tiled(g, s);
