@@ -175,6 +175,8 @@ hipError_t launch_gemm2_bf16(const GroupedGemm& g, hipStream_t s) {
   return launch_gemm2_bf16_tiled(g, s);
 }
 
-int gemm_block_m_bf16(int T, int top_k, int E) { return bf16_use_skinny(T, top_k, E) ? 16 : 128; }
+int gemm_block_m_bf16(int T, int top_k, int E) {
+  return bf16_use_skinny(T, top_k, E) ? 16 : bf16_tiled_block_m();
+}
 
 }  // namespace moe

@@ -19,9 +19,9 @@
 //
 // Scheduling is persistent and XCD-aware: the launch has a few workgroups per
 // CU; workgroups that land on one XCD (block ids congruent mod 8) own one
-// contiguous range of logical tiles, ordered in groups of GM row tiles x all
-// column tiles, so the row tiles (gathered hidden rows) and weight slabs a
-// group shares are served from that XCD's L2.  The number of real row tiles
+// contiguous range of logical tiles, ordered expert by expert in chunks of at
+// most GM row tiles x all column tiles, so the weight slab and row tiles that
+// concurrently running workgroups share are read from HBM about once.  The number of real row tiles
 // is read on the device from expert_offsets[E] (segments are padded to BM).
 #include <algorithm>
 
@@ -31,6 +31,7 @@
 namespace moe {
 
 constexpr int kXcds = 8;
+constexpr int MOE_MAX_EXPERTS_DEV = 1024;  // the ABI's expert limit
 
 template <int FMT>
 struct FmtTraits;
@@ -58,24 +59,71 @@ __device__ __forceinline__ bf16x8 dequant_int4x8(uint32_t w, float s) {
   return r;
 }
 
+// Direct global -> LDS copy of one 16-byte (or 4-byte) element per lane: lane
+// l of the wave lands at LDS byte `lds + 16*l` (`lds + 4*l`).  Issued as
+// inline asm so the compiler does not treat every later LDS read as
+// dependent on it; completion is awaited explicitly with vm_wait<N>().
+// `lds` must be uniform across the wave.
+__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
+               "v"(gptr) : "memory", "m0");
+}
+__device__ __forceinline__ void dma4(const void* gptr, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
+               "v"(gptr) : "memory", "m0");
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p)));
+}
+// s_waitcnt with only the vector-memory count: at most N loads outstanding.
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt(((N >> 4) & 3) << 14 | (0xF << 8) | (7 << 4) | (N & 0xF));
+}
+// Workgroup barrier without a memory fence (the fence of __syncthreads would
+// also drain the loads still in flight for later stages).
+__device__ __forceinline__ void bar() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// XOR swizzle of the 16-byte chunks of a 128-byte LDS row: row r stores its
+// chunk c in slot c ^ swz(r).  For the fragment reads (32 consecutive rows,
+// lanes l and l+32 on neighbouring chunks of one row) (r >> 1) & 7 measured
+// 1.6x the LDS read throughput of r & 7 on gfx950.
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
+
 template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM>
-__global__ __launch_bounds__(256) void moe_gemm_tiled(GroupedGemm g) {
-  static_assert(WM * WN == 4, "four waves");
+__global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
+  constexpr int NW = WM * WN, NT = NW * 64;
+  static_assert(NW == 4 || NW == 8, "four or eight waves");
   constexpr int KE = FmtTraits<FMT>::KE;  // K elements per step
   constexpr int KB = 128;                 // A bytes per row per step
   constexpr int BB = FmtTraits<FMT>::BB;  // B bytes per row per step
   constexpr int WTM = BM / WM, WTN = BNW / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
   constexpr int NC = GEMM1 ? BNW / 2 : BNW;  // output columns per tile
-  constexpr int A_CH = BM * KB / 16 / 256, B_CH = BNW * BB / 16 / 256;
-  static_assert(A_CH >= 1 && B_CH >= 1 && A_CH * 4096 == BM * KB && B_CH * 4096 == BNW * BB, "");
+  // 16-byte DMA instructions per wave per stage (each moves 1 KB)
+  constexpr int A_CH = BM * KB / 1024 / NW, B_CH = BNW * BB / 1024 / NW;
+  static_assert(A_CH >= 1 && B_CH >= 1 && A_CH * NW * 1024 == BM * KB && B_CH * NW * 1024 == BNW * BB, "");
   static_assert(!GEMM1 || TN % 2 == 0, "gate/up pairs");
   static_assert(FMT != 1 || !GEMM1 || NC == 128, "fp8 requant needs one 128-column group per tile");
+  // per-stage scale block: one 4-byte DMA instruction per wave (64 floats),
+  // fp8: waves [0, BM/64) the row scales of A, wave BM/64 the block scales of
+  // B; int4: waves [0, BNW/64) the bf16 pair holding each B row's group scale
+  constexpr int SC = FMT == 0 ? 0 : 1;
+  static_assert(FMT != 1 || (NW == 4 && BM / 64 < NW), "fp8 scale DMA layout");
+  static_assert(FMT != 2 || (NW == 4 && BNW / 64 <= NW), "int4 scale DMA layout");
+  constexpr int STAGES = 3;
+  constexpr int A_BYTES = BM * KB, B_BYTES = BNW * BB, S_BYTES = SC * NW * 256;
+  constexpr int STAGE = A_BYTES + B_BYTES + S_BYTES;
+  constexpr int N_DMA = A_CH + B_CH + SC;  // loads per wave per stage
 
-  __shared__ __attribute__((aligned(16))) uint8_t lds_a[2][BM * KB];
-  __shared__ __attribute__((aligned(16))) uint8_t lds_b[2][BNW * BB];
-  __shared__ __attribute__((aligned(16))) float lds_sa[FMT == 1 ? 2 : 1][FMT == 1 ? BM : 1];
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES][STAGE];
   __shared__ float lds_amax[FMT == 1 && GEMM1 ? WN : 1][FMT == 1 && GEMM1 ? BM : 1];
+  __shared__ int lds_off[MOE_MAX_EXPERTS_DEV + 1];  // expert_offsets, read once per workgroup
 
   const int tid = threadIdx.x, lane = lane_id(), wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -84,7 +132,9 @@ __global__ __launch_bounds__(256) void moe_gemm_tiled(GroupedGemm g) {
   const int N = GEMM1 ? g.I : g.H;       // output columns of the product
   const int nk = K / KE;
   const int n_tiles_n = N / NC;
-  const int n_tiles_m = g.offsets[g.E] / BM;
+  for (int i = tid; i <= g.E; i += NT) lds_off[i] = g.offsets[i];
+  __syncthreads();
+  const int n_tiles_m = lds_off[g.E] / BM;
   const int total = n_tiles_m * n_tiles_n;
 
   // this workgroup's share of the logical tiles: a contiguous range per XCD
@@ -92,20 +142,31 @@ __global__ __launch_bounds__(256) void moe_gemm_tiled(GroupedGemm g) {
   const int per_xcd = gridDim.x / kXcds;
   const int chunk = (total + kXcds - 1) / kXcds;
   const int t_end = min(total, (xcd + 1) * chunk);
+  const uint32_t smem0 = lds_addr(&smem[0][0]);
 
   for (int t = xcd * chunk + slot; t < t_end; t += per_xcd) {
-    const int grp = t / (GM * n_tiles_n), in = t % (GM * n_tiles_n);
-    const int m_first = grp * GM, gm = min(GM, n_tiles_m - m_first);
-    const int mt = m_first + in % gm, nt = in / gm;
+    // Logical tile order: expert by expert; inside expert e (row tiles
+    // [base, base+cnt)) chunks of at most GM row tiles, each chunk swept
+    // column tile by column tile with its row tiles adjacent.  Workgroups
+    // running together then share one expert's weight slab and a few row tiles.
+    const int e = find_segment(lds_off, g.E, (t / n_tiles_n) * BM);
+    const int base = lds_off[e] / BM, cnt = (lds_off[e + 1] - lds_off[e]) / BM;
+    const int local = t - base * n_tiles_n;
+    const int c = local / (GM * n_tiles_n), within = local % (GM * n_tiles_n);
+    const int sz = min(GM, cnt - c * GM);
+    const int mt = base + c * GM + within % sz, nt = within / sz;
     const int m0 = mt * BM, n0 = nt * NC;
-    const int e = find_segment(g.offsets, g.E, m0);
+    __syncthreads();  // the previous tile's last stages are no longer read
 
-    // ---- global source rows of this thread's chunks
+    // ---- per-lane DMA sources.  Instruction i of wave w fills the 1 KB block
+    // (i*NW + w) of a stage: 8 rows of A / of fp8-bf16 B (lane -> row l/8,
+    // 16-byte slot l%8) or 32 rows of int4 B (row l/2, slot l%2).  Slot s of
+    // row r holds the row's chunk s ^ swz(r), the XOR swizzle the fragment
+    // reads undo.
     const uint8_t* a_src[A_CH];
-    int a_dst[A_CH];
 #pragma unroll
     for (int i = 0; i < A_CH; ++i) {
-      const int q = tid + i * 256, r = q >> 3, c = q & 7;
+      const int r = (i * NW + wave) * 8 + (lane >> 3);
       const uint8_t* row;
       if (GEMM1) {
         const int sid = g.sorted_ids[m0 + r];
@@ -114,35 +175,76 @@ __global__ __launch_bounds__(256) void moe_gemm_tiled(GroupedGemm g) {
       } else {
         row = static_cast<const uint8_t*>(g.inter) + static_cast<size_t>(m0 + r) * g.I * (FMT == 1 ? 1 : 2);
       }
-      a_src[i] = row + c * 16;
-      a_dst[i] = r * KB + ((c ^ (r & 7)) << 4);
+      a_src[i] = row + (((lane & 7) ^ swz(r)) << 4);
     }
     const size_t w_row_bytes = FMT == 0 ? K * 2 : (FMT == 1 ? K : K / 2);
     const uint8_t* wbase = static_cast<const uint8_t*>(GEMM1 ? g.w1 : g.w2) +
                            static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) * w_row_bytes;
     const uint8_t* b_src[B_CH];
-    int b_dst[B_CH];
 #pragma unroll
     for (int i = 0; i < B_CH; ++i) {
-      const int q = tid + i * 256;
-      const int r = FMT == 2 ? q >> 1 : q >> 3, c = FMT == 2 ? q & 1 : q & 7;
+      const int blk = i * NW + wave;
+      const int r = FMT == 2 ? blk * 32 + (lane >> 1) : blk * 8 + (lane >> 3);
+      const int sl = FMT == 2 ? (lane & 1) ^ ((r >> 2) & 1) : (lane & 7) ^ swz(r);
       int n;
       if (GEMM1) n = r < NC ? n0 + r : g.I + n0 + (r - NC);
       else n = n0 + r;
-      b_src[i] = wbase + static_cast<size_t>(n) * w_row_bytes + c * 16;
-      b_dst[i] = FMT == 2 ? r * BB + ((c ^ ((r >> 2) & 1)) << 4) : r * BB + ((c ^ (r & 7)) << 4);
+      b_src[i] = wbase + static_cast<size_t>(n) * w_row_bytes + (sl << 4);
     }
-    // fp8 activation scales: thread r < BM owns row r's per-K-block scale
-    const float* sa_src = nullptr;
-    if (FMT == 1 && tid < BM) {
-      if (GEMM1) {
-        const int sid = g.sorted_ids[m0 + tid];
-        const int tok = sid < g.n_routed ? sid / g.top_k : 0;
-        sa_src = g.x_scale + static_cast<size_t>(tok) * (g.H / 128);
-      } else {
-        sa_src = g.inter_scale + static_cast<size_t>(m0 + tid) * (g.I / 128);
+    // scale DMA source of this lane (advanced by one K block / half group per step)
+    const uint8_t* s_src = a_src[0];  // waves without a scale role load a harmless dummy
+    int s_step = 0;
+    if constexpr (FMT == 1) {
+      if (wave < BM / 64) {
+        const int r = wave * 64 + lane;
+        if (GEMM1) {
+          const int sid = g.sorted_ids[m0 + r];
+          const int tok = sid < g.n_routed ? sid / g.top_k : 0;
+          s_src = reinterpret_cast<const uint8_t*>(g.x_scale + static_cast<size_t>(tok) * (g.H / 128));
+        } else {
+          s_src = reinterpret_cast<const uint8_t*>(g.inter_scale + static_cast<size_t>(m0 + r) * (g.I / 128));
+        }
+        s_step = 4;
+      } else if (wave == BM / 64) {
+        // lane l: block row of W (GEMM1: l odd -> up half, even -> gate half;
+        // GEMM2: block row n0/128 + l % (BNW/128))
+        const float* wsc = static_cast<const float*>(GEMM1 ? g.w1_scale : g.w2_scale) +
+                           static_cast<size_t>(e) * ((GEMM1 ? 2 * g.I : g.H) / 128) * (K / 128);
+        const int br = GEMM1 ? ((lane & 1) ? (g.I + n0) / 128 : n0 / 128) : n0 / 128 + lane % (BNW / 128);
+        s_src = reinterpret_cast<const uint8_t*>(wsc + static_cast<size_t>(br) * (K / 128));
+        s_step = 4;
+      }
+    } else if constexpr (FMT == 2) {
+      if (wave < BNW / 64) {
+        const int r = wave * 64 + lane;
+        const int n = GEMM1 ? (r < NC ? n0 + r : g.I + n0 + (r - NC)) : n0 + r;
+        // bf16 scale [n][group] of K step kt sits at element n*(K/128) + kt/2;
+        // the dword holding it starts at the even element below
+        s_src = reinterpret_cast<const uint8_t*>(static_cast<const uint16_t*>(GEMM1 ? g.w1_scale : g.w2_scale) +
+                                                 (static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) + n) * (K / 128));
+        s_step = 1;  // advanced per step in elements below
       }
     }
+
+    // issue stage kt (all DMA of this wave for one K step) into buffer kt % 3
+    auto issue = [&](int kt) {
+      const uint32_t base = smem0 + (kt % STAGES) * STAGE;
+#pragma unroll
+      for (int i = 0; i < A_CH; ++i) dma16(a_src[i] + kt * KB, base + (i * NW + wave) * 1024);
+#pragma unroll
+      for (int i = 0; i < B_CH; ++i) dma16(b_src[i] + kt * BB, base + A_BYTES + (i * NW + wave) * 1024);
+      if constexpr (FMT == 1) {
+        dma4(s_src + kt * s_step, base + A_BYTES + B_BYTES + wave * 256);
+      } else if constexpr (FMT == 2) {
+        // element offset kt/2 within the row, rounded down to an even element (4-byte aligned)
+        const uint8_t* p = s_src;
+        if (s_step) {
+          const uintptr_t a = reinterpret_cast<uintptr_t>(s_src) + (kt >> 1) * 2;
+          p = reinterpret_cast<const uint8_t*>(a & ~static_cast<uintptr_t>(3));
+        }
+        dma4(p, base + A_BYTES + B_BYTES + wave * 256);
+      }
+    };
 
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -150,102 +252,87 @@ __global__ __launch_bounds__(256) void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
       for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
 
-    u32x4 ra[A_CH], rb[B_CH];
-    float rsa = 0.f;
-#define MOE_TILE_LOAD(kt_)                                                                    \
-  do {                                                                                        \
-    _Pragma("unroll") for (int i = 0; i < A_CH; ++i) ra[i] =                                  \
-        ld16(a_src[i] + (kt_) * KB);                               \
-    _Pragma("unroll") for (int i = 0; i < B_CH; ++i) rb[i] =                                  \
-        ld16(b_src[i] + (kt_) * BB);                               \
-    if constexpr (FMT == 1) {                                                                 \
-      if (sa_src) rsa = sa_src[kt_];                                                          \
-    }                                                                                         \
-  } while (0)
-#define MOE_TILE_STORE(buf_)                                                                  \
-  do {                                                                                        \
-    _Pragma("unroll") for (int i = 0; i < A_CH; ++i)                                          \
-        st16(&lds_a[buf_][a_dst[i]], ra[i]);                            \
-    _Pragma("unroll") for (int i = 0; i < B_CH; ++i)                                          \
-        st16(&lds_b[buf_][b_dst[i]], rb[i]);                            \
-    if constexpr (FMT == 1) {                                                                 \
-      if (tid < BM) lds_sa[buf_][tid] = rsa;                                                  \
-    }                                                                                         \
-  } while (0)
-
     // B row (within the tile) of wave tile j
 #define brow(j) (GEMM1 ? ((j) < TN / 2 ? wn * (WTN / 2) + (j) * 32 : NC + wn * (WTN / 2) + ((j) - TN / 2) * 32) \
                        : wn * WTN + (j) * 32)
 
-    MOE_TILE_LOAD(0);
-    MOE_TILE_STORE(0);
-    __syncthreads();
+    issue(0);
+    if (nk > 1) issue(1);
     for (int kt = 0; kt < nk; ++kt) {
-      const int buf = kt & 1;
-      if (kt + 1 < nk) MOE_TILE_LOAD(kt + 1);
-      const uint8_t* As = lds_a[buf];
-      const uint8_t* Bs = lds_b[buf];
+      // stage kt has landed (only stage kt+1 may still be in flight) in every wave
+      if (kt + 1 < nk) vm_wait<N_DMA>(); else vm_wait<0>();
+      bar();
+      if (kt + 2 < nk) issue(kt + 2);  // into the buffer read in step kt-1
+      const uint8_t* As = &smem[kt % STAGES][0];
+      const uint8_t* Bs = As + A_BYTES;
+      const uint8_t* Ss = Bs + B_BYTES;
       if constexpr (FMT == 0) {
+        // every fragment of the K step is requested before the first MFMA
+        bf16x8 af[4][TM], bfr[4][TN];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
           const int ch = 2 * kk + kg;
-          bf16x8 a[TM], b[TN];
 #pragma unroll
           for (int i = 0; i < TM; ++i) {
             const int r = wm * WTM + i * 32 + l32;
-            a[i] = as_bf16x8(ld16(As + r * KB + ((ch ^ (r & 7)) << 4)));
+            af[kk][i] = as_bf16x8(ld16(As + r * KB + ((ch ^ swz(r)) << 4)));
           }
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
             const int r = brow(j) + l32;
-            b[j] = as_bf16x8(ld16(Bs + r * BB + ((ch ^ (r & 7)) << 4)));
+            bfr[kk][j] = as_bf16x8(ld16(Bs + r * BB + ((ch ^ swz(r)) << 4)));
           }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
           for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(a[i], b[j], acc[i][j]);
-        }
+            for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(af[kk][i], bfr[kk][j], acc[i][j]);
       } else if constexpr (FMT == 1) {
         f32x16 part[TM][TN];
+        i32x8 af[2][TM], bfr[2][TN];
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
           const int c0 = 4 * kk + 2 * kg;
-          i32x8 a[TM], b[TN];
 #pragma unroll
           for (int i = 0; i < TM; ++i) {
             const int r = wm * WTM + i * 32 + l32;
-            const u32x4 lo = ld16(As + r * KB + ((c0 ^ (r & 7)) << 4));
-            const u32x4 hi = ld16(As + r * KB + (((c0 + 1) ^ (r & 7)) << 4));
-            a[i] = i32x8{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+            const u32x4 lo = ld16(As + r * KB + ((c0 ^ swz(r)) << 4));
+            const u32x4 hi = ld16(As + r * KB + (((c0 + 1) ^ swz(r)) << 4));
+            af[kk][i] = i32x8{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
           }
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
             const int r = brow(j) + l32;
-            const u32x4 lo = ld16(Bs + r * BB + ((c0 ^ (r & 7)) << 4));
-            const u32x4 hi = ld16(Bs + r * BB + (((c0 + 1) ^ (r & 7)) << 4));
-            b[j] = i32x8{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+            const u32x4 lo = ld16(Bs + r * BB + ((c0 ^ swz(r)) << 4));
+            const u32x4 hi = ld16(Bs + r * BB + (((c0 + 1) ^ swz(r)) << 4));
+            bfr[kk][j] = i32x8{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
           }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
           for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int j = 0; j < TN; ++j)
-              part[i][j] = mfma32x32x64_fp8(a[i], b[j], kk == 0 ? f32x16{} : part[i][j]);
-        }
-        // acc += part * s_row * s_block(B) for this K block
-        const float* wsc = static_cast<const float*>(GEMM1 ? g.w1_scale : g.w2_scale) +
-                           static_cast<size_t>(e) * ((GEMM1 ? 2 * g.I : g.H) / 128) * (K / 128);
+              part[i][j] = mfma32x32x64_fp8(af[kk][i], bfr[kk][j], kk == 0 ? f32x16{} : part[i][j]);
+        // acc += part * s_row(A) * s_block(B) for this K block
+        const float* sA = reinterpret_cast<const float*>(Ss);                 // [BM]
+        const float* sB = reinterpret_cast<const float*>(Ss + (BM / 64) * 256);  // [64]
         float sb[TN];
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
           const int r = brow(j);
-          const int n_glob = GEMM1 ? (r < NC ? n0 + r : g.I + n0 + (r - NC)) : n0 + r;
-          sb[j] = wsc[static_cast<size_t>(n_glob / 128) * (K / 128) + kt];
+          sb[j] = GEMM1 ? sB[r < NC ? 0 : 1] : sB[(r / 128) % (BNW / 128)];
         }
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
 #pragma unroll
           for (int v4 = 0; v4 < 4; ++v4) {
-            const float4 sr = *reinterpret_cast<const float4*>(&lds_sa[buf][wm * WTM + i * 32 + 8 * v4 + 4 * kg]);
+            const float4 sr = *reinterpret_cast<const float4*>(&sA[wm * WTM + i * 32 + 8 * v4 + 4 * kg]);
             const float s4[4] = {sr.x, sr.y, sr.z, sr.w};
 #pragma unroll
             for (int j = 0; j < TN; ++j)
@@ -256,8 +343,7 @@ __global__ __launch_bounds__(256) void moe_gemm_tiled(GroupedGemm g) {
         }
       } else {  // int4
         // this lane's B words for the four 16-wide K substeps, and its scales
-        const uint16_t* wsc = static_cast<const uint16_t*>(GEMM1 ? g.w1_scale : g.w2_scale) +
-                              static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) * (K / 128);
+        const uint32_t* sW = reinterpret_cast<const uint32_t*>(Ss);  // one dword per tile row
         u32x4 bw[TN];
         float sb[TN];
 #pragma unroll
@@ -265,7 +351,9 @@ __global__ __launch_bounds__(256) void moe_gemm_tiled(GroupedGemm g) {
           const int r = brow(j) + l32;
           bw[j] = ld16(Bs + r * BB + ((kg ^ ((r >> 2) & 1)) << 4));
           const int n_glob = GEMM1 ? (r < NC ? n0 + r : g.I + n0 + (r - NC)) : n0 + r;
-          sb[j] = bf16_to_f32(wsc[static_cast<size_t>(n_glob) * (K / 128) + (kt * KE) / 128]);
+          const int idx = (e * (GEMM1 ? 2 * g.I : g.H) + n_glob) * (K / 128) + (kt >> 1);
+          const uint32_t d = sW[r];
+          sb[j] = __uint_as_float((idx & 1) ? (d & 0xFFFF0000u) : (d << 16));
         }
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
@@ -275,7 +363,7 @@ __global__ __launch_bounds__(256) void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
           for (int i = 0; i < TM; ++i) {
             const int r = wm * WTM + i * 32 + l32;
-            a[i] = as_bf16x8(ld16(As + r * KB + ((ch ^ (r & 7)) << 4)));
+            a[i] = as_bf16x8(ld16(As + r * KB + ((ch ^ swz(r)) << 4)));
           }
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
@@ -288,11 +376,7 @@ __global__ __launch_bounds__(256) void moe_gemm_tiled(GroupedGemm g) {
             for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(a[i], b[j], acc[i][j]);
         }
       }
-      if (kt + 1 < nk) MOE_TILE_STORE(buf ^ 1);
-      __syncthreads();
     }
-#undef MOE_TILE_LOAD
-#undef MOE_TILE_STORE
 #undef brow
 
     // ---- epilogue.  D element v of a 32x32 tile: row 8*(v/4) + 4*kg + v%4, column l32.
@@ -386,9 +470,9 @@ int cu_count() {
 // multiple of the XCD count), never more than the largest possible number of
 // tiles.
 template <class Kernel>
-dim3 persistent_grid(Kernel k, long max_tiles) {
+dim3 persistent_grid(Kernel k, int threads, long max_tiles) {
   int per_cu = 1;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, 256, 0) != hipSuccess || per_cu < 1)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, threads, 0) != hipSuccess || per_cu < 1)
     per_cu = 1;
   long n = static_cast<long>(cu_count()) * per_cu;
   n = (n + kXcds - 1) / kXcds * kXcds;
@@ -399,38 +483,61 @@ dim3 persistent_grid(Kernel k, long max_tiles) {
 template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM>
 hipError_t launch_tiled(const GroupedGemm& g, hipStream_t s) {
   constexpr int NC = GEMM1 ? BNW / 2 : BNW;
+  constexpr int NT = WM * WN * 64;
   const long mt = g.max_rows / BM, nt = (GEMM1 ? g.I : g.H) / NC;
   auto kern = moe_gemm_tiled<FMT, GEMM1, BM, BNW, WM, WN, GM>;
-  hipLaunchKernelGGL(kern, persistent_grid(kern, mt * nt), dim3(256), 0, s, g);
+  hipLaunchKernelGGL(kern, persistent_grid(kern, NT, mt * nt), dim3(NT), 0, s, g);
   return hipGetLastError();
 }
 
 }  // namespace
 
+// bf16 tile shapes: rows x weight rows per workgroup, waves as WM x WN.
+#ifndef MOE_T1_BNW
+#define MOE_T1_BNW 256
+#define MOE_T1_WM 2
+#define MOE_T1_WN 2
+#endif
+#ifndef MOE_T2_BNW
+#define MOE_T2_BNW 256
+#define MOE_T2_WM 2
+#define MOE_T2_WN 2
+#endif
+#ifndef MOE_TBF_BM
+#define MOE_TBF_BM 128
+#endif
+// most row tiles of one expert swept together per column tile
+#ifndef MOE_TGM
+#define MOE_TGM 8
+#endif
+#ifndef MOE_TGM_INT4
+#define MOE_TGM_INT4 16
+#endif
+int bf16_tiled_block_m() { return MOE_TBF_BM; }
 hipError_t launch_gemm1_bf16_tiled(const GroupedGemm& g, hipStream_t s) {
-  return launch_tiled<0, true, 128, 256, 2, 2, 4>(g, s);
+  return launch_tiled<0, true, MOE_TBF_BM, MOE_T1_BNW, MOE_T1_WM, MOE_T1_WN, MOE_TGM>(g, s);
 }
 hipError_t launch_gemm2_bf16_tiled(const GroupedGemm& g, hipStream_t s) {
-  if (g.H % 256) return launch_tiled<0, false, 128, 128, 2, 2, 4>(g, s);
-  return launch_tiled<0, false, 128, 256, 2, 2, 4>(g, s);
+  if (g.H % MOE_T2_BNW) return launch_tiled<0, false, MOE_TBF_BM, 128, MOE_T2_WM, MOE_T2_WN, MOE_TGM>(g, s);
+  return launch_tiled<0, false, MOE_TBF_BM, MOE_T2_BNW, MOE_T2_WM, MOE_T2_WN, MOE_TGM>(g, s);
 }
 
 int gemm_block_m_fp8(int, int, int) { return 128; }
 hipError_t launch_gemm1_fp8(const GroupedGemm& g, hipStream_t s) {
-  return launch_tiled<1, true, 128, 256, 2, 2, 4>(g, s);
+  return launch_tiled<1, true, 128, 256, 2, 2, MOE_TGM>(g, s);
 }
 hipError_t launch_gemm2_fp8(const GroupedGemm& g, hipStream_t s) {
-  if (g.H % 256) return launch_tiled<1, false, 128, 128, 2, 2, 4>(g, s);
-  return launch_tiled<1, false, 128, 256, 2, 2, 4>(g, s);
+  if (g.H % 256) return launch_tiled<1, false, 128, 128, 2, 2, MOE_TGM>(g, s);
+  return launch_tiled<1, false, 128, 256, 2, 2, MOE_TGM>(g, s);
 }
 
 int gemm_block_m_int4(int, int, int) { return 64; }
 hipError_t launch_gemm1_int4(const GroupedGemm& g, hipStream_t s) {
-  return launch_tiled<2, true, 64, 256, 1, 4, 4>(g, s);
+  return launch_tiled<2, true, 64, 256, 1, 4, MOE_TGM_INT4>(g, s);
 }
 hipError_t launch_gemm2_int4(const GroupedGemm& g, hipStream_t s) {
-  if (g.H % 256) return launch_tiled<2, false, 64, 128, 1, 4, 4>(g, s);
-  return launch_tiled<2, false, 64, 256, 1, 4, 4>(g, s);
+  if (g.H % 256) return launch_tiled<2, false, 64, 128, 1, 4, MOE_TGM_INT4>(g, s);
+  return launch_tiled<2, false, 64, 256, 1, 4, MOE_TGM_INT4>(g, s);
 }
 
 }  // namespace moe

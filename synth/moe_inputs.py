@@ -15,10 +15,12 @@ as Sec. 6.2 and the "FP8 representation" row of Table 3 require.
 Value recipe (the five workloads):
   * hidden  ~ N(0, 1) drawn in fp32, stored as bf16 (round-to-nearest-even).
   * logits  ~ N(0, 1) fp32, plus an optional per-expert bias:
-      - "normal:<var>"  b_e ~ N(0, var), added to the logits (uneven loads);
+      - "normal:<std>"  b_e ~ N(0, std^2), added to the logits (uneven loads);
       - "zipf:<s>"      b_e = -s * ln(rank_e), rank_e a seeded permutation
                         of 1..E, so exp(b_e) follows a Zipf(s) law (skew).
-  * sel_bias (sigmoid scoring only) ~ N(0, var): used for selection only.
+  * sel_bias (sigmoid scoring only) ~ N(0, std^2): used for selection only.
+  (Weight spreads are variances, N(0, 1/fan_in) = LeCun init; the bias
+  spreads are standard deviations.)
   * W1[E, 2I, H], W2[E, H, I] ~ N(0, 1/fan_in) in fp32 (fan_in = H for W1,
     I for W2), then stored as
       - bf16:  round-to-nearest-even bf16 bits (uint16);
@@ -63,8 +65,8 @@ class MoeConfig:
     mode: str = "softmax"       # "softmax" | "sigmoid"
     renormalize: bool = True
     routed_scale: float = 1.0
-    logit_bias: str = "none"    # "none" | "normal:<var>" | "zipf:<s>"
-    sel_bias_var: float = 0.0   # sigmoid selection-bias variance (0 = no bias)
+    logit_bias: str = "none"    # "none" | "normal:<std>" | "zipf:<s>"
+    sel_bias_std: float = 0.0   # sigmoid selection-bias standard deviation (0 = no bias)
     seed: int = 0
 
     @property
@@ -82,7 +84,7 @@ CONFIGS = {
     3: MoeConfig("prefill", T=4096, H=4096, E=64, I=1408, top_k=6,
                  logit_bias="normal:0.5", seed=3),
     4: MoeConfig("fp8", T=8192, H=7168, E=256, I=2048, top_k=8, wfmt="fp8",
-                 mode="sigmoid", routed_scale=2.5, sel_bias_var=0.1, seed=4),
+                 mode="sigmoid", routed_scale=2.5, sel_bias_std=0.1, seed=4),
     5: MoeConfig("int4", T=512, H=4096, E=128, I=1536, top_k=8, wfmt="int4",
                  logit_bias="zipf:1.1", seed=5),
 }
@@ -146,7 +148,7 @@ def make_routing_inputs(cfg: MoeConfig, threads=None) -> dict:
     logits = _rng(cfg.seed, TID_LOGITS).standard_normal((T, E), dtype=np.float32)
     kind, _, arg = cfg.logit_bias.partition(":")
     if kind == "normal":
-        std = np.float32(np.sqrt(float(arg)))
+        std = np.float32(float(arg))
         b = _rng(cfg.seed, TID_LOGIT_BIAS).standard_normal(E, dtype=np.float32) * std
         logits = (logits + b[None, :]).astype(np.float32)
     elif kind == "zipf":
@@ -158,8 +160,8 @@ def make_routing_inputs(cfg: MoeConfig, threads=None) -> dict:
         raise ValueError(f"unknown logit bias {cfg.logit_bias!r}")
 
     sel_bias = None
-    if cfg.sel_bias_var > 0:
-        std = np.float32(np.sqrt(cfg.sel_bias_var))
+    if cfg.sel_bias_std > 0:
+        std = np.float32(cfg.sel_bias_std)
         sel_bias = (_rng(cfg.seed, TID_SEL_BIAS).standard_normal(E, dtype=np.float32) * std).astype(np.float32)
     return {"hidden": hidden, "logits": np.ascontiguousarray(logits), "sel_bias": sel_bias}
 

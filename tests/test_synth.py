@@ -53,4 +53,4 @@ def test_skewed_routing_bias():
     assert b.max() > -0.5 and b.min() < -1.1 * np.log(128) + 0.5
     cfg3 = synth.config(3)
     assert synth.make_routing_inputs(cfg3)["logits"].shape == (cfg3.T, cfg3.E)
-    assert S.CONFIGS[4].sel_bias_var == 0.1
+    assert S.CONFIGS[4].sel_bias_std == 0.1
