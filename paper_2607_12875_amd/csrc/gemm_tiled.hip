@@ -90,18 +90,22 @@ __device__ __forceinline__ void bar() {
 }
 
 // XOR swizzle of the 16-byte chunks of a 128-byte LDS row: row r stores its
-// chunk c in slot c ^ swz(r).  For the fragment reads (32 consecutive rows,
+// chunk c in slot c ^ swz<KB>(r).  For the fragment reads (32 consecutive rows,
 // lanes l and l+32 on neighbouring chunks of one row) (r >> 1) & 7 measured
 // 1.6x the LDS read throughput of r & 7 on gfx950.
-__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
+// With 64-byte rows (4 chunks) the analogous choice is (r >> 2) & 3.
+template <int KB>
+__device__ __forceinline__ int swz(int r) { return KB == 128 ? (r >> 1) & 7 : (r >> 2) & 3; }
 
-template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM>
+template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM, int KBT = 128, int STAGES = 3>
 __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
   constexpr int NW = WM * WN, NT = NW * 64;
   static_assert(NW == 4 || NW == 8, "four or eight waves");
-  constexpr int KE = FmtTraits<FMT>::KE;  // K elements per step
-  constexpr int KB = 128;                 // A bytes per row per step
-  constexpr int BB = FmtTraits<FMT>::BB;  // B bytes per row per step
+  static_assert(KBT == 128 || (KBT == 64 && FMT == 0), "64-byte steps are bf16 only");
+  constexpr int KB = KBT;                                       // A bytes per row per step
+  constexpr int KE = FMT == 0 ? KB / 2 : FmtTraits<FMT>::KE;   // K elements per step
+  constexpr int BB = FMT == 0 ? KB : FmtTraits<FMT>::BB;       // B bytes per row per step
+  constexpr int RPI = 1024 / KB, LPR = KB / 16;  // rows per DMA instruction, lanes per row
   constexpr int WTM = BM / WM, WTN = BNW / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
   constexpr int NC = GEMM1 ? BNW / 2 : BNW;  // output columns per tile
@@ -116,7 +120,7 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
   constexpr int SC = FMT == 0 ? 0 : 1;
   static_assert(FMT != 1 || (NW == 4 && BM / 64 < NW), "fp8 scale DMA layout");
   static_assert(FMT != 2 || (NW == 4 && BNW / 64 <= NW), "int4 scale DMA layout");
-  constexpr int STAGES = 3;
+  static_assert(STAGES >= 2 && (STAGES - 2) * (A_CH + B_CH + (FMT == 0 ? 0 : 1)) < 64, "vmcnt range");
   constexpr int A_BYTES = BM * KB, B_BYTES = BNW * BB, S_BYTES = SC * NW * 256;
   constexpr int STAGE = A_BYTES + B_BYTES + S_BYTES;
   constexpr int N_DMA = A_CH + B_CH + SC;  // loads per wave per stage
@@ -161,12 +165,12 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
     // ---- per-lane DMA sources.  Instruction i of wave w fills the 1 KB block
     // (i*NW + w) of a stage: 8 rows of A / of fp8-bf16 B (lane -> row l/8,
     // 16-byte slot l%8) or 32 rows of int4 B (row l/2, slot l%2).  Slot s of
-    // row r holds the row's chunk s ^ swz(r), the XOR swizzle the fragment
+    // row r holds the row's chunk s ^ swz<KB>(r), the XOR swizzle the fragment
     // reads undo.
     const uint8_t* a_src[A_CH];
 #pragma unroll
     for (int i = 0; i < A_CH; ++i) {
-      const int r = (i * NW + wave) * 8 + (lane >> 3);
+      const int r = (i * NW + wave) * RPI + lane / LPR;
       const uint8_t* row;
       if (GEMM1) {
         const int sid = g.sorted_ids[m0 + r];
@@ -175,7 +179,7 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
       } else {
         row = static_cast<const uint8_t*>(g.inter) + static_cast<size_t>(m0 + r) * g.I * (FMT == 1 ? 1 : 2);
       }
-      a_src[i] = row + (((lane & 7) ^ swz(r)) << 4);
+      a_src[i] = row + (((lane % LPR) ^ swz<KB>(r)) << 4);
     }
     const size_t w_row_bytes = FMT == 0 ? K * 2 : (FMT == 1 ? K : K / 2);
     const uint8_t* wbase = static_cast<const uint8_t*>(GEMM1 ? g.w1 : g.w2) +
@@ -184,8 +188,8 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
     for (int i = 0; i < B_CH; ++i) {
       const int blk = i * NW + wave;
-      const int r = FMT == 2 ? blk * 32 + (lane >> 1) : blk * 8 + (lane >> 3);
-      const int sl = FMT == 2 ? (lane & 1) ^ ((r >> 2) & 1) : (lane & 7) ^ swz(r);
+      const int r = FMT == 2 ? blk * 32 + (lane >> 1) : blk * RPI + lane / LPR;
+      const int sl = FMT == 2 ? (lane & 1) ^ ((r >> 2) & 1) : (lane % LPR) ^ swz<KB>(r);
       int n;
       if (GEMM1) n = r < NC ? n0 + r : g.I + n0 + (r - NC);
       else n = n0 + r;
@@ -226,13 +230,17 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
       }
     }
 
-    // issue stage kt (all DMA of this wave for one K step) into buffer kt % 3
-    auto issue = [&](int kt) {
+    // issue stage kt (DMA q in [q0, q1) of this wave's A_CH + B_CH tile
+    // loads for one K step, plus the scale load with q1 == N_DMA) into buffer kt % STAGES
+    auto issue_part = [&](int kt, int q0, int q1) {
       const uint32_t base = smem0 + (kt % STAGES) * STAGE;
 #pragma unroll
-      for (int i = 0; i < A_CH; ++i) dma16(a_src[i] + kt * KB, base + (i * NW + wave) * 1024);
+      for (int i = 0; i < A_CH; ++i)
+        if (i >= q0 && i < q1) dma16(a_src[i] + kt * KB, base + (i * NW + wave) * 1024);
 #pragma unroll
-      for (int i = 0; i < B_CH; ++i) dma16(b_src[i] + kt * BB, base + A_BYTES + (i * NW + wave) * 1024);
+      for (int i = 0; i < B_CH; ++i)
+        if (A_CH + i >= q0 && A_CH + i < q1) dma16(b_src[i] + kt * BB, base + A_BYTES + (i * NW + wave) * 1024);
+      if (q1 < N_DMA) return;
       if constexpr (FMT == 1) {
         dma4(s_src + kt * s_step, base + A_BYTES + B_BYTES + wave * 256);
       } else if constexpr (FMT == 2) {
@@ -245,6 +253,7 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
         dma4(p, base + A_BYTES + B_BYTES + wave * 256);
       }
     };
+    auto issue = [&](int kt) { issue_part(kt, 0, N_DMA); };
 
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -256,40 +265,58 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
 #define brow(j) (GEMM1 ? ((j) < TN / 2 ? wn * (WTN / 2) + (j) * 32 : NC + wn * (WTN / 2) + ((j) - TN / 2) * 32) \
                        : wn * WTN + (j) * 32)
 
-    issue(0);
-    if (nk > 1) issue(1);
+    // STAGES-1 steps are loaded ahead; step kt+STAGES-1 goes into the buffer
+    // read in step kt-1, once the barrier shows every wave is past it
+#pragma unroll
+    for (int q = 0; q < STAGES - 1; ++q)
+      if (q < nk) issue(q);
     for (int kt = 0; kt < nk; ++kt) {
-      // stage kt has landed (only stage kt+1 may still be in flight) in every wave
-      if (kt + 1 < nk) vm_wait<N_DMA>(); else vm_wait<0>();
+      // stage kt has landed in every wave; the later stages may still fly
+      const int ahead = min(STAGES - 2, nk - 1 - kt);  // stages issued after kt
+      if constexpr (STAGES >= 6) { if (ahead >= 4) { vm_wait<4 * N_DMA>(); goto landed; } }
+      if constexpr (STAGES >= 5) { if (ahead == 3) { vm_wait<3 * N_DMA>(); goto landed; } }
+      if constexpr (STAGES >= 4) { if (ahead == 2) { vm_wait<2 * N_DMA>(); goto landed; } }
+      if constexpr (STAGES >= 3) { if (ahead == 1) { vm_wait<N_DMA>(); goto landed; } }
+      vm_wait<0>();
+    landed:
       bar();
-      if (kt + 2 < nk) issue(kt + 2);  // into the buffer read in step kt-1
+      const bool pre = kt + STAGES - 1 < nk;  // a later stage to start loading
+      if (FMT != 0 && pre) issue(kt + STAGES - 1);
       const uint8_t* As = &smem[kt % STAGES][0];
       const uint8_t* Bs = As + A_BYTES;
       const uint8_t* Ss = Bs + B_BYTES;
       if constexpr (FMT == 0) {
         // every fragment of the K step is requested before the first MFMA
-        bf16x8 af[4][TM], bfr[4][TN];
+        constexpr int NKK = KE / 16;  // MFMA K substeps per step
+        bf16x8 af[NKK][TM], bfr[NKK][TN];
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
+        for (int kk = 0; kk < NKK; ++kk) {
           const int ch = 2 * kk + kg;
 #pragma unroll
           for (int i = 0; i < TM; ++i) {
             const int r = wm * WTM + i * 32 + l32;
-            af[kk][i] = as_bf16x8(ld16(As + r * KB + ((ch ^ swz(r)) << 4)));
+            af[kk][i] = as_bf16x8(ld16(As + r * KB + ((ch ^ swz<KB>(r)) << 4)));
           }
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
             const int r = brow(j) + l32;
-            bfr[kk][j] = as_bf16x8(ld16(Bs + r * BB + ((ch ^ swz(r)) << 4)));
+            bfr[kk][j] = as_bf16x8(ld16(Bs + r * BB + ((ch ^ swz<KB>(r)) << 4)));
           }
         }
         __builtin_amdgcn_sched_barrier(0);
+        // the next stage's loads are issued between the MFMA groups, so the
+        // matrix pipe keeps running while the address unit takes them
+        constexpr int PER = (A_CH + B_CH + NKK - 1) / NKK;
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
+        for (int kk = 0; kk < NKK; ++kk) {
 #pragma unroll
           for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(af[kk][i], bfr[kk][j], acc[i][j]);
+          __builtin_amdgcn_sched_barrier(0);
+          if (pre) issue_part(kt + STAGES - 1, kk * PER, min((kk + 1) * PER, A_CH + B_CH));
+          __builtin_amdgcn_sched_barrier(0);
+        }
       } else if constexpr (FMT == 1) {
         f32x16 part[TM][TN];
         i32x8 af[2][TM], bfr[2][TN];
@@ -299,15 +326,15 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
           for (int i = 0; i < TM; ++i) {
             const int r = wm * WTM + i * 32 + l32;
-            const u32x4 lo = ld16(As + r * KB + ((c0 ^ swz(r)) << 4));
-            const u32x4 hi = ld16(As + r * KB + (((c0 + 1) ^ swz(r)) << 4));
+            const u32x4 lo = ld16(As + r * KB + ((c0 ^ swz<KB>(r)) << 4));
+            const u32x4 hi = ld16(As + r * KB + (((c0 + 1) ^ swz<KB>(r)) << 4));
             af[kk][i] = i32x8{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
           }
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
             const int r = brow(j) + l32;
-            const u32x4 lo = ld16(Bs + r * BB + ((c0 ^ swz(r)) << 4));
-            const u32x4 hi = ld16(Bs + r * BB + (((c0 + 1) ^ swz(r)) << 4));
+            const u32x4 lo = ld16(Bs + r * BB + ((c0 ^ swz<KB>(r)) << 4));
+            const u32x4 hi = ld16(Bs + r * BB + (((c0 + 1) ^ swz<KB>(r)) << 4));
             bfr[kk][j] = i32x8{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
           }
         }
@@ -363,7 +390,7 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
           for (int i = 0; i < TM; ++i) {
             const int r = wm * WTM + i * 32 + l32;
-            a[i] = as_bf16x8(ld16(As + r * KB + ((ch ^ swz(r)) << 4)));
+            a[i] = as_bf16x8(ld16(As + r * KB + ((ch ^ swz<KB>(r)) << 4)));
           }
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
@@ -480,12 +507,12 @@ dim3 persistent_grid(Kernel k, int threads, long max_tiles) {
   return dim3(static_cast<unsigned>(std::max<long>(kXcds, std::min(n, cap))));
 }
 
-template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM>
+template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM, int KBT = 128, int STAGES = 3>
 hipError_t launch_tiled(const GroupedGemm& g, hipStream_t s) {
   constexpr int NC = GEMM1 ? BNW / 2 : BNW;
   constexpr int NT = WM * WN * 64;
   const long mt = g.max_rows / BM, nt = (GEMM1 ? g.I : g.H) / NC;
-  auto kern = moe_gemm_tiled<FMT, GEMM1, BM, BNW, WM, WN, GM>;
+  auto kern = moe_gemm_tiled<FMT, GEMM1, BM, BNW, WM, WN, GM, KBT, STAGES>;
   hipLaunchKernelGGL(kern, persistent_grid(kern, NT, mt * nt), dim3(NT), 0, s, g);
   return hipGetLastError();
 }
@@ -506,6 +533,12 @@ hipError_t launch_tiled(const GroupedGemm& g, hipStream_t s) {
 #ifndef MOE_TBF_BM
 #define MOE_TBF_BM 128
 #endif
+#ifndef MOE_TBF_KB
+#define MOE_TBF_KB 128
+#endif
+#ifndef MOE_TBF_STAGES
+#define MOE_TBF_STAGES 3
+#endif
 // most row tiles of one expert swept together per column tile
 #ifndef MOE_TGM
 #define MOE_TGM 8
@@ -515,11 +548,11 @@ hipError_t launch_tiled(const GroupedGemm& g, hipStream_t s) {
 #endif
 int bf16_tiled_block_m() { return MOE_TBF_BM; }
 hipError_t launch_gemm1_bf16_tiled(const GroupedGemm& g, hipStream_t s) {
-  return launch_tiled<0, true, MOE_TBF_BM, MOE_T1_BNW, MOE_T1_WM, MOE_T1_WN, MOE_TGM>(g, s);
+  return launch_tiled<0, true, MOE_TBF_BM, MOE_T1_BNW, MOE_T1_WM, MOE_T1_WN, MOE_TGM, MOE_TBF_KB, MOE_TBF_STAGES>(g, s);
 }
 hipError_t launch_gemm2_bf16_tiled(const GroupedGemm& g, hipStream_t s) {
-  if (g.H % MOE_T2_BNW) return launch_tiled<0, false, MOE_TBF_BM, 128, MOE_T2_WM, MOE_T2_WN, MOE_TGM>(g, s);
-  return launch_tiled<0, false, MOE_TBF_BM, MOE_T2_BNW, MOE_T2_WM, MOE_T2_WN, MOE_TGM>(g, s);
+  if (g.H % MOE_T2_BNW) return launch_tiled<0, false, MOE_TBF_BM, 128, MOE_T2_WM, MOE_T2_WN, MOE_TGM, MOE_TBF_KB, MOE_TBF_STAGES>(g, s);
+  return launch_tiled<0, false, MOE_TBF_BM, MOE_T2_BNW, MOE_T2_WM, MOE_T2_WN, MOE_TGM, MOE_TBF_KB, MOE_TBF_STAGES>(g, s);
 }
 
 int gemm_block_m_fp8(int, int, int) { return 128; }
