@@ -11,10 +11,12 @@ of the other four workloads for exploration.  Prints ONE JSON line on stdout.
 
 Timing:
   * whole layer: HIP events on the launch stream around exactly K calls,
-    bracketed by device synchronisation; host wall clock reported beside it;
-  * per stage: ``moe_forward_profiled`` (the same launches with events between
-    the stages), averaged over K further calls; the dominant kernel's roofline
-    fraction uses this live per-launch duration;
+    bracketed by device synchronisation; host wall clock reported beside it.
+    Each timed call is ``moe_forward_profiled`` with only the two events
+    around GEMM1 set, so the dominant kernel's per-launch duration (the
+    roofline's denominator) is measured live inside the same timed region;
+  * per stage: after the timed region, K further calls with events between
+    all stages (a breakdown only; these events cost a few microseconds each);
   * traffic: HBM bytes per launch from committed rocprofv3 FETCH_SIZE /
     WRITE_SIZE counters, only if the kernel sources still hash to the value
     they were taken at (else null);
@@ -24,7 +26,6 @@ from __future__ import annotations
 
 import argparse
 import ctypes
-import glob
 import hashlib
 import json
 import os
@@ -49,13 +50,15 @@ DESCR = {
     5: "int4 weight-only MoE layer: T=512 H=4096 E=128 I=1536 top_k=8, int4 g128 weights, "
        "Zipf(1.1)-skewed softmax top-8",
 }
-# which bound and kernel dominate each workload
-BOUND = {1: "hbm", 2: "hbm", 3: "mfma", 4: "mfma", 5: "hbm"}
+
+
+# sources that define the GEMM1 kernels (the roofline's dominant kernel)
+GEMM_SOURCES = ("common.hpp", "launch.hpp", "dispatch.hip", "gemm_bf16.hip", "gemm_tiled.hip")
 
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2607_12875_amd", "csrc", "*"))):
+    for p in sorted(os.path.join(ROOT, "paper_2607_12875_amd", "csrc", n) for n in GEMM_SOURCES):
         with open(p, "rb") as f:
             h.update(os.path.basename(p).encode() + f.read())
     return h.hexdigest()[:16]
@@ -164,7 +167,7 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="host-time budget of the oracle baseline (0 disables it)")
@@ -219,30 +222,35 @@ def main():
         moe.moe_forward_args(margs, ws)
     torch.cuda.synchronize()
 
-    # ---- whole layer: exactly K steps between two synchronisations
-    ev = HipEvents(2 + moe.NUM_STAGES + 1)
+    # ---- whole layer: exactly K steps between two synchronisations; every
+    # step brackets its GEMM1 launch with a pair of events of its own
+    K = args.steps
+    ev = HipEvents(2 + 2 * K)
     rt = ev.rt
     rt.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    g1_marks = [[None, None, None, ev.ev[2 + 2 * i], ev.ev[3 + 2 * i], None, None] for i in range(K)]
     torch.cuda.synchronize()
     w0 = time.perf_counter()
     rt.hipEventRecord(ev.ev[0], ctypes.c_void_p(stream.cuda_stream))
-    for _ in range(args.steps):
-        moe.moe_forward_args(margs, ws)
+    for i in range(K):
+        moe.moe_forward_profiled(margs, ws, g1_marks[i])
     rt.hipEventRecord(ev.ev[1], ctypes.c_void_p(stream.cuda_stream))
     torch.cuda.synchronize()
-    wall_ms = (time.perf_counter() - w0) * 1e3 / args.steps
-    ms = ev.elapsed_ms(0, 1) / args.steps
+    wall_ms = (time.perf_counter() - w0) * 1e3 / K
+    ms = ev.elapsed_ms(0, 1) / K
+    g1_launch_us = [ev.elapsed_ms(2 + 2 * i, 3 + 2 * i) * 1e3 for i in range(K)]
+    ev.close()
 
-    # ---- per stage, live: the same launches with events between the stages
-    stage_ev = ev.ev[2:]
+    # ---- per-stage breakdown (after the timed region): events between stages
+    sev = HipEvents(moe.NUM_STAGES + 1)
     stage_sum = np.zeros(moe.NUM_STAGES)
-    for _ in range(args.steps):
-        moe.moe_forward_profiled(margs, ws, stage_ev)
+    for _ in range(K):
+        moe.moe_forward_profiled(margs, ws, sev.ev)
         torch.cuda.synchronize()
         for i in range(moe.NUM_STAGES):
-            stage_sum[i] += ev.elapsed_ms(2 + i, 3 + i)
-    stage_us = {name: float(v * 1e3 / args.steps) for name, v in zip(moe.STAGES, stage_sum)}
-    ev.close()
+            stage_sum[i] += sev.elapsed_ms(i, i + 1)
+    stage_us = {name: float(v * 1e3 / K) for name, v in zip(moe.STAGES, stage_sum)}
+    sev.close()
 
     # routing statistics of this batch (from the layer's own workspace)
     offs = ws[layout["expert_offsets"]:layout["expert_offsets"] + 4 * (cfg.E + 1)].view(torch.int32).cpu().numpy()
@@ -260,22 +268,26 @@ def main():
     act_bytes = {"bf16": 2, "fp8": 1, "int4": 2}[cfg.wfmt]
     g1_bytes = n_active * (2 * I * H * wb + w1_scale_bytes) + T * H * (1 if cfg.wfmt == "fp8" else 2) + n * I * act_bytes
     g1_flops = 2.0 * n * H * 2 * I
-    g1_us = stage_us["gemm1"]
-    bound = BOUND[args.config]
+    g1_us = float(np.mean(g1_launch_us))
+    # the roof that binds GEMM1: the larger of bytes / HBM peak and flops / MFMA peak
+    mfma_peak = PEAK_TFLOPS["fp8" if cfg.wfmt == "fp8" else "bf16"]
+    t_hbm = g1_bytes / (PEAK_HBM_GBS * 1e9)
+    t_mfma = g1_flops / (mfma_peak * 1e12)
+    bound = "hbm" if t_hbm >= t_mfma else "mfma"
     src_hash = kernel_source_hash()
     key = f"{synth.config(args.config).name}_gemm1"
     traffic = load_traffic(key, src_hash)
+    common = {"kernel": "gemm1 (+SiLU*up)", "traffic": traffic, "launch_us": g1_us,
+              "algorithmic_bytes_per_launch": g1_bytes, "algorithmic_flops_per_launch": g1_flops,
+              "roof_us": {"hbm": t_hbm * 1e6, "mfma": t_mfma * 1e6}}
     if bound == "hbm":
         achieved = g1_bytes / (g1_us * 1e-6) / 1e9
-        roof = {"bound": "hbm", "kernel": "gemm1 (+SiLU*up)", "achieved": achieved, "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
-                "algorithmic_bytes_per_launch": g1_bytes, "launch_us": g1_us}
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, **common}
     else:
-        peak = PEAK_TFLOPS["fp8" if cfg.wfmt == "fp8" else "bf16"]
         achieved = g1_flops / (g1_us * 1e-6) / 1e12
-        roof = {"bound": "mfma", "kernel": "gemm1 (+SiLU*up)", "achieved": achieved, "peak": peak,
-                "unit": "TFLOP/s", "frac": achieved / peak, "traffic": traffic,
-                "algorithmic_flops_per_launch": g1_flops, "launch_us": g1_us}
+        roof = {"bound": "mfma", "achieved": achieved, "peak": mfma_peak,
+                "unit": "TFLOP/s", "frac": achieved / mfma_peak, **common}
 
     base = None
     if args.cpu_seconds > 0:

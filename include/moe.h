@@ -196,8 +196,10 @@ moe_status moe_forward(const moe_args* a, void* ws, size_t ws_bytes, hipStream_t
  * with events[i] recorded before stage i and events[MOE_NUM_STAGES] after the
  * last stage.  Stages: 0 gate, 1 permute, 2 fp8 activation quantisation
  * (empty for bf16 / int4), 3 GEMM1 + SiLU*up, 4 GEMM2, 5 combine.
- *   events  host array of MOE_NUM_STAGES + 1 caller-created hipEvent_t
- * Errors: those of moe_forward; MOE_ERR_NULL for a NULL event.
+ *   events  host array of MOE_NUM_STAGES + 1 caller-created hipEvent_t; a
+ *           NULL entry skips that mark (e.g. only GEMM1 bracketed: entries 3
+ *           and 4 set)
+ * Errors: those of moe_forward; MOE_ERR_NULL for a NULL array.
  */
 #define MOE_NUM_STAGES 6
 moe_status moe_forward_profiled(const moe_args* a, void* ws, size_t ws_bytes,

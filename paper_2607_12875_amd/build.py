@@ -4,7 +4,8 @@ library, ``libmoe_mi355x.so``, next to this file.
     python -m paper_2607_12875_amd.build
 
 Every source is compiled with hipcc (``--offload-arch=gfx950``), packed-fp32
-instruction selection disabled, then linked with ``-shared``.  The library is
+instruction selection disabled (plus the per-source flags in EXTRA_FLAGS),
+then linked with ``-shared``.  The library is
 written to a temporary name and renamed, so a concurrent loader never sees a
 half-written file.
 """
@@ -30,13 +31,21 @@ FLAGS = [
 ]
 
 
+# Per-source extra flags.  The tiled GEMMs keep MFMA results in architectural
+# VGPRs, so the fp8 K-block rescale reads its partials without a per-value
+# AGPR-to-VGPR copy (the bf16 and int4 loops compile the same either way).
+EXTRA_FLAGS = {
+    "gemm_tiled.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
+
+
 def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA_FLAGS.get(os.path.basename(src), []), "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stdout}\n{r.stderr}")

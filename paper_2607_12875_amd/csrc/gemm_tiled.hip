@@ -6,10 +6,12 @@
 //
 //  bf16  A, B bf16; v_mfma_f32_32x32x16_bf16.
 //  fp8   A (activations) and B (weights) OCP e4m3; v_mfma_f32_32x32x64_f8f6f4
-//        over one 128-wide K block at a time into a fresh partial, then
-//        acc += partial * s_row(A) * s_block(B) on the VALU.  The GEMM1
-//        epilogue requantises the intermediate per (row, 128 columns): the
-//        tile holds exactly one such group per row.
+//        with W as the first operand (the product is formed transposed),
+//        one 128-wide K block at a time into a fresh partial, then
+//        acc += partial * s_row(A) * s_block(B) on the VALU, overlapped with
+//        the next blocks' MFMAs.  The GEMM1 epilogue requantises the
+//        intermediate per (row, 128 columns): the tile holds exactly one such
+//        group per row.
 //  int4  A bf16; B signed int4 words decoded in registers (q * bf16 scale,
 //        rounded to bf16) right before the bf16 MFMA, never materialised.
 //
@@ -118,7 +120,7 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
   // fp8: waves [0, BM/64) the row scales of A, wave BM/64 the block scales of
   // B; int4: waves [0, BNW/64) the bf16 pair holding each B row's group scale
   constexpr int SC = FMT == 0 ? 0 : 1;
-  static_assert(FMT != 1 || (NW == 4 && BM / 64 < NW), "fp8 scale DMA layout");
+  static_assert(FMT != 1 || BM / 64 < NW, "fp8 scale DMA layout");
   static_assert(FMT != 2 || (NW == 4 && BNW / 64 <= NW), "int4 scale DMA layout");
   static_assert(STAGES >= 2 && (STAGES - 2) * (A_CH + B_CH + (FMT == 0 ? 0 : 1)) < 64, "vmcnt range");
   constexpr int A_BYTES = BM * KB, B_BYTES = BNW * BB, S_BYTES = SC * NW * 256;
@@ -318,7 +320,11 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
           __builtin_amdgcn_sched_barrier(0);
         }
       } else if constexpr (FMT == 1) {
-        f32x16 part[TM][TN];
+        // Transposed product: the MFMA's first operand is a 32-row block of
+        // W (output columns n), the second a 32-row block of A (rows m), so
+        // a lane's 16 values run down n for one row m.  Every value of a
+        // lane then shares one A row scale and one W block scale: the K-block
+        // rescale is one multiply per 32x32 block and one fma per value.
         i32x8 af[2][TM], bfr[2][TN];
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
@@ -326,47 +332,58 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
           for (int i = 0; i < TM; ++i) {
             const int r = wm * WTM + i * 32 + l32;
-            const u32x4 lo = ld16(As + r * KB + ((c0 ^ swz<KB>(r)) << 4));
-            const u32x4 hi = ld16(As + r * KB + (((c0 + 1) ^ swz<KB>(r)) << 4));
-            af[kk][i] = i32x8{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+            const i32x4 lo = __builtin_bit_cast(i32x4, ld16(As + r * KB + ((c0 ^ swz<KB>(r)) << 4)));
+            const i32x4 hi = __builtin_bit_cast(i32x4, ld16(As + r * KB + (((c0 + 1) ^ swz<KB>(r)) << 4)));
+            af[kk][i] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
           }
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
             const int r = brow(j) + l32;
-            const u32x4 lo = ld16(Bs + r * BB + ((c0 ^ swz<KB>(r)) << 4));
-            const u32x4 hi = ld16(Bs + r * BB + (((c0 + 1) ^ swz<KB>(r)) << 4));
-            bfr[kk][j] = i32x8{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+            const i32x4 lo = __builtin_bit_cast(i32x4, ld16(Bs + r * BB + ((c0 ^ swz<KB>(r)) << 4)));
+            const i32x4 hi = __builtin_bit_cast(i32x4, ld16(Bs + r * BB + (((c0 + 1) ^ swz<KB>(r)) << 4)));
+            bfr[kk][j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
           }
         }
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-          for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-              part[i][j] = mfma32x32x64_fp8(af[kk][i], bfr[kk][j], kk == 0 ? f32x16{} : part[i][j]);
-        // acc += part * s_row(A) * s_block(B) for this K block
-        const float* sA = reinterpret_cast<const float*>(Ss);                 // [BM]
+        const float* sA = reinterpret_cast<const float*>(Ss);                    // [BM]
         const float* sB = reinterpret_cast<const float*>(Ss + (BM / 64) * 256);  // [64]
-        float sb[TN];
+        float fa[TM], sb[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) fa[i] = sA[wm * WTM + i * 32 + l32];
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
           const int r = brow(j);
           sb[j] = GEMM1 ? sB[r < NC ? 0 : 1] : sB[(r / 128) % (BNW / 128)];
         }
+        __builtin_amdgcn_sched_barrier(0);
+        // Blocks in pairs: the two K halves of pair q go to the matrix pipe
+        // (independent MFMAs back to back), then the VALU folds pair q-1 into
+        // the accumulators while those run.  Four partial blocks are live.
+        constexpr int NB = TM * TN;
+        static_assert(NB % 2 == 0, "block pairs");
+        f32x16 part[4];
 #pragma unroll
-        for (int i = 0; i < TM; ++i) {
+        for (int q = 0; q <= NB / 2; ++q) {
+          if (q < NB / 2) {
 #pragma unroll
-          for (int v4 = 0; v4 < 4; ++v4) {
-            const float4 sr = *reinterpret_cast<const float4*>(&sA[wm * WTM + i * 32 + 8 * v4 + 4 * kg]);
-            const float s4[4] = {sr.x, sr.y, sr.z, sr.w};
+            for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-            for (int j = 0; j < TN; ++j)
-#pragma unroll
-              for (int u = 0; u < 4; ++u)
-                acc[i][j][4 * v4 + u] = fmaf(part[i][j][4 * v4 + u], s4[u] * sb[j], acc[i][j][4 * v4 + u]);
+              for (int u = 0; u < 2; ++u) {
+                const int bi = 2 * q + u, i = bi / TN, j = bi % TN;
+                f32x16& pp = part[(q & 1) * 2 + u];
+                pp = mfma32x32x64_fp8(bfr[kk][j], af[kk][i], kk == 0 ? f32x16{} : pp);
+              }
           }
+          if (q > 0) {
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+              const int bi = 2 * (q - 1) + u, i = bi / TN, j = bi % TN;
+              const f32x16& pp = part[((q - 1) & 1) * 2 + u];
+              const float f = fa[i] * sb[j];
+#pragma unroll
+              for (int v = 0; v < 16; ++v) acc[i][j][v] = fmaf(pp[v], f, acc[i][j][v]);
+            }
+          }
+          __builtin_amdgcn_sched_barrier(0);
         }
       } else {  // int4
         // this lane's B words for the four 16-wide K substeps, and its scales
@@ -406,7 +423,8 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
     }
 #undef brow
 
-    // ---- epilogue.  D element v of a 32x32 tile: row 8*(v/4) + 4*kg + v%4, column l32.
+    // ---- epilogue.  D element v of a 32x32 tile (bf16, int4): row
+    // 8*(v/4) + 4*kg + v%4, column l32; fp8 holds the transpose.
     if constexpr (GEMM1) {
       constexpr int TH = TN / 2;  // gate tiles (paired with up tile j + TH)
       float av[TM][TH][16];
@@ -417,38 +435,42 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
           for (int v = 0; v < 16; ++v) av[i][j][v] = silu_mul(acc[i][j][v], acc[i][j + TH][v]);
       if constexpr (FMT == 1) {
-        // per-row amax over the tile's 128 columns: lanes, then waves (LDS)
+        // transposed layout: lane (kg, l32) of row block i holds row
+        // wm*WTM + i*32 + l32 at columns 8*(v/4) + 4*kg + v%4 of each gate
+        // block.  Row amax over the tile's 128 columns: the lane's values,
+        // the other k-group lane, then the WN waves (LDS).
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i) {
+          float m = 0.f;
 #pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            float m = 0.f;
+          for (int j = 0; j < TH; ++j)
 #pragma unroll
-            for (int j = 0; j < TH; ++j) m = fmaxf(m, fabsf(av[i][j][v]));
-#pragma unroll
-            for (int off = 1; off < 32; off <<= 1) m = fmaxf(m, __shfl_xor(m, off));
-            if (l32 == 0) lds_amax[wn][wm * WTM + i * 32 + 8 * (v >> 2) + 4 * kg + (v & 3)] = m;
-          }
+            for (int v = 0; v < 16; ++v) m = fmaxf(m, fabsf(av[i][j][v]));
+          m = fmaxf(m, __shfl_xor(m, 32));
+          if (kg == 0) lds_amax[wn][wm * WTM + i * 32 + l32] = m;
+        }
         __syncthreads();
         uint8_t* q = static_cast<uint8_t*>(g.inter);
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i) {
+          const int rl = wm * WTM + i * 32 + l32;
+          float m = 0.f;
 #pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int rl = wm * WTM + i * 32 + 8 * (v >> 2) + 4 * kg + (v & 3);
-            float m = 0.f;
+          for (int w = 0; w < WN; ++w) m = fmaxf(m, lds_amax[w][rl]);
+          const float sc = fmaxf(m, 1e-10f) / 448.0f;
+          const size_t row = static_cast<size_t>(m0 + rl);
 #pragma unroll
-            for (int w = 0; w < WN; ++w) m = fmaxf(m, lds_amax[w][rl]);
-            const float s = fmaxf(m, 1e-10f) / 448.0f;
-            const int row = m0 + rl;
+          for (int j = 0; j < TH; ++j)
 #pragma unroll
-            for (int j = 0; j < TH; ++j) {
-              const int col = n0 + wn * (WTN / 2) + j * 32 + l32;
-              q[static_cast<size_t>(row) * g.I + col] =
-                  static_cast<uint8_t>(f32x2_to_e4m3(sat_e4m3(av[i][j][v] / s), 0.f) & 0xFF);
+            for (int v4 = 0; v4 < 4; ++v4) {
+              const int col = n0 + wn * (WTN / 2) + j * 32 + 8 * v4 + 4 * kg;
+              const float* a4 = &av[i][j][4 * v4];
+              const uint32_t codes = f32x2_to_e4m3(sat_e4m3(a4[0] / sc), sat_e4m3(a4[1] / sc)) |
+                                     (f32x2_to_e4m3(sat_e4m3(a4[2] / sc), sat_e4m3(a4[3] / sc)) << 16);
+              *reinterpret_cast<uint32_t*>(q + row * g.I + col) = codes;
             }
-            if (wn == 0 && l32 == 0) g.inter_scale[static_cast<size_t>(row) * (g.I / 128) + n0 / 128] = s;
-          }
+          if (wn == 0 && kg == 0) g.inter_scale[row * (g.I / 128) + n0 / 128] = sc;
+        }
         __syncthreads();  // lds_amax is reused by the next tile
       } else {
         uint16_t* o = static_cast<uint16_t*>(g.inter);
@@ -462,6 +484,23 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
               const int col = n0 + wn * (WTN / 2) + j * 32 + l32;
               o[static_cast<size_t>(row) * g.I + col] = f32_to_bf16(av[i][j][v]);
             }
+      }
+    } else if constexpr (FMT == 1) {
+      // transposed layout: four consecutive output columns per 8-byte store
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int row = m0 + wm * WTM + i * 32 + l32;
+        if (g.sorted_ids[row] >= g.n_routed) continue;  // pad rows are never read
+        uint16_t* yr = static_cast<uint16_t*>(g.y) + static_cast<size_t>(row) * g.H;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int v4 = 0; v4 < 4; ++v4) {
+            const int col = n0 + wn * WTN + j * 32 + 8 * v4 + 4 * kg;
+            const f32x16& c = acc[i][j];
+            const uint2 pk = {pack_bf16x2(c[4 * v4], c[4 * v4 + 1]), pack_bf16x2(c[4 * v4 + 2], c[4 * v4 + 3])};
+            *reinterpret_cast<uint2*>(yr + col) = pk;
+          }
       }
     } else {
 #pragma unroll
@@ -555,13 +594,18 @@ hipError_t launch_gemm2_bf16_tiled(const GroupedGemm& g, hipStream_t s) {
   return launch_tiled<0, false, MOE_TBF_BM, MOE_T2_BNW, MOE_T2_WM, MOE_T2_WN, MOE_TGM, MOE_TBF_KB, MOE_TBF_STAGES>(g, s);
 }
 
+// fp8 waves per workgroup as WM x WN over the 128 x 256 tile
+#ifndef MOE_F8_WM
+#define MOE_F8_WM 2
+#define MOE_F8_WN 4
+#endif
 int gemm_block_m_fp8(int, int, int) { return 128; }
 hipError_t launch_gemm1_fp8(const GroupedGemm& g, hipStream_t s) {
-  return launch_tiled<1, true, 128, 256, 2, 2, MOE_TGM>(g, s);
+  return launch_tiled<1, true, 128, 256, MOE_F8_WM, MOE_F8_WN, MOE_TGM>(g, s);
 }
 hipError_t launch_gemm2_fp8(const GroupedGemm& g, hipStream_t s) {
-  if (g.H % 256) return launch_tiled<1, false, 128, 128, 2, 2, MOE_TGM>(g, s);
-  return launch_tiled<1, false, 128, 256, 2, 2, MOE_TGM>(g, s);
+  if (g.H % 256) return launch_tiled<1, false, 128, 128, MOE_F8_WM, MOE_F8_WN, MOE_TGM>(g, s);
+  return launch_tiled<1, false, 128, 256, MOE_F8_WM, MOE_F8_WN, MOE_TGM>(g, s);
 }
 
 int gemm_block_m_int4(int, int, int) { return 64; }
