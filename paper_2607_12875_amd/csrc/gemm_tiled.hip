@@ -99,10 +99,17 @@ __device__ __forceinline__ void bar() {
 template <int KB>
 __device__ __forceinline__ int swz(int r) { return KB == 128 ? (r >> 1) & 7 : (r >> 2) & 3; }
 
-template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM, int KBT = 128, int STAGES = 3>
-__global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
-  constexpr int NW = WM * WN, NT = NW * 64;
-  static_assert(NW == 4 || NW == 8, "four or eight waves");
+// NP > 0: NP extra waves only issue the global->LDS copies and the NW math
+// waves never touch global memory in the main loop, so a stalled load queue
+// (L1 waiting on L2) cannot hold up the MFMA stream behind an in-order copy
+// instruction.  NP == 0: the math waves issue the copies themselves.
+template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM, int KBT = 128, int STAGES = 3, int NP = 0>
+__global__ __launch_bounds__((WM * WN + NP) * 64) void moe_gemm_tiled(GroupedGemm g) {
+  constexpr int NW = WM * WN, NT = (NW + NP) * 64;
+  constexpr int LW = NP > 0 ? NP : NW;  // waves that issue the copies
+  static_assert(NW == 4 || NW == 8, "four or eight math waves");
+  static_assert(NP == 0 || NW % NP == 0, "scale slots split evenly over the copy waves");
+  static_assert(NP == 0 || !(FMT == 1 && GEMM1), "the fp8 GEMM1 epilogue synchronises the math waves only");
   static_assert(KBT == 128 || (KBT == 64 && FMT == 0), "64-byte steps are bf16 only");
   constexpr int KB = KBT;                                       // A bytes per row per step
   constexpr int KE = FMT == 0 ? KB / 2 : FmtTraits<FMT>::KE;   // K elements per step
@@ -111,21 +118,22 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
   constexpr int WTM = BM / WM, WTN = BNW / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
   constexpr int NC = GEMM1 ? BNW / 2 : BNW;  // output columns per tile
-  // 16-byte DMA instructions per wave per stage (each moves 1 KB)
-  constexpr int A_CH = BM * KB / 1024 / NW, B_CH = BNW * BB / 1024 / NW;
-  static_assert(A_CH >= 1 && B_CH >= 1 && A_CH * NW * 1024 == BM * KB && B_CH * NW * 1024 == BNW * BB, "");
+  // 16-byte DMA instructions per copy wave per stage (each moves 1 KB)
+  constexpr int A_CH = BM * KB / 1024 / LW, B_CH = BNW * BB / 1024 / LW;
+  static_assert(A_CH >= 1 && B_CH >= 1 && A_CH * LW * 1024 == BM * KB && B_CH * LW * 1024 == BNW * BB, "");
   static_assert(!GEMM1 || TN % 2 == 0, "gate/up pairs");
   static_assert(FMT != 1 || !GEMM1 || NC == 128, "fp8 requant needs one 128-column group per tile");
-  // per-stage scale block: one 4-byte DMA instruction per wave (64 floats),
-  // fp8: waves [0, BM/64) the row scales of A, wave BM/64 the block scales of
-  // B; int4: waves [0, BNW/64) the bf16 pair holding each B row's group scale
-  constexpr int SC = FMT == 0 ? 0 : 1;
+  // per-stage scale block: NW slots of 256 bytes, one 4-byte DMA instruction
+  // each (64 floats); fp8: slots [0, BM/64) the row scales of A, slot BM/64
+  // the block scales of B; int4: slots [0, BNW/64) the bf16 pair holding each
+  // B row's group scale.  Copy wave lw fills slots lw, lw + LW, ...
+  constexpr int SC = FMT == 0 ? 0 : NW / LW;  // scale loads per copy wave per stage
   static_assert(FMT != 1 || BM / 64 < NW, "fp8 scale DMA layout");
   static_assert(FMT != 2 || (NW == 4 && BNW / 64 <= NW), "int4 scale DMA layout");
-  static_assert(STAGES >= 2 && (STAGES - 2) * (A_CH + B_CH + (FMT == 0 ? 0 : 1)) < 64, "vmcnt range");
-  constexpr int A_BYTES = BM * KB, B_BYTES = BNW * BB, S_BYTES = SC * NW * 256;
+  static_assert(STAGES >= 2 && (STAGES - 2) * (A_CH + B_CH + SC) < 64, "vmcnt range");
+  constexpr int A_BYTES = BM * KB, B_BYTES = BNW * BB, S_BYTES = FMT == 0 ? 0 : NW * 256;
   constexpr int STAGE = A_BYTES + B_BYTES + S_BYTES;
-  constexpr int N_DMA = A_CH + B_CH + SC;  // loads per wave per stage
+  constexpr int N_DMA = A_CH + B_CH + SC;  // loads per copy wave per stage
 
   __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES][STAGE];
   __shared__ float lds_amax[FMT == 1 && GEMM1 ? WN : 1][FMT == 1 && GEMM1 ? BM : 1];
@@ -133,6 +141,10 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
 
   const int tid = threadIdx.x, lane = lane_id(), wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
+  const bool is_math = wave < NW;                       // uniform per wave
+  const bool is_loader = NP == 0 || wave >= NW;
+  // copy-wave index (math waves of a split launch take 0: their sources stay in range, unused)
+  const int lw = NP > 0 ? (is_loader ? wave - NW : 0) : wave;
   const int l32 = lane & 31, kg = lane >> 5;
   const int K = GEMM1 ? g.H : g.I;
   const int N = GEMM1 ? g.I : g.H;       // output columns of the product
@@ -164,15 +176,15 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
     const int m0 = mt * BM, n0 = nt * NC;
     __syncthreads();  // the previous tile's last stages are no longer read
 
-    // ---- per-lane DMA sources.  Instruction i of wave w fills the 1 KB block
-    // (i*NW + w) of a stage: 8 rows of A / of fp8-bf16 B (lane -> row l/8,
-    // 16-byte slot l%8) or 32 rows of int4 B (row l/2, slot l%2).  Slot s of
-    // row r holds the row's chunk s ^ swz<KB>(r), the XOR swizzle the fragment
-    // reads undo.
+    // ---- per-lane DMA sources.  Instruction i of copy wave lw fills the 1 KB
+    // block (i*LW + lw) of a stage: 8 rows of A / of fp8-bf16 B (lane -> row
+    // l/8, 16-byte slot l%8) or 32 rows of int4 B (row l/2, slot l%2).  Slot s
+    // of row r holds the row's chunk s ^ swz<KB>(r), the XOR swizzle the
+    // fragment reads undo.
     const uint8_t* a_src[A_CH];
 #pragma unroll
     for (int i = 0; i < A_CH; ++i) {
-      const int r = (i * NW + wave) * RPI + lane / LPR;
+      const int r = (i * LW + lw) * RPI + lane / LPR;
       const uint8_t* row;
       if (GEMM1) {
         const int sid = g.sorted_ids[m0 + r];
@@ -189,7 +201,7 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
     const uint8_t* b_src[B_CH];
 #pragma unroll
     for (int i = 0; i < B_CH; ++i) {
-      const int blk = i * NW + wave;
+      const int blk = i * LW + lw;
       const int r = FMT == 2 ? blk * 32 + (lane >> 1) : blk * RPI + lane / LPR;
       const int sl = FMT == 2 ? (lane & 1) ^ ((r >> 2) & 1) : (lane % LPR) ^ swz<KB>(r);
       int n;
@@ -197,62 +209,75 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
       else n = n0 + r;
       b_src[i] = wbase + static_cast<size_t>(n) * w_row_bytes + (sl << 4);
     }
-    // scale DMA source of this lane (advanced by one K block / half group per step)
-    const uint8_t* s_src = a_src[0];  // waves without a scale role load a harmless dummy
-    int s_step = 0;
-    if constexpr (FMT == 1) {
-      if (wave < BM / 64) {
-        const int r = wave * 64 + lane;
-        if (GEMM1) {
-          const int sid = g.sorted_ids[m0 + r];
-          const int tok = sid < g.n_routed ? sid / g.top_k : 0;
-          s_src = reinterpret_cast<const uint8_t*>(g.x_scale + static_cast<size_t>(tok) * (g.H / 128));
-        } else {
-          s_src = reinterpret_cast<const uint8_t*>(g.inter_scale + static_cast<size_t>(m0 + r) * (g.I / 128));
+    // scale DMA sources of this lane, one per slot lw + k*LW (advanced by one
+    // K block / half group per step); slots without a scale role load a
+    // harmless dummy
+    constexpr int NSL = SC > 0 ? SC : 1;
+    const uint8_t* s_src[NSL];
+    int s_step[NSL];
+#pragma unroll
+    for (int k = 0; k < NSL; ++k) {
+      const int sl = lw + k * LW;
+      s_src[k] = a_src[0];
+      s_step[k] = 0;
+      if constexpr (FMT == 1) {
+        if (sl < BM / 64) {
+          const int r = sl * 64 + lane;
+          if (GEMM1) {
+            const int sid = g.sorted_ids[m0 + r];
+            const int tok = sid < g.n_routed ? sid / g.top_k : 0;
+            s_src[k] = reinterpret_cast<const uint8_t*>(g.x_scale + static_cast<size_t>(tok) * (g.H / 128));
+          } else {
+            s_src[k] = reinterpret_cast<const uint8_t*>(g.inter_scale + static_cast<size_t>(m0 + r) * (g.I / 128));
+          }
+          s_step[k] = 4;
+        } else if (sl == BM / 64) {
+          // lane l: block row of W (GEMM1: l odd -> up half, even -> gate half;
+          // GEMM2: block row n0/128 + l % (BNW/128))
+          const float* wsc = static_cast<const float*>(GEMM1 ? g.w1_scale : g.w2_scale) +
+                             static_cast<size_t>(e) * ((GEMM1 ? 2 * g.I : g.H) / 128) * (K / 128);
+          const int br = GEMM1 ? ((lane & 1) ? (g.I + n0) / 128 : n0 / 128) : n0 / 128 + lane % (BNW / 128);
+          s_src[k] = reinterpret_cast<const uint8_t*>(wsc + static_cast<size_t>(br) * (K / 128));
+          s_step[k] = 4;
         }
-        s_step = 4;
-      } else if (wave == BM / 64) {
-        // lane l: block row of W (GEMM1: l odd -> up half, even -> gate half;
-        // GEMM2: block row n0/128 + l % (BNW/128))
-        const float* wsc = static_cast<const float*>(GEMM1 ? g.w1_scale : g.w2_scale) +
-                           static_cast<size_t>(e) * ((GEMM1 ? 2 * g.I : g.H) / 128) * (K / 128);
-        const int br = GEMM1 ? ((lane & 1) ? (g.I + n0) / 128 : n0 / 128) : n0 / 128 + lane % (BNW / 128);
-        s_src = reinterpret_cast<const uint8_t*>(wsc + static_cast<size_t>(br) * (K / 128));
-        s_step = 4;
-      }
-    } else if constexpr (FMT == 2) {
-      if (wave < BNW / 64) {
-        const int r = wave * 64 + lane;
-        const int n = GEMM1 ? (r < NC ? n0 + r : g.I + n0 + (r - NC)) : n0 + r;
-        // bf16 scale [n][group] of K step kt sits at element n*(K/128) + kt/2;
-        // the dword holding it starts at the even element below
-        s_src = reinterpret_cast<const uint8_t*>(static_cast<const uint16_t*>(GEMM1 ? g.w1_scale : g.w2_scale) +
-                                                 (static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) + n) * (K / 128));
-        s_step = 1;  // advanced per step in elements below
+      } else if constexpr (FMT == 2) {
+        if (sl < BNW / 64) {
+          const int r = sl * 64 + lane;
+          const int n = GEMM1 ? (r < NC ? n0 + r : g.I + n0 + (r - NC)) : n0 + r;
+          // bf16 scale [n][group] of K step kt sits at element n*(K/128) + kt/2;
+          // the dword holding it starts at the even element below
+          s_src[k] = reinterpret_cast<const uint8_t*>(static_cast<const uint16_t*>(GEMM1 ? g.w1_scale : g.w2_scale) +
+                                                      (static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) + n) * (K / 128));
+          s_step[k] = 1;  // advanced per step in elements below
+        }
       }
     }
 
-    // issue stage kt (DMA q in [q0, q1) of this wave's A_CH + B_CH tile
-    // loads for one K step, plus the scale load with q1 == N_DMA) into buffer kt % STAGES
+    // issue stage kt (DMA q in [q0, q1) of this copy wave's A_CH + B_CH tile
+    // loads for one K step, plus the scale loads with q1 == N_DMA) into buffer kt % STAGES
     auto issue_part = [&](int kt, int q0, int q1) {
       const uint32_t base = smem0 + (kt % STAGES) * STAGE;
 #pragma unroll
       for (int i = 0; i < A_CH; ++i)
-        if (i >= q0 && i < q1) dma16(a_src[i] + kt * KB, base + (i * NW + wave) * 1024);
+        if (i >= q0 && i < q1) dma16(a_src[i] + kt * KB, base + (i * LW + lw) * 1024);
 #pragma unroll
       for (int i = 0; i < B_CH; ++i)
-        if (A_CH + i >= q0 && A_CH + i < q1) dma16(b_src[i] + kt * BB, base + A_BYTES + (i * NW + wave) * 1024);
+        if (A_CH + i >= q0 && A_CH + i < q1) dma16(b_src[i] + kt * BB, base + A_BYTES + (i * LW + lw) * 1024);
       if (q1 < N_DMA) return;
-      if constexpr (FMT == 1) {
-        dma4(s_src + kt * s_step, base + A_BYTES + B_BYTES + wave * 256);
-      } else if constexpr (FMT == 2) {
-        // element offset kt/2 within the row, rounded down to an even element (4-byte aligned)
-        const uint8_t* p = s_src;
-        if (s_step) {
-          const uintptr_t a = reinterpret_cast<uintptr_t>(s_src) + (kt >> 1) * 2;
-          p = reinterpret_cast<const uint8_t*>(a & ~static_cast<uintptr_t>(3));
+#pragma unroll
+      for (int k = 0; k < SC; ++k) {
+        const uint32_t dst = base + A_BYTES + B_BYTES + (lw + k * LW) * 256;
+        if constexpr (FMT == 1) {
+          dma4(s_src[k] + kt * s_step[k], dst);
+        } else if constexpr (FMT == 2) {
+          // element offset kt/2 within the row, rounded down to an even element (4-byte aligned)
+          const uint8_t* p = s_src[k];
+          if (s_step[k]) {
+            const uintptr_t a = reinterpret_cast<uintptr_t>(s_src[k]) + (kt >> 1) * 2;
+            p = reinterpret_cast<const uint8_t*>(a & ~static_cast<uintptr_t>(3));
+          }
+          dma4(p, dst);
         }
-        dma4(p, base + A_BYTES + B_BYTES + wave * 256);
       }
     };
     auto issue = [&](int kt) { issue_part(kt, 0, N_DMA); };
@@ -268,21 +293,36 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_gemm_tiled(GroupedGemm g) {
                        : wn * WTN + (j) * 32)
 
     // STAGES-1 steps are loaded ahead; step kt+STAGES-1 goes into the buffer
-    // read in step kt-1, once the barrier shows every wave is past it
-#pragma unroll
-    for (int q = 0; q < STAGES - 1; ++q)
-      if (q < nk) issue(q);
-    for (int kt = 0; kt < nk; ++kt) {
-      // stage kt has landed in every wave; the later stages may still fly
+    // read in step kt-1, once the barrier shows every wave is past it.
+    // stage kt has landed in this copy wave once at most `ahead` later stages fly
+    auto wait_landed = [&](int kt) {
       const int ahead = min(STAGES - 2, nk - 1 - kt);  // stages issued after kt
-      if constexpr (STAGES >= 6) { if (ahead >= 4) { vm_wait<4 * N_DMA>(); goto landed; } }
-      if constexpr (STAGES >= 5) { if (ahead == 3) { vm_wait<3 * N_DMA>(); goto landed; } }
-      if constexpr (STAGES >= 4) { if (ahead == 2) { vm_wait<2 * N_DMA>(); goto landed; } }
-      if constexpr (STAGES >= 3) { if (ahead == 1) { vm_wait<N_DMA>(); goto landed; } }
+      if constexpr (STAGES >= 6) { if (ahead >= 4) { vm_wait<4 * N_DMA>(); return; } }
+      if constexpr (STAGES >= 5) { if (ahead == 3) { vm_wait<3 * N_DMA>(); return; } }
+      if constexpr (STAGES >= 4) { if (ahead == 2) { vm_wait<2 * N_DMA>(); return; } }
+      if constexpr (STAGES >= 3) { if (ahead == 1) { vm_wait<N_DMA>(); return; } }
       vm_wait<0>();
-    landed:
-      bar();
-      const bool pre = kt + STAGES - 1 < nk;  // a later stage to start loading
+    };
+    if (is_loader) {
+#pragma unroll
+      for (int q = 0; q < STAGES - 1; ++q)
+        if (q < nk) issue(q);
+    }
+    if constexpr (NP > 0) {
+      if (!is_math) {
+        // copy waves: the same one barrier per step as the math loop below
+        for (int kt = 0; kt < nk; ++kt) {
+          wait_landed(kt);
+          bar();
+          if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
+        }
+        continue;  // no epilogue
+      }
+    }
+    for (int kt = 0; kt < nk; ++kt) {
+      if constexpr (NP == 0) wait_landed(kt);
+      bar();  // every stage-kt copy of every copy wave has landed
+      const bool pre = NP == 0 && kt + STAGES - 1 < nk;  // this wave starts a later stage
       if (FMT != 0 && pre) issue(kt + STAGES - 1);
       const uint8_t* As = &smem[kt % STAGES][0];
       const uint8_t* Bs = As + A_BYTES;
@@ -546,12 +586,12 @@ dim3 persistent_grid(Kernel k, int threads, long max_tiles) {
   return dim3(static_cast<unsigned>(std::max<long>(kXcds, std::min(n, cap))));
 }
 
-template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM, int KBT = 128, int STAGES = 3>
+template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM, int KBT = 128, int STAGES = 3, int NP = 0>
 hipError_t launch_tiled(const GroupedGemm& g, hipStream_t s) {
   constexpr int NC = GEMM1 ? BNW / 2 : BNW;
-  constexpr int NT = WM * WN * 64;
+  constexpr int NT = (WM * WN + NP) * 64;
   const long mt = g.max_rows / BM, nt = (GEMM1 ? g.I : g.H) / NC;
-  auto kern = moe_gemm_tiled<FMT, GEMM1, BM, BNW, WM, WN, GM, KBT, STAGES>;
+  auto kern = moe_gemm_tiled<FMT, GEMM1, BM, BNW, WM, WN, GM, KBT, STAGES, NP>;
   hipLaunchKernelGGL(kern, persistent_grid(kern, NT, mt * nt), dim3(NT), 0, s, g);
   return hipGetLastError();
 }
@@ -578,6 +618,21 @@ hipError_t launch_tiled(const GroupedGemm& g, hipStream_t s) {
 #ifndef MOE_TBF_STAGES
 #define MOE_TBF_STAGES 3
 #endif
+// Copy waves beside the math waves (0: the math waves copy).  GEMM1 gains
+// from them; the GEMM2 launches (short K loops, and for int4 a second
+// workgroup per CU that the extra waves' registers would evict) do not.
+#ifndef MOE_TBF_NP1
+#define MOE_TBF_NP1 4
+#endif
+#ifndef MOE_TBF_NP2
+#define MOE_TBF_NP2 0
+#endif
+#ifndef MOE_TI4_NP1
+#define MOE_TI4_NP1 4
+#endif
+#ifndef MOE_TI4_NP2
+#define MOE_TI4_NP2 0
+#endif
 // most row tiles of one expert swept together per column tile
 #ifndef MOE_TGM
 #define MOE_TGM 8
@@ -587,11 +642,11 @@ hipError_t launch_tiled(const GroupedGemm& g, hipStream_t s) {
 #endif
 int bf16_tiled_block_m() { return MOE_TBF_BM; }
 hipError_t launch_gemm1_bf16_tiled(const GroupedGemm& g, hipStream_t s) {
-  return launch_tiled<0, true, MOE_TBF_BM, MOE_T1_BNW, MOE_T1_WM, MOE_T1_WN, MOE_TGM, MOE_TBF_KB, MOE_TBF_STAGES>(g, s);
+  return launch_tiled<0, true, MOE_TBF_BM, MOE_T1_BNW, MOE_T1_WM, MOE_T1_WN, MOE_TGM, MOE_TBF_KB, MOE_TBF_STAGES, MOE_TBF_NP1>(g, s);
 }
 hipError_t launch_gemm2_bf16_tiled(const GroupedGemm& g, hipStream_t s) {
-  if (g.H % MOE_T2_BNW) return launch_tiled<0, false, MOE_TBF_BM, 128, MOE_T2_WM, MOE_T2_WN, MOE_TGM, MOE_TBF_KB, MOE_TBF_STAGES>(g, s);
-  return launch_tiled<0, false, MOE_TBF_BM, MOE_T2_BNW, MOE_T2_WM, MOE_T2_WN, MOE_TGM, MOE_TBF_KB, MOE_TBF_STAGES>(g, s);
+  if (g.H % MOE_T2_BNW) return launch_tiled<0, false, MOE_TBF_BM, 128, MOE_T2_WM, MOE_T2_WN, MOE_TGM, MOE_TBF_KB, MOE_TBF_STAGES, MOE_TBF_NP2>(g, s);
+  return launch_tiled<0, false, MOE_TBF_BM, MOE_T2_BNW, MOE_T2_WM, MOE_T2_WN, MOE_TGM, MOE_TBF_KB, MOE_TBF_STAGES, MOE_TBF_NP2>(g, s);
 }
 
 // fp8 waves per workgroup as WM x WN over the 128 x 256 tile
@@ -610,11 +665,11 @@ hipError_t launch_gemm2_fp8(const GroupedGemm& g, hipStream_t s) {
 
 int gemm_block_m_int4(int, int, int) { return 64; }
 hipError_t launch_gemm1_int4(const GroupedGemm& g, hipStream_t s) {
-  return launch_tiled<2, true, 64, 256, 1, 4, MOE_TGM_INT4>(g, s);
+  return launch_tiled<2, true, 64, 256, 1, 4, MOE_TGM_INT4, 128, 3, MOE_TI4_NP1>(g, s);
 }
 hipError_t launch_gemm2_int4(const GroupedGemm& g, hipStream_t s) {
-  if (g.H % 256) return launch_tiled<2, false, 64, 128, 1, 4, MOE_TGM_INT4>(g, s);
-  return launch_tiled<2, false, 64, 256, 1, 4, MOE_TGM_INT4>(g, s);
+  if (g.H % 256) return launch_tiled<2, false, 64, 128, 1, 4, MOE_TGM_INT4, 128, 3, MOE_TI4_NP2>(g, s);
+  return launch_tiled<2, false, 64, 256, 1, 4, MOE_TGM_INT4, 128, 3, MOE_TI4_NP2>(g, s);
 }
 
 }  // namespace moe

@@ -48,6 +48,12 @@ def test_small_shapes_skinny_and_tiled(dev, T):
     _check(synth.tiny_config(1, T=T, H=384, I=256, E=4, top_k=2))
 
 
+@pytest.mark.parametrize("T", [5, 400])
+def test_minimum_k(dev, T):
+    # H = I = 128: two K steps per tile, fewer than the pipeline has stages
+    _check(synth.tiny_config(1, T=T, H=128, I=128, E=4, top_k=2))
+
+
 def test_many_experts_ragged(dev):
     _check(synth.tiny_config(1, T=201, H=512, I=384, E=40, top_k=5))
 

@@ -91,6 +91,12 @@ def test_int4_h_not_multiple_of_256(dev):
     _check(synth.tiny_config(5, T=150, H=384, I=384, E=8, top_k=3))
 
 
+@pytest.mark.parametrize("wcfg", [4, 5])
+def test_quant_minimum_k(dev, wcfg):
+    # H = I = 128: one (fp8) or two (int4) K steps per tile
+    _check(synth.tiny_config(wcfg, T=400, H=128, I=128, E=4, top_k=2))
+
+
 def test_int4_workload_full_size(dev):
     _check(synth.config(5))
 
