@@ -109,7 +109,7 @@ __global__ __launch_bounds__((WM * WN + NP) * 64) void moe_gemm_tiled(GroupedGem
   constexpr int LW = NP > 0 ? NP : NW;  // waves that issue the copies
   static_assert(NW == 4 || NW == 8, "four or eight math waves");
   static_assert(NP == 0 || NW % NP == 0, "scale slots split evenly over the copy waves");
-  static_assert(NP == 0 || !(FMT == 1 && GEMM1), "the fp8 GEMM1 epilogue synchronises the math waves only");
+  static_assert(NP == 0 || WM * WN == 4, "split launches have one math wave per SIMD");
   static_assert(KBT == 128 || (KBT == 64 && FMT == 0), "64-byte steps are bf16 only");
   constexpr int KB = KBT;                                       // A bytes per row per step
   constexpr int KE = FMT == 0 ? KB / 2 : FmtTraits<FMT>::KE;   // K elements per step
@@ -316,10 +316,60 @@ __global__ __launch_bounds__((WM * WN + NP) * 64) void moe_gemm_tiled(GroupedGem
           bar();
           if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
         }
+        if constexpr (FMT == 1 && GEMM1) {  // the two barriers of the requant epilogue
+          __syncthreads();
+          __syncthreads();
+        }
         continue;  // no epilogue
       }
     }
-    for (int kt = 0; kt < nk; ++kt) {
+    if constexpr (NP > 0 && FMT == 0) {
+      // Math waves of a split bf16 launch: fragments are read one MFMA K
+      // substep ahead into a double buffer.  The barrier for stage kt+1 sits
+      // before the last substep's MFMAs of step kt (once this wave's reads of
+      // stage kt are complete), so the next stage's first fragments load
+      // while those MFMAs run; the barrier count is still one per step.
+      constexpr int NKK = KE / 16;
+      static_assert(NKK % 2 == 0, "substep parity");
+      bf16x8 fa[2][TM], fb[2][TN];
+      auto read_frags = [&](int kt, int kk, int buf) {
+        const uint8_t* As = &smem[kt % STAGES][0];
+        const uint8_t* Bs = As + A_BYTES;
+        const int ch = 2 * kk + kg;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int r = wm * WTM + i * 32 + l32;
+          fa[buf][i] = as_bf16x8(ld16(As + r * KB + ((ch ^ swz<KB>(r)) << 4)));
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int r = brow(j) + l32;
+          fb[buf][j] = as_bf16x8(ld16(Bs + r * BB + ((ch ^ swz<KB>(r)) << 4)));
+        }
+      };
+      bar();  // stage 0 has landed
+      read_frags(0, 0, 0);
+      for (int kt = 0; kt < nk; ++kt) {
+#pragma unroll
+        for (int kk = 0; kk < NKK; ++kk) {
+          if (kk + 1 < NKK) {
+            read_frags(kt, kk + 1, (kk + 1) & 1);
+          } else if (kt + 1 < nk) {
+            __atomic_signal_fence(__ATOMIC_SEQ_CST);
+            __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): stage kt is in registers
+            bar();                               // stage kt+1 has landed; buffer kt is free
+            read_frags(kt + 1, 0, 0);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(fa[kk & 1][i], fb[kk & 1][j], acc[i][j]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+    for (int kt = 0; kt < nk && !(NP > 0 && FMT == 0); ++kt) {
       if constexpr (NP == 0) wait_landed(kt);
       bar();  // every stage-kt copy of every copy wave has landed
       const bool pre = NP == 0 && kt + STAGES - 1 < nk;  // this wave starts a later stage
@@ -357,6 +407,68 @@ __global__ __launch_bounds__((WM * WN + NP) * 64) void moe_gemm_tiled(GroupedGem
             for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(af[kk][i], bfr[kk][j], acc[i][j]);
           __builtin_amdgcn_sched_barrier(0);
           if (pre) issue_part(kt + STAGES - 1, kk * PER, min((kk + 1) * PER, A_CH + B_CH));
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      } else if constexpr (FMT == 1 && NP > 0) {
+        // fp8 math waves of a split launch (two waves per SIMD, so at most 256
+        // registers each): transposed product as below, but one 32x32 block
+        // at a time -- its two K halves are MFMAs on one partial, and the
+        // VALU folds the previous block's partial in between them -- with
+        // the W fragments read per column block, one block ahead.
+        i32x8 af[2][TM];
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          const int c0 = 4 * kk + 2 * kg;
+#pragma unroll
+          for (int i = 0; i < TM; ++i) {
+            const int r = wm * WTM + i * 32 + l32;
+            const i32x4 lo = __builtin_bit_cast(i32x4, ld16(As + r * KB + ((c0 ^ swz<KB>(r)) << 4)));
+            const i32x4 hi = __builtin_bit_cast(i32x4, ld16(As + r * KB + (((c0 + 1) ^ swz<KB>(r)) << 4)));
+            af[kk][i] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          }
+        }
+        i32x8 bq[2][2];  // [buffer][K half] of one column block
+        auto read_b = [&](int j, int buf) {
+          const int r = brow(j) + l32;
+#pragma unroll
+          for (int kk = 0; kk < 2; ++kk) {
+            const int c0 = 4 * kk + 2 * kg;
+            const i32x4 lo = __builtin_bit_cast(i32x4, ld16(Bs + r * BB + ((c0 ^ swz<KB>(r)) << 4)));
+            const i32x4 hi = __builtin_bit_cast(i32x4, ld16(Bs + r * BB + (((c0 + 1) ^ swz<KB>(r)) << 4)));
+            bq[buf][kk] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          }
+        };
+        read_b(0, 0);
+        const float* sA = reinterpret_cast<const float*>(Ss);                    // [BM]
+        const float* sB = reinterpret_cast<const float*>(Ss + (BM / 64) * 256);  // [64]
+        float fa[TM], sb[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) fa[i] = sA[wm * WTM + i * 32 + l32];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int r = brow(j);
+          sb[j] = GEMM1 ? sB[r < NC ? 0 : 1] : sB[(r / 128) % (BNW / 128)];
+        }
+        f32x16 part[2];
+        // blocks column-major: b = j*TM + i
+#pragma unroll
+        for (int b = 0; b <= TM * TN; ++b) {
+          const int i = b % TM, j = b / TM;
+          const int ip = (b - 1) % TM, jp = (b - 1) / TM;  // the block folded in this round
+          if (b < TM * TN && i == 0 && j + 1 < TN) read_b(j + 1, (j + 1) & 1);
+          __builtin_amdgcn_sched_barrier(0);
+          if (b < TM * TN) part[b & 1] = mfma32x32x64_fp8(bq[j & 1][0], af[0][i], f32x16{});
+          if (b > 0) {
+            const float f = fa[ip] * sb[jp];
+#pragma unroll
+            for (int v = 0; v < 8; ++v) acc[ip][jp][v] = fmaf(part[(b - 1) & 1][v], f, acc[ip][jp][v]);
+          }
+          if (b < TM * TN) part[b & 1] = mfma32x32x64_fp8(bq[j & 1][1], af[1][i], part[b & 1]);
+          if (b > 0) {
+            const float f = fa[ip] * sb[jp];
+#pragma unroll
+            for (int v = 8; v < 16; ++v) acc[ip][jp][v] = fmaf(part[(b - 1) & 1][v], f, acc[ip][jp][v]);
+          }
           __builtin_amdgcn_sched_barrier(0);
         }
       } else if constexpr (FMT == 1) {
@@ -649,18 +761,30 @@ hipError_t launch_gemm2_bf16_tiled(const GroupedGemm& g, hipStream_t s) {
   return launch_tiled<0, false, MOE_TBF_BM, MOE_T2_BNW, MOE_T2_WM, MOE_T2_WN, MOE_TGM, MOE_TBF_KB, MOE_TBF_STAGES, MOE_TBF_NP2>(g, s);
 }
 
-// fp8 waves per workgroup as WM x WN over the 128 x 256 tile
+// fp8 over the 128 x 256 tile: with copy waves (NP > 0) four math waves
+// (2 x 2), else eight (MOE_F8_WM x MOE_F8_WN) that copy for themselves
 #ifndef MOE_F8_WM
 #define MOE_F8_WM 2
 #define MOE_F8_WN 4
 #endif
+#ifndef MOE_F8_NP1
+#define MOE_F8_NP1 4
+#endif
+#ifndef MOE_F8_NP2
+#define MOE_F8_NP2 4
+#endif
 int gemm_block_m_fp8(int, int, int) { return 128; }
+template <bool GEMM1, int BNW, int NP>
+hipError_t launch_fp8(const GroupedGemm& g, hipStream_t s) {
+  if constexpr (NP > 0) return launch_tiled<1, GEMM1, 128, BNW, 2, 2, MOE_TGM, 128, 3, NP>(g, s);
+  else return launch_tiled<1, GEMM1, 128, BNW, MOE_F8_WM, MOE_F8_WN, MOE_TGM>(g, s);
+}
 hipError_t launch_gemm1_fp8(const GroupedGemm& g, hipStream_t s) {
-  return launch_tiled<1, true, 128, 256, MOE_F8_WM, MOE_F8_WN, MOE_TGM>(g, s);
+  return launch_fp8<true, 256, MOE_F8_NP1>(g, s);
 }
 hipError_t launch_gemm2_fp8(const GroupedGemm& g, hipStream_t s) {
-  if (g.H % 256) return launch_tiled<1, false, 128, 128, MOE_F8_WM, MOE_F8_WN, MOE_TGM>(g, s);
-  return launch_tiled<1, false, 128, 256, MOE_F8_WM, MOE_F8_WN, MOE_TGM>(g, s);
+  if (g.H % 256) return launch_fp8<false, 128, MOE_F8_NP2>(g, s);
+  return launch_fp8<false, 256, MOE_F8_NP2>(g, s);
 }
 
 int gemm_block_m_int4(int, int, int) { return 64; }
