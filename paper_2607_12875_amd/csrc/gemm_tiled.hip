@@ -730,14 +730,14 @@ hipError_t launch_tiled(const GroupedGemm& g, hipStream_t s) {
 #ifndef MOE_TBF_STAGES
 #define MOE_TBF_STAGES 3
 #endif
-// Copy waves beside the math waves (0: the math waves copy).  GEMM1 gains
-// from them; the GEMM2 launches (short K loops, and for int4 a second
-// workgroup per CU that the extra waves' registers would evict) do not.
+// Copy waves beside the math waves (0: the math waves copy).  The int4
+// GEMM2 launch keeps its math waves copying: the extra waves' registers
+// would evict the second workgroup per CU it otherwise runs.
 #ifndef MOE_TBF_NP1
 #define MOE_TBF_NP1 4
 #endif
 #ifndef MOE_TBF_NP2
-#define MOE_TBF_NP2 0
+#define MOE_TBF_NP2 4
 #endif
 #ifndef MOE_TI4_NP1
 #define MOE_TI4_NP1 4
