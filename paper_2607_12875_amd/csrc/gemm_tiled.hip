@@ -457,17 +457,26 @@ __global__ __launch_bounds__((WM * WN + NP) * 64) void moe_gemm_tiled(GroupedGem
           const int ip = (b - 1) % TM, jp = (b - 1) / TM;  // the block folded in this round
           if (b < TM * TN && i == 0 && j + 1 < TN) read_b(j + 1, (j + 1) & 1);
           __builtin_amdgcn_sched_barrier(0);
+          const float f = b > 0 ? fa[ip] * sb[jp] : 0.f;
           if (b < TM * TN) part[b & 1] = mfma32x32x64_fp8(bq[j & 1][0], af[0][i], f32x16{});
           if (b > 0) {
-            const float f = fa[ip] * sb[jp];
 #pragma unroll
             for (int v = 0; v < 8; ++v) acc[ip][jp][v] = fmaf(part[(b - 1) & 1][v], f, acc[ip][jp][v]);
           }
           if (b < TM * TN) part[b & 1] = mfma32x32x64_fp8(bq[j & 1][1], af[1][i], part[b & 1]);
           if (b > 0) {
-            const float f = fa[ip] * sb[jp];
 #pragma unroll
             for (int v = 8; v < 16; ++v) acc[ip][jp][v] = fmaf(part[(b - 1) & 1][v], f, acc[ip][jp][v]);
+          }
+          // keep the order written: each MFMA, then eight fmas that run on the
+          // VALU while it executes (the compiler otherwise pairs the MFMAs and
+          // stalls the fmas behind the second one)
+          if (b > 0 && b < TM * TN) {
+            __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);  // the scale product
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
           }
           __builtin_amdgcn_sched_barrier(0);
         }
