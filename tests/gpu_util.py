@@ -36,6 +36,27 @@ def ws_view(ws, layout, name, dtype, count):
     return ws[off:off + nbytes].view(dtype)[:count].cpu().numpy()
 
 
+def check_forward(cfg, inp=None, out_dtype="f32"):
+    """Whole-layer parity against the oracle: ids, offsets, sorted ids and
+    inverse positions bit-exact, max|err| <= TOL * rms(oracle out)."""
+    from oracle import moe_oracle as O
+    print(f"forward parity {cfg}", flush=True)
+    inp = synth.make_inputs(cfg) if inp is None else inp
+    out, ws, L, _ = run_forward(cfg, inp, out_dtype)
+    ref = O.forward(cfg, inp)
+    n = cfg.T * cfg.top_k
+    ids = ws_view(ws, L, "topk_ids", torch.int32, n).reshape(cfg.T, cfg.top_k)
+    assert np.array_equal(ids, ref["ids"])
+    ro, rs, ri = O.permute(ref["ids"], cfg.E, L["block_m"])
+    assert np.array_equal(ws_view(ws, L, "expert_offsets", torch.int32, cfg.E + 1), ro)
+    assert np.array_equal(ws_view(ws, L, "sorted_ids", torch.int32, L["cap"]), rs)
+    assert np.array_equal(ws_view(ws, L, "inv_pos", torch.int32, n), ri)
+    err = rel_err(out, ref["out"])
+    print(f"  max|err|/rms = {err:.3e} (block_m={L['block_m']})", flush=True)
+    assert err <= TOL[cfg.wfmt]
+    return out, ref, L
+
+
 def rel_err(out, ref):
     rms = np.sqrt((ref ** 2).mean())
     return np.max(np.abs(out - ref)) / rms

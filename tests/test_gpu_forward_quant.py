@@ -73,9 +73,65 @@ def _check(cfg, inp=None, tokens=None):
     return err
 
 
+# gfx950's fp8 MFMA aligns the 64 products of one instruction with truncation
+# (65536 + 63 * 2^-6 comes back as 65536.875, not 65536.984), so the GPU's
+# intermediate before requantisation differs from the oracle's by ~1e-5
+# relative and an e4m3 code whose value sits on a rounding tie can land one
+# step away.  One such step moves an output by ~1/sqrt(I) of its rms, so the
+# output-level fp8 cases use I >= 1024 (the workload has I = 2048); the codes
+# themselves are pinned by test_fp8_intermediate_codes at small I.
 @pytest.mark.parametrize("T", [1, 33, 200, 700])
 def test_fp8_small(dev, T):
-    _check(synth.tiny_config(4, T=T, H=512, I=256, E=16, top_k=4))
+    _check(synth.tiny_config(4, T=T, H=512, I=1024, E=16, top_k=4))
+
+
+def _oracle_preq_intermediate(cfg, inp):
+    """The oracle's SwiGLU intermediate of every routed row, before its
+    requantisation, rounded once to fp32 (the precision the quantiser sees)."""
+    n = cfg.T * cfg.top_k
+    ids, _ = O.gate(inp["logits"], inp["sel_bias"], cfg.top_k, cfg.mode, cfg.renormalize, cfg.routed_scale)
+    x = O.activation_operand(inp["hidden"], cfg.wfmt, True)
+    flat = ids.reshape(-1)
+    a = np.zeros((n, cfg.I))
+    for e in np.unique(flat):
+        rows = np.nonzero(flat == e)[0]
+        w1 = O.dequant_weight(cfg.wfmt, inp["w1"][e], inp["w1_scale"][e])
+        w2 = O.dequant_weight(cfg.wfmt, inp["w2"][e], inp["w2_scale"][e])
+        a[rows] = O.swiglu_expert(x[rows // cfg.top_k], w1, w2, cfg.wfmt, mirror=False)[0]
+    return a.astype(np.float32)
+
+
+@pytest.mark.parametrize("shape", [dict(T=700, H=512, I=256, E=16, top_k=4),
+                                   dict(T=1500, H=384, I=384, E=8, top_k=2, logit_bias="zipf:6.0", sel_bias_std=0.0)])
+def test_fp8_intermediate_codes(dev, shape):
+    """The requantised intermediate GEMM1 writes (e4m3 codes + per (row, 128)
+    scales) against the oracle's quantiser applied to its own fp32
+    intermediate: scales within 2e-4 relative; every code the rounding of a
+    value within 2e-4 * 448 (in units of the scale) of the oracle's a/s --
+    exact away from rounding ties, at most the neighbouring code at a tie."""
+    cfg = synth.tiny_config(4, **shape)
+    inp = synth.make_inputs(cfg)
+    out, ws, L, _ = run_forward(cfg, inp)
+    n, I, cap = cfg.T * cfg.top_k, cfg.I, L["cap"]
+    sid = ws_view(ws, L, "sorted_ids", torch.int32, cap)
+    codes = ws_view(ws, L, "inter", torch.uint8, cap * I).reshape(cap, I)
+    scales = ws_view(ws, L, "inter_s", torch.float32, cap * (I // 128)).reshape(cap, I // 128)
+    rows = np.nonzero(sid < n)[0]
+    a32 = _oracle_preq_intermediate(cfg, inp)[sid[rows]]
+    qref, sref = O.act_quant_fp8(a32)
+    s_gpu = scales[rows]
+    assert np.all(np.abs(s_gpu.astype(np.float64) - sref) <= 2e-4 * sref)
+    x = a32.astype(np.float64) / np.repeat(sref, 128, axis=1).astype(np.float64)
+    slack = 2e-4 * O.E4M3_MAX
+    v_lo = O.e4m3_decode(O.e4m3_encode(x - slack))
+    v_hi = O.e4m3_decode(O.e4m3_encode(x + slack))
+    v_g = O.e4m3_decode(codes[rows])
+    ok = (v_g >= v_lo) & (v_g <= v_hi)
+    bad = np.argwhere(~ok)
+    assert bad.size == 0, (bad[:3], x[tuple(bad[0])], v_g[tuple(bad[0])], v_lo[tuple(bad[0])], v_hi[tuple(bad[0])])
+    ties = int((codes[rows] != qref).sum())
+    print(f"  {ties} of {qref.size} codes one tie away from the oracle's", flush=True)
+    assert ties <= 0.01 * qref.size
 
 
 def test_fp8_h_not_multiple_of_256(dev):
