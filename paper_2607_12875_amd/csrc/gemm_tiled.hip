@@ -796,13 +796,18 @@ hipError_t launch_gemm2_fp8(const GroupedGemm& g, hipStream_t s) {
   return launch_fp8<false, 256, MOE_F8_NP2>(g, s);
 }
 
-int gemm_block_m_int4(int, int, int) { return 64; }
+// int4 row tile: one math wave per 64 columns covers all MOE_TI4_BM rows, so
+// each decoded weight fragment feeds MOE_TI4_BM / 32 MFMAs
+#ifndef MOE_TI4_BM
+#define MOE_TI4_BM 64
+#endif
+int gemm_block_m_int4(int, int, int) { return MOE_TI4_BM; }
 hipError_t launch_gemm1_int4(const GroupedGemm& g, hipStream_t s) {
-  return launch_tiled<2, true, 64, 256, 1, 4, MOE_TGM_INT4, 128, 3, MOE_TI4_NP1>(g, s);
+  return launch_tiled<2, true, MOE_TI4_BM, 256, 1, 4, MOE_TGM_INT4, 128, 3, MOE_TI4_NP1>(g, s);
 }
 hipError_t launch_gemm2_int4(const GroupedGemm& g, hipStream_t s) {
-  if (g.H % 256) return launch_tiled<2, false, 64, 128, 1, 4, MOE_TGM_INT4, 128, 3, MOE_TI4_NP2>(g, s);
-  return launch_tiled<2, false, 64, 256, 1, 4, MOE_TGM_INT4, 128, 3, MOE_TI4_NP2>(g, s);
+  if (g.H % 256) return launch_tiled<2, false, MOE_TI4_BM, 128, 1, 4, MOE_TGM_INT4, 128, 3, MOE_TI4_NP2>(g, s);
+  return launch_tiled<2, false, MOE_TI4_BM, 256, 1, 4, MOE_TGM_INT4, 128, 3, MOE_TI4_NP2>(g, s);
 }
 
 }  // namespace moe
