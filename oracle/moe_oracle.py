@@ -27,8 +27,10 @@ bincount, matmul, exp) and no blocking or fusion:
   combine   out[t] = sum_j w[t,j] * y[t,j].
 
 Quantisation points the kernels take are mirrored (``mirror=True``):
-  * bf16 / int4 weights: the intermediate ``a`` is rounded to fp32, then to
-    bf16 (round to nearest even) before the second product;
+  * bf16 / int4 weights, and fp8 weights with bf16 activations ("fp8a16",
+    the weight-only fp8 route): the intermediate ``a`` is rounded to fp32,
+    then to bf16 (round to nearest even) before the second product; the
+    hidden rows enter exactly;
   * fp8: the hidden rows and the intermediate ``a`` are each quantised per
     (row, 128-column group): s = fp32(max(amax, 1e-10) / 448) with an IEEE
     fp32 divide, q = e4m3fn(RNE(fp32(x / s))) saturated to +-448, and the
@@ -128,7 +130,7 @@ def dequant_weight(wfmt: str, w: np.ndarray, scale) -> np.ndarray:
     """One expert's stored weight [N, K] (+ scales) -> exact float64 values."""
     if wfmt == "bf16":
         return bf16_to_f64(w)
-    if wfmt == "fp8":
+    if wfmt in ("fp8", "fp8a16"):                       # same storage, same values
         q = e4m3_decode(w)                                  # [N, K]
         N, K = q.shape
         s = np.asarray(scale, dtype=np.float64)            # [N/128, K/128]

@@ -12,7 +12,7 @@ The layer is the MoE Gate -> Fused MoE -> Weight Sum skeleton of the paper
 semantics explicitly (e4m3 format, scale granularity, zero points, layout),
 as Sec. 6.2 and the "FP8 representation" row of Table 3 require.
 
-Value recipe (the five workloads):
+Value recipe (the five workloads, plus a decode step on fp8 weights):
   * hidden  ~ N(0, 1) drawn in fp32, stored as bf16 (round-to-nearest-even).
   * logits  ~ N(0, 1) fp32, plus an optional per-expert bias:
       - "normal:<std>"  b_e ~ N(0, std^2), added to the logits (uneven loads);
@@ -61,7 +61,7 @@ class MoeConfig:
     E: int
     I: int
     top_k: int
-    wfmt: str = "bf16"          # "bf16" | "fp8" | "int4"
+    wfmt: str = "bf16"          # "bf16" | "fp8" | "int4" | "fp8a16" (fp8 storage, bf16 activations)
     mode: str = "softmax"       # "softmax" | "sigmoid"
     renormalize: bool = True
     routed_scale: float = 1.0
@@ -87,6 +87,10 @@ CONFIGS = {
                  mode="sigmoid", routed_scale=2.5, sel_bias_std=0.1, seed=4),
     5: MoeConfig("int4", T=512, H=4096, E=128, I=1536, top_k=8, wfmt="int4",
                  logit_bias="zipf:1.1", seed=5),
+    # one decode step of workload 4's layer on its fp8 weights, activations
+    # kept bf16 (the weight-only fp8 route)
+    6: MoeConfig("fp8-decode", T=16, H=7168, E=256, I=2048, top_k=8, wfmt="fp8a16",
+                 mode="sigmoid", routed_scale=2.5, sel_bias_std=0.1, seed=6),
 }
 
 
@@ -100,7 +104,7 @@ def tiny_config(n: int, **overrides) -> MoeConfig:
     kernels still see several tiles and a ragged tail."""
     base = CONFIGS[n]
     small = dict(T=77, H=384, E=8, I=256, top_k=min(base.top_k, 3))
-    if base.wfmt == "fp8":
+    if base.wfmt in ("fp8", "fp8a16"):
         small.update(E=16, top_k=4)
     if base.wfmt == "int4":
         small.update(E=12, top_k=4)
@@ -197,7 +201,7 @@ def _int4_group_quant(w: np.ndarray):
 def _weight_arrays(cfg: MoeConfig, N: int, K: int, n_exp: int):
     if cfg.wfmt == "bf16":
         return np.empty((n_exp, N, K), np.uint16), None
-    if cfg.wfmt == "fp8":
+    if cfg.wfmt in ("fp8", "fp8a16"):
         return np.empty((n_exp, N, K), np.uint8), np.empty((n_exp, N // 128, K // 128), np.float32)
     if cfg.wfmt == "int4":
         return np.empty((n_exp, N, K // 8), np.int32), np.empty((n_exp, N, K // 128), np.uint16)
@@ -210,7 +214,7 @@ def make_expert_weights(cfg: MoeConfig, experts=None, threads=None, identical_ex
     stream (a test fixture: all experts then hold the same weights)."""
     experts = list(range(cfg.E)) if experts is None else list(experts)
     H, I = cfg.H, cfg.I
-    if cfg.wfmt in ("fp8", "int4") and (H % 128 or I % 128):
+    if cfg.wfmt != "bf16" and (H % 128 or I % 128):
         raise ValueError("fp8/int4 storage needs H and I to be multiples of 128")
     w1, w1s = _weight_arrays(cfg, 2 * I, H, len(experts))
     w2, w2s = _weight_arrays(cfg, H, I, len(experts))
@@ -218,7 +222,7 @@ def make_expert_weights(cfg: MoeConfig, experts=None, threads=None, identical_ex
     def encode(dst, dst_s, slot, w):
         if cfg.wfmt == "bf16":
             dst[slot] = _bf16_bits(w)
-        elif cfg.wfmt == "fp8":
+        elif cfg.wfmt in ("fp8", "fp8a16"):
             dst[slot], dst_s[slot] = _fp8_block_quant(w)
         else:
             dst[slot], dst_s[slot] = _int4_group_quant(w)

@@ -72,7 +72,28 @@ def test_single_expert_top1_is_dense_swiglu(mirror):
     assert np.all(r["w"] == 1.0)
 
 
-@pytest.mark.parametrize("n", [1, 4, 5])
+@pytest.mark.parametrize("mirror", [False, True])
+def test_fp8_weights_bf16_activations_single_expert(mirror):
+    # the weight-only fp8 route: E = 1, k = 1 is a dense SwiGLU on the exactly
+    # dequantised fp8 weights with the hidden rows unquantised -- operands
+    # built here with torch's own float8_e4m3fn decode
+    cfg = synth.MoeConfig("dense8", T=33, H=256, E=1, I=128, top_k=1, wfmt="fp8a16", seed=12)
+    inp = synth.make_inputs(cfg)
+    r = O.forward(cfg, inp, mirror=mirror)
+
+    def deq(codes, s):
+        q = torch.from_numpy(np.ascontiguousarray(codes)).view(torch.float8_e4m3fn).to(torch.float64)
+        sc = torch.from_numpy(s).to(torch.float64).repeat_interleave(128, 0).repeat_interleave(128, 1)
+        return (q * sc).numpy()
+
+    x = torch.from_numpy(inp["hidden"].view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    ref = _dense_torch(x, deq(inp["w1"][0], inp["w1_scale"][0]), deq(inp["w2"][0], inp["w2_scale"][0]), mirror)
+    rms = np.sqrt((ref ** 2).mean())
+    tol = 1e-12 if not mirror else 2 ** -8
+    assert np.max(np.abs(r["out"] - ref)) <= tol * rms
+
+
+@pytest.mark.parametrize("n", [1, 4, 5, 6])
 def test_identical_experts_any_routing(n):
     cfg = synth.tiny_config(n)
     inp = synth.make_inputs(cfg, identical_experts=True)
@@ -83,7 +104,7 @@ def test_identical_experts_any_routing(n):
     assert np.max(np.abs(r["out"] - ref)) <= 1e-12 * np.sqrt((ref ** 2).mean())
 
 
-@pytest.mark.parametrize("n", [1, 4, 5])
+@pytest.mark.parametrize("n", [1, 4, 5, 6])
 def test_token_order_invariance(n):
     cfg = synth.tiny_config(n)
     inp = synth.make_inputs(cfg)
@@ -135,7 +156,7 @@ def _brute_layer(cfg, inp, mirror):
     return np.array(outs)
 
 
-@pytest.mark.parametrize("n", [1, 4, 5])
+@pytest.mark.parametrize("n", [1, 4, 5, 6])
 @pytest.mark.parametrize("mirror", [False, True])
 def test_brute_force_tiny(n, mirror):
     cfg = synth.tiny_config(n, T=9, H=256, I=128, E=6, top_k=3)
