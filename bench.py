@@ -7,7 +7,7 @@ weighted combine) on one MI355X.
 One step is one ``moe_forward`` call over one batch of synthetic inputs that
 are already resident in HBM.  The default workload is the decode-shaped layer
 (T=16, H=4096, E=64, I=1408, top_k=6, bf16 weights); ``--config`` selects one
-of the other four workloads for exploration.  Prints ONE JSON line on stdout.
+of the other workloads for exploration.  Prints ONE JSON line on stdout.
 
 Timing:
   * whole layer: HIP events on the launch stream around exactly K calls,
@@ -40,7 +40,7 @@ sys.path.insert(0, ROOT)
 METRIC = "fused-MoE layer TFLOP/s (active FLOPs) + µs/layer; fraction of MFMA/HBM peak"
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0}
-W_BYTES = {"bf16": 2.0, "fp8": 1.0, "int4": 0.5}
+W_BYTES = {"bf16": 2.0, "fp8": 1.0, "int4": 0.5, "fp8a16": 1.0}
 DESCR = {
     1: "tiny MoE layer: T=64 H=256 E=8 I=128 top_k=2, bf16 weights, softmax top-2 renormalised",
     2: "decode-shaped MoE layer: T=16 H=4096 E=64 I=1408 top_k=6, bf16 weights, softmax top-6 renormalised",
@@ -49,6 +49,8 @@ DESCR = {
        "per-(token,128) e4m3 activations, sigmoid+bias top-8 x2.5",
     5: "int4 weight-only MoE layer: T=512 H=4096 E=128 I=1536 top_k=8, int4 g128 weights, "
        "Zipf(1.1)-skewed softmax top-8",
+    6: "weight-only fp8 decode MoE layer: T=16 H=7168 E=256 I=2048 top_k=8, e4m3 128x128 weights, "
+       "bf16 activations, sigmoid+bias top-8 x2.5",
 }
 
 
@@ -114,8 +116,10 @@ def cpu_baseline(cfg, inputs, budget_s: float):
         cores = 1
     tokens = None
     n_tok = cfg.T
-    if cfg.T * cfg.top_k * cfg.H * cfg.I * 6 > 2e12:          # fp8 workload: sample tokens
-        n_tok = 8
+    # the oracle dequantises every expert a token routes to: bound that work
+    per_token = cfg.top_k * 3.0 * cfg.H * cfg.I
+    if cfg.T * per_token > 2e9:
+        n_tok = max(1, min(cfg.T, int(2e9 / per_token)))
         tokens = np.linspace(0, cfg.T - 1, n_tok).astype(np.int64)
     reps, t0 = 0, time.perf_counter()
     while True:
@@ -168,7 +172,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=2, choices=sorted(DESCR))
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="host-time budget of the oracle baseline (0 disables it)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -264,8 +268,9 @@ def main():
     H, I, T, n = cfg.H, cfg.I, cfg.T, cfg.n_routed
     # GEMM1 per launch: W1 of every active expert (+ its scales), hidden read
     # once, the SwiGLU intermediate written once
-    w1_scale_bytes = {"bf16": 0, "fp8": 2 * I * H / (128 * 128) * 4, "int4": 2 * I * H / 128 * 2}[cfg.wfmt]
-    act_bytes = {"bf16": 2, "fp8": 1, "int4": 2}[cfg.wfmt]
+    w1_scale_bytes = {"bf16": 0, "fp8": 2 * I * H / (128 * 128) * 4, "int4": 2 * I * H / 128 * 2,
+                      "fp8a16": 2 * I * H / (128 * 128) * 4}[cfg.wfmt]
+    act_bytes = {"bf16": 2, "fp8": 1, "int4": 2, "fp8a16": 2}[cfg.wfmt]
     g1_bytes = n_active * (2 * I * H * wb + w1_scale_bytes) + T * H * (1 if cfg.wfmt == "fp8" else 2) + n * I * act_bytes
     g1_flops = 2.0 * n * H * 2 * I
     g1_us = float(np.mean(g1_launch_us))
@@ -293,7 +298,7 @@ def main():
     if args.cpu_seconds > 0:
         base = cpu_baseline(cfg, inputs, args.cpu_seconds)
 
-    dtype = {"bf16": "bf16", "fp8": "fp8e4m3", "int4": "bf16"}[cfg.wfmt]
+    dtype = {"bf16": "bf16", "fp8": "fp8e4m3", "int4": "bf16", "fp8a16": "bf16"}[cfg.wfmt]
     rec = {
         "metric": METRIC,
         "value": flops / (ms * 1e-3) / 1e12,

@@ -74,7 +74,15 @@ typedef enum {
      k = 8w+j sits in bits [4j,4j+4) of word w (low nibble first):
      w[e][n][K/8] (int32_t); bf16 scale per 128 along K: scale[e][n][k/128];
      value = q * scale. */
-  MOE_W_INT4_G128 = 2
+  MOE_W_INT4_G128 = 2,
+  /* Weight-only fp8 (a decode route): the MOE_W_FP8E4M3_B128 storage and
+     scales, but the hidden rows enter unquantised (bf16) and the SwiGLU
+     intermediate is rounded to bf16 as with MOE_W_BF16; the weights are
+     decoded to bf16 in registers (exact) and each 128-wide K block's partial
+     sum is scaled by its block scale.  Requires T * top_k <= 32 * E (at most
+     32 routed rows per expert on average), else MOE_ERR_UNSUPPORTED: larger
+     batches take MOE_W_FP8E4M3_B128. */
+  MOE_W_FP8E4M3_B128_A16 = 3
 } moe_wfmt;
 
 typedef enum { MOE_OUT_F32 = 0, MOE_OUT_BF16 = 1 } moe_ofmt;
@@ -168,8 +176,8 @@ typedef struct moe_ws_layout {
   int64_t sorted_ids, inv_pos;       /* int32 [cap], int32 [T*top_k]             */
   int64_t act_q, act_s;              /* fp8: uint8 [T,H], fp32 [T,H/128]         */
   int64_t inter, inter_s;            /* bf16 [cap,I] (fp8: uint8 [cap,I], fp32 [cap,I/128]) */
-  int64_t y;                         /* [cap,H] rows in sorted order: fp32 for bf16
-                                        weights, bf16 for fp8 / int4; pad rows unspecified */
+  int64_t y;                         /* [cap,H] rows in sorted order: bf16 for
+                                        MOE_W_FP8E4M3_B128, fp32 otherwise; pad rows unspecified */
   int64_t permute_ws;                /* moe_permute scratch                      */
   int32_t block_m, cap;              /* padding granule and sorted_ids length   */
   int64_t total;                     /* == moe_workspace_bytes                  */
@@ -186,6 +194,7 @@ moe_status moe_workspace_layout(const moe_args* a, moe_ws_layout* layout);
  * aligned; ws_bytes >= moe_workspace_bytes(a); sel_bias only with a format
  * that reads it (both scoring modes do).  Padding rows of the intermediates
  * are unspecified.  T == 0 is a no-op.
+ * MOE_W_FP8E4M3_B128_A16 additionally needs T * top_k <= 32 * E.
  * Errors: MOE_ERR_NULL, MOE_ERR_SHAPE, MOE_ERR_UNSUPPORTED, MOE_ERR_ALIGN,
  * MOE_ERR_WORKSPACE, MOE_ERR_HIP.
  */

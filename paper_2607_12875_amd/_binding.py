@@ -19,7 +19,7 @@ MOE_ERR_NULL, MOE_ERR_SHAPE, MOE_ERR_UNSUPPORTED, MOE_ERR_ALIGN, MOE_ERR_WORKSPA
 STATUS_NAMES = {0: "MOE_OK", 1: "MOE_ERR_NULL", 2: "MOE_ERR_SHAPE", 3: "MOE_ERR_UNSUPPORTED",
                 4: "MOE_ERR_ALIGN", 5: "MOE_ERR_WORKSPACE", 6: "MOE_ERR_HIP"}
 SCORE = {"softmax": 0, "sigmoid": 1}
-WFMT = {"bf16": 0, "fp8": 1, "int4": 2}
+WFMT = {"bf16": 0, "fp8": 1, "int4": 2, "fp8a16": 3}
 OFMT = {"f32": 0, "bf16": 1}
 
 EXPORTED = ("moe_status_str", "moe_permute_capacity", "moe_permute_workspace_bytes",
@@ -205,7 +205,8 @@ def moe_forward(hidden, logits, w1, w2, top_k, *, mode="softmax", renormalize=Tr
     hidden bf16 [T,H]; logits fp32 [T,E]; weights in the wfmt storage:
     bf16 [E,2I,H] / [E,H,I]; fp8 uint8 codes with fp32 block scales
     [E,2I/128,H/128] / [E,H/128,I/128]; int4 int32 [E,2I,H/8] / [E,H,I/8] with
-    bf16 scales [E,2I,H/128] / [E,H,I/128]."""
+    bf16 scales [E,2I,H/128] / [E,H,I/128]; "fp8a16" (weight-only fp8, a decode
+    route) takes the fp8 storage with bf16 activations."""
     _dev(hidden, logits, w1, w2, sel_bias, w1_scale, w2_scale, out, topk_ids_out, topk_w_out)
     T, H = hidden.shape
     E = logits.shape[1]

@@ -135,6 +135,138 @@ __global__ __launch_bounds__(256) void gemm_bf16_skinny(GroupedGemm g) {
   }
 }
 
+// ------------------------------------------------- skinny, weight-only fp8
+// The decode kernel on fp8 weights with bf16 activations: the same 16-row
+// tile and reduction, the K range split over the four waves in 128-wide
+// blocks (the weight scale granule).  Per block a lane reads 64 contiguous
+// bytes of its activation row and 32 bytes of each weight row: within the
+// block, MFMA u takes K elements [32 kg + 8 u, +8) for lane group kg (one K
+// permutation, applied to both operands).  The e4m3 codes decode exactly to
+// bf16 (v_cvt_pk_f32_fp8); the block's partial is scaled by the block's
+// fp32 scale and added to the accumulator.  The loads of block b+1 are in
+// flight while block b computes.
+__device__ __forceinline__ bf16x8 e4m3x8_to_bf16(uint32_t lo, uint32_t hi) {
+  bf16x8 r;
+  const auto f0 = __builtin_amdgcn_cvt_pk_f32_fp8(lo, false), f1 = __builtin_amdgcn_cvt_pk_f32_fp8(lo, true);
+  const auto f2 = __builtin_amdgcn_cvt_pk_f32_fp8(hi, false), f3 = __builtin_amdgcn_cvt_pk_f32_fp8(hi, true);
+  r[0] = static_cast<__bf16>(f0[0]); r[1] = static_cast<__bf16>(f0[1]);  // exact: e4m3 fits bf16
+  r[2] = static_cast<__bf16>(f1[0]); r[3] = static_cast<__bf16>(f1[1]);
+  r[4] = static_cast<__bf16>(f2[0]); r[5] = static_cast<__bf16>(f2[1]);
+  r[6] = static_cast<__bf16>(f3[0]); r[7] = static_cast<__bf16>(f3[1]);
+  return r;
+}
+
+template <int NSUB, bool GEMM1>
+__global__ __launch_bounds__(256) void gemm_w8a16_skinny(GroupedGemm g) {
+  constexpr int BM = 16;
+  constexpr int BN = GEMM1 ? NSUB / 2 * 16 : NSUB * 16;
+  __shared__ f32x4 red[3][NSUB][64];
+
+  const int m0 = blockIdx.y * BM;
+  if (m0 >= g.offsets[g.E]) return;
+  const int e = find_segment(g.offsets, g.E, m0);
+  const int n0 = blockIdx.x * BN;
+  const int K = GEMM1 ? g.H : g.I;
+  const int NR = GEMM1 ? 2 * g.I : g.H;  // weight rows of one expert
+  const int lane = lane_id(), wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+
+  const uint16_t* arow;
+  if (GEMM1) {
+    const int sid = g.sorted_ids[m0 + r16];
+    const int tok = sid < g.n_routed ? sid / g.top_k : 0;
+    arow = static_cast<const uint16_t*>(g.x) + static_cast<size_t>(tok) * g.H;
+  } else {
+    arow = static_cast<const uint16_t*>(g.inter) + static_cast<size_t>(m0 + r16) * g.I;
+  }
+  arow += kg * 32;
+  const uint8_t* wbase = static_cast<const uint8_t*>(GEMM1 ? g.w1 : g.w2) + static_cast<size_t>(e) * NR * K;
+  const float* sbase = static_cast<const float*>(GEMM1 ? g.w1_scale : g.w2_scale) +
+                       static_cast<size_t>(e) * (NR / 128) * (K / 128);
+  const uint8_t* brow[NSUB];
+  const float* srow[NSUB];  // the subtile's 16 weight rows share one 128-row scale block
+#pragma unroll
+  for (int s = 0; s < NSUB; ++s) {
+    int nf;  // first weight row of subtile s
+    if (GEMM1) nf = s < NSUB / 2 ? n0 + s * 16 : g.I + n0 + (s - NSUB / 2) * 16;
+    else nf = n0 + s * 16;
+    brow[s] = wbase + static_cast<size_t>(nf + r16) * K + kg * 32;
+    srow[s] = sbase + static_cast<size_t>(nf / 128) * (K / 128);
+  }
+
+  f32x4 acc[NSUB];
+#pragma unroll
+  for (int s = 0; s < NSUB; ++s) acc[s] = f32x4{};
+  const int nb = K / 128, lb = nb / 4, lr = nb % 4;
+  const int bbeg = wave * lb + min(wave, lr);
+  const int bend = bbeg + lb + (wave < lr ? 1 : 0);
+
+  u32x4 a0[4], b0[NSUB][2], a1[4], b1[NSUB][2];
+#define MOE_W8_LOAD(A, Bv, blk)                                                                   \
+  do {                                                                                            \
+    _Pragma("unroll") for (int u = 0; u < 4; ++u) A[u] = ld16(arow + (blk) * 128 + u * 8);       \
+    _Pragma("unroll") for (int s = 0; s < NSUB; ++s) {                                          \
+      Bv[s][0] = ld16(brow[s] + (blk) * 128);                                                    \
+      Bv[s][1] = ld16(brow[s] + (blk) * 128 + 16);                                               \
+    }                                                                                             \
+  } while (0)
+#define MOE_W8_MMA(A, Bv, blk)                                                                    \
+  do {                                                                                            \
+    _Pragma("unroll") for (int s = 0; s < NSUB; ++s) {                                          \
+      f32x4 part = {};                                                                            \
+      _Pragma("unroll") for (int u = 0; u < 4; ++u) {                                           \
+        const u32x4& w = Bv[s][u >> 1];                                                           \
+        const bf16x8 b = (u & 1) ? e4m3x8_to_bf16(w.z, w.w) : e4m3x8_to_bf16(w.x, w.y);          \
+        part = mfma16x16x32(as_bf16x8(A[u]), b, part);                                           \
+      }                                                                                           \
+      acc[s] += part * srow[s][blk];                                                              \
+    }                                                                                             \
+  } while (0)
+  int b = bbeg;
+  if (b < bend) MOE_W8_LOAD(a0, b0, b);
+  for (; b + 1 < bend; b += 2) {
+    MOE_W8_LOAD(a1, b1, b + 1);
+    MOE_W8_MMA(a0, b0, b);
+    if (b + 2 < bend) MOE_W8_LOAD(a0, b0, b + 2);
+    MOE_W8_MMA(a1, b1, b + 1);
+  }
+  if (b < bend) MOE_W8_MMA(a0, b0, b);
+#undef MOE_W8_LOAD
+#undef MOE_W8_MMA
+
+  if (wave > 0) {
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s) red[wave - 1][s][lane] = acc[s];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int s = 0; s < NSUB; ++s)
+#pragma unroll
+    for (int w = 0; w < 3; ++w) acc[s] += red[w][s][lane];
+
+  // D element i of a 16x16 tile is (row 4*(lane/16) + i, col lane%16)
+  if (GEMM1) {
+#pragma unroll
+    for (int s = 0; s < NSUB / 2; ++s)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = m0 + 4 * kg + i, col = n0 + s * 16 + r16;
+        static_cast<uint16_t*>(g.inter)[static_cast<size_t>(row) * g.I + col] =
+            f32_to_bf16(silu_mul(acc[s][i], acc[s + NSUB / 2][i]));
+      }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = m0 + 4 * kg + i;
+      if (g.sorted_ids[row] >= g.n_routed) continue;  // pad rows are never read
+#pragma unroll
+      for (int s = 0; s < NSUB; ++s)
+        static_cast<float*>(g.y)[static_cast<size_t>(row) * g.H + n0 + s * 16 + r16] = acc[s][i];
+    }
+  }
+}
+
 // ----------------------------------------------------------------- dispatch
 bool bf16_use_skinny(int T, int top_k, int E) {
   return static_cast<long>(T) * top_k <= 32L * E;  // <= 32 rows per expert on average
@@ -173,6 +305,23 @@ hipError_t launch_gemm2_bf16(const GroupedGemm& g, hipStream_t s) {
     return hipGetLastError();
   }
   return launch_gemm2_bf16_tiled(g, s);
+}
+
+// Weight-only fp8 (decode route; the host guarantees T*k <= 32*E).
+#ifndef MOE_W8_NSUB
+#define MOE_W8_NSUB 4
+#endif
+hipError_t launch_gemm1_w8a16(const GroupedGemm& g, hipStream_t s) {
+  constexpr int NS = MOE_W8_NSUB;
+  const dim3 grid(g.I / (NS / 2 * 16), g.max_rows / 16);
+  hipLaunchKernelGGL((gemm_w8a16_skinny<NS, true>), grid, dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+hipError_t launch_gemm2_w8a16(const GroupedGemm& g, hipStream_t s) {
+  constexpr int NS = MOE_W8_NSUB;
+  const dim3 grid(g.H / (NS * 16), g.max_rows / 16);
+  hipLaunchKernelGGL((gemm_w8a16_skinny<NS, false>), grid, dim3(256), 0, s, g);
+  return hipGetLastError();
 }
 
 int gemm_block_m_bf16(int T, int top_k, int E) {

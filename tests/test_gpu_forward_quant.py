@@ -169,3 +169,51 @@ def test_quant_run_twice_bit_identical(dev):
         a, ws, _, _ = run_forward(cfg, inp)
         b, _, _, _ = run_forward(cfg, inp, workspace=ws)
         assert np.array_equal(a, b)
+
+
+def _scale_blocks(inp, wfmt, seed=1):
+    """Multiply every stored weight scale by its own power of two in
+    [2^-3, 2^3] (exact in fp32 and bf16).  The inputs stay valid and the
+    oracle reads the same tensors, but a scale applied to the wrong K block or
+    row block now moves the outputs far beyond the tolerance."""
+    rng = np.random.default_rng(seed)
+    out = dict(inp)
+    for k in ("w1_scale", "w2_scale"):
+        f = 2.0 ** rng.integers(-3, 4, size=inp[k].shape)
+        if wfmt == "int4":      # bf16 bits
+            out[k] = O.f32_to_bf16_rne((O.bf16_to_f64(inp[k]) * f).astype(np.float32))
+        else:                   # fp32
+            out[k] = (inp[k] * f).astype(np.float32)
+    return out
+
+
+@pytest.mark.parametrize("wcfg", [4, 5, 6])
+def test_block_scales_vary(dev, wcfg):
+    cfg = synth.tiny_config(wcfg, T=100, H=512, I=1024 if wcfg == 4 else 256, E=8, top_k=2)
+    _check(cfg, inp=_scale_blocks(synth.make_inputs(cfg), cfg.wfmt))
+
+
+# ---- weight-only fp8: e4m3 weights with their block scales, bf16 activations
+@pytest.mark.parametrize("T", [1, 5, 16, 33, 128])
+def test_w8a16_small(dev, T):
+    # T = 128: T * top_k = 512 = 32 * E, the largest batch the route accepts
+    _check(synth.tiny_config(6, T=T, H=512, I=256, E=16, top_k=4))
+
+
+def test_w8a16_ragged_k(dev):
+    # H = I = 384: three 128-wide K blocks over four waves (one wave idle);
+    # H = I = 128: a single block
+    _check(synth.tiny_config(6, T=40, H=384, I=384, E=8, top_k=3))
+    _check(synth.tiny_config(6, T=60, H=128, I=128, E=4, top_k=2))
+
+
+def test_w8a16_workload_full_size_sampled(dev):
+    _check(synth.config(6), tokens=np.array([0, 5, 11, 15]))
+
+
+def test_w8a16_large_batch_rejected(dev):
+    cfg = synth.tiny_config(6, T=129, H=256, I=128, E=16, top_k=4)   # T*k = 516 > 32*E
+    inp = synth.make_inputs(cfg)
+    with pytest.raises(moe.MoeError) as ei:
+        run_forward(cfg, inp)
+    assert ei.value.status == 3   # MOE_ERR_UNSUPPORTED
