@@ -14,6 +14,7 @@
 // tiles past the last segment exit at once.
 #include "common.hpp"
 #include "launch.hpp"
+#include "lds_dma.hpp"
 
 namespace moe {
 
@@ -131,6 +132,130 @@ __global__ __launch_bounds__(256) void gemm_bf16_skinny(GroupedGemm g) {
 #pragma unroll
       for (int s = 0; s < NSUB; ++s)
         static_cast<float*>(g.y)[static_cast<size_t>(row) * g.H + n0 + s * 16 + r16] = acc[s][i];
+    }
+  }
+}
+
+// ------------------------------------------------------ streamed (decode)
+// The decode GEMMs read every weight byte once, so they are bound by how
+// fast HBM delivers the weight slab.  The skinny kernel above walks 16 rows
+// per load instruction (64 bytes of each, at the row stride); this one reads
+// the slab the way HBM streams best: the four waves split K in quarters and
+// the workgroup walks its weight rows in order, each row's quarters read
+// together, with non-temporal direct-to-LDS copies of 512 bytes of one row
+// per instruction (measured on the MI355X: 7.3 TB/s for this pattern,
+// against 6.2 TB/s for loads that walk 16 rows at a time).  Stage (group gi,
+// piece p) holds 16 rows x 512 bytes of the wave's quarter; two stages per
+// wave are in flight, and two workgroups fit a CU.  The activation fragments
+// of the wave's K quarter (NP pieces: K = 1024 NP) are loaded once and stay
+// in registers.  Each stage row sits at a stride of 528 bytes, so the 16
+// rows of a fragment read fall in distinct LDS bank groups.
+// NG: 16-row weight groups per workgroup (GEMM1: NG/2 gate + NG/2 up).
+template <int NG, int NP, bool GEMM1>
+__global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
+  constexpr int PC = 512;
+  constexpr int ROWB = PC + 16, STAGE = 16 * ROWB;
+  constexpr int JP = PC / 64;   // MFMAs (32 K elements each) per piece
+  constexpr int NJ = NP * JP;   // MFMA slots over the quarter
+  constexpr int NC = GEMM1 ? NG / 2 * 16 : NG * 16;
+  constexpr int NST = NG * NP;  // stages per tile
+  static_assert(4 * NG * 64 * 16 <= 4 * 2 * STAGE, "the reduction fits in the stage buffers");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[4][2][STAGE];
+
+  const int m0 = blockIdx.y * 16;
+  if (m0 >= g.offsets[g.E]) return;
+  const int e = find_segment(g.offsets, g.E, m0);
+  const int n0 = blockIdx.x * NC;
+  const int K = GEMM1 ? g.H : g.I;
+  const int lane = lane_id(), wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+  constexpr int qe = NP * PC / 2;  // this wave's K elements of each row (K = 4 qe)
+  const int k0 = wave * qe;
+
+  // A fragments: MFMA j covers K [k0 + 32 j, +32), lane group kg its
+  // elements [8 kg, 8 kg + 8); the B fragments use the same K order.  All
+  // of them have landed before the first weight copy is issued, so the
+  // compiler's own wait counts never cover a copy.
+  const uint16_t* arow;
+  if (GEMM1) {
+    const int sid = g.sorted_ids[m0 + r16];
+    const int tok = sid < g.n_routed ? sid / g.top_k : 0;
+    arow = static_cast<const uint16_t*>(g.x) + static_cast<size_t>(tok) * g.H;
+  } else {
+    arow = static_cast<const uint16_t*>(g.inter) + static_cast<size_t>(m0 + r16) * g.I;
+  }
+  arow += k0 + 8 * kg;
+  u32x4 a[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) a[j] = ld16(arow + 32 * j);
+  vm_wait<0>();
+
+  const size_t rowbytes = static_cast<size_t>(K) * 2;
+  const uint8_t* wq = static_cast<const uint8_t*>(GEMM1 ? g.w1 : g.w2) +
+                      static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) * rowbytes + 2 * static_cast<size_t>(k0) +
+                      16 * lane;
+  const uint32_t sbase = lds_addr(&smem[wave][0][0]);
+  // stage s = gi * NP + p: rows of group gi, bytes [p*PC, (p+1)*PC) of the quarter
+  auto issue = [&](int s) {
+    const int gi = s / NP, p = s % NP;
+    const int wr = GEMM1 ? (gi < NG / 2 ? n0 + gi * 16 : g.I + n0 + (gi - NG / 2) * 16) : n0 + gi * 16;
+    const uint8_t* src = wq + static_cast<size_t>(wr) * rowbytes + p * PC;
+    const uint32_t dst = sbase + (s & 1) * STAGE;
+    if (16 * lane < PC) {  // 32 lanes x 16 bytes per row
+#pragma unroll
+      for (int i = 0; i < 16; ++i) dma16_nt(src + i * rowbytes, dst + i * ROWB);
+    }
+  };
+
+  f32x4 acc[NG];
+#pragma unroll
+  for (int gi = 0; gi < NG; ++gi) acc[gi] = f32x4{};
+  issue(0);
+  if (NST > 1) issue(1);
+#pragma unroll
+  for (int s = 0; s < NST; ++s) {
+    const int gi = s / NP, p = s % NP;
+    if (s + 1 < NST) vm_wait<16>();  // stage s has landed
+    else vm_wait<0>();
+    const uint8_t* B = &smem[wave][s & 1][0] + r16 * ROWB + 16 * kg;
+#pragma unroll
+    for (int jj = 0; jj < JP; ++jj)
+      acc[gi] = mfma16x16x32(as_bf16x8(a[p * JP + jj]), as_bf16x8(ld16(B + 64 * jj)), acc[gi]);
+    lds_wait();  // buffer s & 1 is read out before stage s + 2 overwrites it
+    if (s + 2 < NST) issue(s + 2);
+  }
+
+  // reduce the four K quarters through LDS; wave w finishes groups w, w+4, ...
+  __syncthreads();
+  f32x4* red = reinterpret_cast<f32x4*>(&smem[0][0][0]);  // [4 waves][NG][64 lanes]
+#pragma unroll
+  for (int gi = 0; gi < NG; ++gi) red[(wave * NG + gi) * 64 + lane] = acc[gi];
+  __syncthreads();
+  auto sum = [&](int gi) {
+    f32x4 v = red[gi * 64 + lane];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) v += red[(w * NG + gi) * 64 + lane];
+    return v;
+  };
+  // D element i of a 16x16 tile is (row 4*(lane/16) + i, col lane%16)
+  if (GEMM1) {
+    for (int gi = wave; gi < NG / 2; gi += 4) {
+      const f32x4 gt = sum(gi), up = sum(gi + NG / 2);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = m0 + 4 * kg + i, col = n0 + gi * 16 + r16;
+        static_cast<uint16_t*>(g.inter)[static_cast<size_t>(row) * g.I + col] = f32_to_bf16(silu_mul(gt[i], up[i]));
+      }
+    }
+  } else {
+    for (int gi = wave; gi < NG; gi += 4) {
+      const f32x4 v = sum(gi);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = m0 + 4 * kg + i;
+        if (g.sorted_ids[row] >= g.n_routed) continue;  // pad rows are never read
+        static_cast<float*>(g.y)[static_cast<size_t>(row) * g.H + n0 + gi * 16 + r16] = v[i];
+      }
     }
   }
 }
@@ -287,7 +412,36 @@ bool bf16_use_skinny(int T, int top_k, int E) {
 #define MOE_SKINNY2_UNROLL 2
 #endif
 
+// Streamed decode kernel: 16-row weight groups per workgroup.
+#ifndef MOE_STREAM_NG1
+#define MOE_STREAM_NG1 4
+#endif
+#ifndef MOE_STREAM_NG2
+#define MOE_STREAM_NG2 4
+#endif
+#ifndef MOE_STREAM
+#define MOE_STREAM 1
+#endif
+
+template <int NG, bool GEMM1>
+hipError_t launch_stream(const GroupedGemm& g, hipStream_t s) {
+  constexpr int NC = GEMM1 ? NG / 2 * 16 : NG * 16;
+  const dim3 grid((GEMM1 ? g.I : g.H) / NC, g.max_rows / 16);
+  switch ((GEMM1 ? g.H : g.I) / 1024) {
+    case 1: hipLaunchKernelGGL((gemm_bf16_stream<NG, 1, GEMM1>), grid, dim3(256), 0, s, g); break;
+    case 2: hipLaunchKernelGGL((gemm_bf16_stream<NG, 2, GEMM1>), grid, dim3(256), 0, s, g); break;
+    case 3: hipLaunchKernelGGL((gemm_bf16_stream<NG, 3, GEMM1>), grid, dim3(256), 0, s, g); break;
+    default: hipLaunchKernelGGL((gemm_bf16_stream<NG, 4, GEMM1>), grid, dim3(256), 0, s, g); break;
+  }
+  return hipGetLastError();
+}
+// K = 1024 * NP, NP <= 4 (each wave's quarter of a row is whole 512-byte
+// pieces); other decode shapes take the skinny kernel
+bool stream_fits(int K, int N, int nc) { return MOE_STREAM && K % 1024 == 0 && K <= 4096 && N % nc == 0; }
+
 hipError_t launch_gemm1_bf16(const GroupedGemm& g, hipStream_t s) {
+  if (bf16_use_skinny(g.T, g.top_k, g.E) && stream_fits(g.H, g.I, MOE_STREAM_NG1 / 2 * 16))
+    return launch_stream<MOE_STREAM_NG1, true>(g, s);
   if (bf16_use_skinny(g.T, g.top_k, g.E)) {
     constexpr int NS = MOE_SKINNY1_NSUB;
     const dim3 grid(g.I / (NS / 2 * 16), g.max_rows / 16);
@@ -298,6 +452,8 @@ hipError_t launch_gemm1_bf16(const GroupedGemm& g, hipStream_t s) {
 }
 
 hipError_t launch_gemm2_bf16(const GroupedGemm& g, hipStream_t s) {
+  if (bf16_use_skinny(g.T, g.top_k, g.E) && stream_fits(g.I, g.H, MOE_STREAM_NG2 * 16))
+    return launch_stream<MOE_STREAM_NG2, false>(g, s);
   if (bf16_use_skinny(g.T, g.top_k, g.E)) {
     constexpr int NS = MOE_SKINNY2_NSUB;
     const dim3 grid(g.H / (NS * 16), g.max_rows / 16);

@@ -29,6 +29,7 @@
 
 #include "common.hpp"
 #include "launch.hpp"
+#include "lds_dma.hpp"
 
 namespace moe {
 
@@ -59,36 +60,6 @@ __device__ __forceinline__ bf16x8 dequant_int4x8(uint32_t w, float s) {
     r[i] = static_cast<__bf16>(static_cast<float>(q) * s);
   }
   return r;
-}
-
-// Direct global -> LDS copy of one 16-byte (or 4-byte) element per lane: lane
-// l of the wave lands at LDS byte `lds + 16*l` (`lds + 4*l`).  Issued as
-// inline asm so the compiler does not treat every later LDS read as
-// dependent on it; completion is awaited explicitly with vm_wait<N>().
-// `lds` must be uniform across the wave.
-__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
-               "v"(gptr) : "memory", "m0");
-}
-__device__ __forceinline__ void dma4(const void* gptr, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
-               "v"(gptr) : "memory", "m0");
-}
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p)));
-}
-// s_waitcnt with only the vector-memory count: at most N loads outstanding.
-template <int N>
-__device__ __forceinline__ void vm_wait() {
-  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
-  __builtin_amdgcn_s_waitcnt(((N >> 4) & 3) << 14 | (0xF << 8) | (7 << 4) | (N & 0xF));
-}
-// Workgroup barrier without a memory fence (the fence of __syncthreads would
-// also drain the loads still in flight for later stages).
-__device__ __forceinline__ void bar() {
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_barrier();
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
 // XOR swizzle of the 16-byte chunks of a 128-byte LDS row: row r stores its
@@ -356,7 +327,7 @@ __global__ __launch_bounds__((WM * WN + NP) * 64) void moe_gemm_tiled(GroupedGem
             read_frags(kt, kk + 1, (kk + 1) & 1);
           } else if (kt + 1 < nk) {
             __atomic_signal_fence(__ATOMIC_SEQ_CST);
-            __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): stage kt is in registers
+            lds_wait();  // stage kt is in registers
             bar();                               // stage kt+1 has landed; buffer kt is free
             read_frags(kt + 1, 0, 0);
           }
