@@ -12,6 +12,8 @@
 //    reduced through LDS.
 // Segments are padded to the row tile, so every tile belongs to one expert;
 // tiles past the last segment exit at once.
+#include <algorithm>
+
 #include "common.hpp"
 #include "launch.hpp"
 #include "lds_dma.hpp"
@@ -137,125 +139,163 @@ __global__ __launch_bounds__(256) void gemm_bf16_skinny(GroupedGemm g) {
 }
 
 // ------------------------------------------------------ streamed (decode)
+#ifndef MOE_STREAM_NS
+#define MOE_STREAM_NS 4
+#endif
 // The decode GEMMs read every weight byte once, so they are bound by how
 // fast HBM delivers the weight slab.  The skinny kernel above walks 16 rows
 // per load instruction (64 bytes of each, at the row stride); this one reads
 // the slab the way HBM streams best: the four waves split K in quarters and
 // the workgroup walks its weight rows in order, each row's quarters read
-// together, with non-temporal direct-to-LDS copies of 512 bytes of one row
-// per instruction (measured on the MI355X: 7.3 TB/s for this pattern,
-// against 6.2 TB/s for loads that walk 16 rows at a time).  Stage (group gi,
-// piece p) holds 16 rows x 512 bytes of the wave's quarter; two stages per
-// wave are in flight, and two workgroups fit a CU.  The activation fragments
-// of the wave's K quarter (NP pieces: K = 1024 NP) are loaded once and stay
-// in registers.  Each stage row sits at a stride of 528 bytes, so the 16
-// rows of a fragment read fall in distinct LDS bank groups.
-// NG: 16-row weight groups per workgroup (GEMM1: NG/2 gate + NG/2 up).
-template <int NG, int NP, bool GEMM1>
+// together, with non-temporal direct-to-LDS copies of one piece (up to 1 KB)
+// of one row per instruction (measured on the MI355X: 7.1-7.3 TB/s for this
+// pattern, against 6.2 TB/s for loads that walk 16 rows at a time).
+//
+// Persistent: one workgroup per CU takes an equal share of the (row tile,
+// column block) units, in row-tile order, read from expert_offsets on the
+// device.  A run of units of one row tile shares the activation fragments
+// of the wave's K quarter (loaded once into registers), and the copy
+// pipeline runs on across its blocks (NS stages of 16 rows x one piece per
+// wave), so start-up costs are paid once per run and the per-block epilogue
+// (cross-wave reduction through LDS, SiLU*up or the y store) overlaps the
+// copies in flight.  A stage row sits at a stride of PC + 16 bytes, so the
+// 16 rows of a fragment read fall in distinct LDS bank groups.
+// NG: 16-row weight groups per block (GEMM1: NG/2 gate + NG/2 up); NP
+// pieces of JP MFMAs (64 bytes each) per row and wave: K = 4 * 32 * NP * JP.
+template <int NG, int NP, int JP, bool GEMM1>
 __global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
-  constexpr int PC = 512;
-  constexpr int ROWB = PC + 16, STAGE = 16 * ROWB;
-  constexpr int JP = PC / 64;   // MFMAs (32 K elements each) per piece
-  constexpr int NJ = NP * JP;   // MFMA slots over the quarter
+  constexpr int PC = 64 * JP, ROWB = PC + 16, STAGE = 16 * ROWB;
+  // stage buffers per wave: as many as LDS holds beside the reduction, up to MOE_STREAM_NS
+  constexpr int NSF = (160 * 1024 - 4 * NG * 1024) / (4 * STAGE);
+  constexpr int NS = NSF < MOE_STREAM_NS ? NSF : MOE_STREAM_NS;
+  static_assert(NS >= 2, "two stage buffers per wave");
+  constexpr int NJ = NP * JP;   // MFMAs over the quarter
   constexpr int NC = GEMM1 ? NG / 2 * 16 : NG * 16;
-  constexpr int NST = NG * NP;  // stages per tile
-  static_assert(4 * NG * 64 * 16 <= 4 * 2 * STAGE, "the reduction fits in the stage buffers");
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[4][2][STAGE];
+  constexpr int NST = NG * NP;  // stages per column block
+  static_assert(PC <= 1024 && (PC / 16) % 2 == 0, "row stride an odd number of 16-byte slots");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[4][NS][STAGE];
+  __shared__ f32x4 red[4][NG][64];
 
-  const int m0 = blockIdx.y * 16;
-  if (m0 >= g.offsets[g.E]) return;
-  const int e = find_segment(g.offsets, g.E, m0);
-  const int n0 = blockIdx.x * NC;
-  const int K = GEMM1 ? g.H : g.I;
+  const int N = GEMM1 ? g.I : g.H, K = GEMM1 ? g.H : g.I;
+  const int nb = N / NC;                                           // column blocks per row tile
+  const long units = static_cast<long>(g.offsets[g.E] / 16) * nb;  // (row tile, block) pairs
+  const long u_end = units * (blockIdx.x + 1) / gridDim.x;
   const int lane = lane_id(), wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kg = lane >> 4;
-  constexpr int qe = NP * PC / 2;  // this wave's K elements of each row (K = 4 qe)
+  constexpr int qe = NJ * 32;  // this wave's K elements of each row
   const int k0 = wave * qe;
-
-  // A fragments: MFMA j covers K [k0 + 32 j, +32), lane group kg its
-  // elements [8 kg, 8 kg + 8); the B fragments use the same K order.  All
-  // of them have landed before the first weight copy is issued, so the
-  // compiler's own wait counts never cover a copy.
-  const uint16_t* arow;
-  if (GEMM1) {
-    const int sid = g.sorted_ids[m0 + r16];
-    const int tok = sid < g.n_routed ? sid / g.top_k : 0;
-    arow = static_cast<const uint16_t*>(g.x) + static_cast<size_t>(tok) * g.H;
-  } else {
-    arow = static_cast<const uint16_t*>(g.inter) + static_cast<size_t>(m0 + r16) * g.I;
-  }
-  arow += k0 + 8 * kg;
-  u32x4 a[NJ];
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) a[j] = ld16(arow + 32 * j);
-  vm_wait<0>();
-
   const size_t rowbytes = static_cast<size_t>(K) * 2;
-  const uint8_t* wq = static_cast<const uint8_t*>(GEMM1 ? g.w1 : g.w2) +
-                      static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) * rowbytes + 2 * static_cast<size_t>(k0) +
-                      16 * lane;
   const uint32_t sbase = lds_addr(&smem[wave][0][0]);
-  // stage s = gi * NP + p: rows of group gi, bytes [p*PC, (p+1)*PC) of the quarter
-  auto issue = [&](int s) {
-    const int gi = s / NP, p = s % NP;
-    const int wr = GEMM1 ? (gi < NG / 2 ? n0 + gi * 16 : g.I + n0 + (gi - NG / 2) * 16) : n0 + gi * 16;
-    const uint8_t* src = wq + static_cast<size_t>(wr) * rowbytes + p * PC;
-    const uint32_t dst = sbase + (s & 1) * STAGE;
-    if (16 * lane < PC) {  // 32 lanes x 16 bytes per row
-#pragma unroll
-      for (int i = 0; i < 16; ++i) dma16_nt(src + i * rowbytes, dst + i * ROWB);
-    }
-  };
 
-  f32x4 acc[NG];
-#pragma unroll
-  for (int gi = 0; gi < NG; ++gi) acc[gi] = f32x4{};
-  issue(0);
-  if (NST > 1) issue(1);
-#pragma unroll
-  for (int s = 0; s < NST; ++s) {
-    const int gi = s / NP, p = s % NP;
-    if (s + 1 < NST) vm_wait<16>();  // stage s has landed
-    else vm_wait<0>();
-    const uint8_t* B = &smem[wave][s & 1][0] + r16 * ROWB + 16 * kg;
-#pragma unroll
-    for (int jj = 0; jj < JP; ++jj)
-      acc[gi] = mfma16x16x32(as_bf16x8(a[p * JP + jj]), as_bf16x8(ld16(B + 64 * jj)), acc[gi]);
-    lds_wait();  // buffer s & 1 is read out before stage s + 2 overwrites it
-    if (s + 2 < NST) issue(s + 2);
-  }
+  for (long u = units * blockIdx.x / gridDim.x; u < u_end;) {
+    // one run: row tile rt, column blocks [cb0, cb1)
+    const int rt = static_cast<int>(u / nb), cb0 = static_cast<int>(u % nb);
+    const int cb1 = static_cast<int>(min(static_cast<long>(nb), cb0 + (u_end - u)));
+    u += cb1 - cb0;
+    const int m0 = rt * 16;
+    const int e = find_segment(g.offsets, g.E, m0);
 
-  // reduce the four K quarters through LDS; wave w finishes groups w, w+4, ...
-  __syncthreads();
-  f32x4* red = reinterpret_cast<f32x4*>(&smem[0][0][0]);  // [4 waves][NG][64 lanes]
-#pragma unroll
-  for (int gi = 0; gi < NG; ++gi) red[(wave * NG + gi) * 64 + lane] = acc[gi];
-  __syncthreads();
-  auto sum = [&](int gi) {
-    f32x4 v = red[gi * 64 + lane];
-#pragma unroll
-    for (int w = 1; w < 4; ++w) v += red[(w * NG + gi) * 64 + lane];
-    return v;
-  };
-  // D element i of a 16x16 tile is (row 4*(lane/16) + i, col lane%16)
-  if (GEMM1) {
-    for (int gi = wave; gi < NG / 2; gi += 4) {
-      const f32x4 gt = sum(gi), up = sum(gi + NG / 2);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = m0 + 4 * kg + i, col = n0 + gi * 16 + r16;
-        static_cast<uint16_t*>(g.inter)[static_cast<size_t>(row) * g.I + col] = f32_to_bf16(silu_mul(gt[i], up[i]));
-      }
+    // A fragments: MFMA j covers K [k0 + 32 j, +32), lane group kg its
+    // elements [8 kg, 8 kg + 8); the B fragments use the same K order.
+    // They (and the pad flags of the rows this lane stores) have landed
+    // before the run's first weight copy is issued, and the previous run
+    // ended with every copy landed, so the compiler's own wait counts never
+    // cover a copy.
+    const uint16_t* arow;
+    if (GEMM1) {
+      const int sid = g.sorted_ids[m0 + r16];
+      const int tok = sid < g.n_routed ? sid / g.top_k : 0;
+      arow = static_cast<const uint16_t*>(g.x) + static_cast<size_t>(tok) * g.H;
+    } else {
+      arow = static_cast<const uint16_t*>(g.inter) + static_cast<size_t>(m0 + r16) * g.I;
     }
-  } else {
-    for (int gi = wave; gi < NG; gi += 4) {
-      const f32x4 v = sum(gi);
+    arow += k0 + 8 * kg;
+    u32x4 a[NJ];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = m0 + 4 * kg + i;
-        if (g.sorted_ids[row] >= g.n_routed) continue;  // pad rows are never read
-        static_cast<float*>(g.y)[static_cast<size_t>(row) * g.H + n0 + gi * 16 + r16] = v[i];
+    for (int j = 0; j < NJ; ++j) a[j] = ld16(arow + 32 * j);
+    bool live[4];  // GEMM2: rows m0 + 4 kg + i that are routed rows (pads are never read)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) live[i] = GEMM1 || g.sorted_ids[m0 + 4 * kg + i] < g.n_routed;
+    vm_wait<0>();
+
+    const uint8_t* wq = static_cast<const uint8_t*>(GEMM1 ? g.w1 : g.w2) +
+                        static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) * rowbytes + 2 * static_cast<size_t>(k0) +
+                        16 * lane;
+    const int nsg = (cb1 - cb0) * NST;  // stages of this run
+    // stage q of the run: block cb0 + q / NST, group gi, piece p
+    auto issue = [&](int q) {
+      const int cb = cb0 + q / NST, r = q % NST, gi = r / NP, p = r % NP;
+      const int n0 = cb * NC;
+      const int wr = GEMM1 ? (gi < NG / 2 ? n0 + gi * 16 : g.I + n0 + (gi - NG / 2) * 16) : n0 + gi * 16;
+      const uint8_t* src = wq + static_cast<size_t>(wr) * rowbytes + p * PC;
+      const uint32_t dst = sbase + (q % NS) * STAGE;
+      if (16 * lane < PC) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) dma16_nt(src + i * rowbytes, dst + i * ROWB);
       }
+    };
+#pragma unroll
+    for (int q = 0; q < NS - 1; ++q)
+      if (q < nsg) issue(q);
+
+    for (int cb = cb0, q0 = 0; cb < cb1; ++cb, q0 += NST) {
+      f32x4 acc[NG];
+#pragma unroll
+      for (int gi = 0; gi < NG; ++gi) acc[gi] = f32x4{};
+#pragma unroll
+      for (int r = 0; r < NST; ++r) {
+        const int q = q0 + r, gi = r / NP, p = r % NP;
+        // the copy NS-1 stages ahead goes into the buffer read out in stage q-1
+        if (q + NS - 1 < nsg) issue(q + NS - 1);
+        // stage q has landed once at most the later stages' 16 copies each fly
+        if (NS >= 4 && q + 3 < nsg) vm_wait<48>();
+        else if (NS >= 3 && q + 2 < nsg) vm_wait<32>();
+        else if (q + 1 < nsg) vm_wait<16>();
+        else vm_wait<0>();
+        const uint8_t* B = &smem[wave][0][0] + (q % NS) * STAGE + r16 * ROWB + 16 * kg;
+#pragma unroll
+        for (int jj = 0; jj < JP; ++jj)
+          acc[gi] = mfma16x16x32(as_bf16x8(a[p * JP + jj]), as_bf16x8(ld16(B + 64 * jj)), acc[gi]);
+        lds_wait();  // this stage's buffer is read out before a later copy lands in it
+      }
+
+      // reduce the four K quarters (in wave order); wave w finishes groups w, w+4, ...
+#pragma unroll
+      for (int gi = 0; gi < NG; ++gi) red[wave][gi][lane] = acc[gi];
+      lds_wait();
+      bar();
+      const int n0 = cb * NC;
+      auto sum = [&](int gi) {
+        f32x4 v = red[0][gi][lane];
+#pragma unroll
+        for (int w = 1; w < 4; ++w) v += red[w][gi][lane];
+        return v;
+      };
+      // D element i of a 16x16 tile is (row 4*(lane/16) + i, col lane%16)
+      if (GEMM1) {
+#pragma unroll
+        for (int gi = 0; gi < NG / 2; ++gi) {
+          if (gi % 4 != wave) continue;
+          const f32x4 gt = sum(gi), up = sum(gi + NG / 2);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int row = m0 + 4 * kg + i, col = n0 + gi * 16 + r16;
+            static_cast<uint16_t*>(g.inter)[static_cast<size_t>(row) * g.I + col] =
+                f32_to_bf16(silu_mul(gt[i], up[i]));
+          }
+        }
+      } else {
+#pragma unroll
+        for (int gi = 0; gi < NG; ++gi) {
+          if (gi % 4 != wave) continue;
+          const f32x4 v = sum(gi);
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (live[i]) static_cast<float*>(g.y)[static_cast<size_t>(m0 + 4 * kg + i) * g.H + n0 + gi * 16 + r16] = v[i];
+        }
+      }
+      lds_wait();
+      bar();  // red is read out before the next block writes it
     }
   }
 }
@@ -423,21 +463,58 @@ bool bf16_use_skinny(int T, int top_k, int E) {
 #define MOE_STREAM 1
 #endif
 
+int stream_grid() {
+  static const int cus = [] {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    return n;
+  }();
+  return cus;
+}
 template <int NG, bool GEMM1>
 hipError_t launch_stream(const GroupedGemm& g, hipStream_t s) {
   constexpr int NC = GEMM1 ? NG / 2 * 16 : NG * 16;
-  const dim3 grid((GEMM1 ? g.I : g.H) / NC, g.max_rows / 16);
-  switch ((GEMM1 ? g.H : g.I) / 1024) {
-    case 1: hipLaunchKernelGGL((gemm_bf16_stream<NG, 1, GEMM1>), grid, dim3(256), 0, s, g); break;
-    case 2: hipLaunchKernelGGL((gemm_bf16_stream<NG, 2, GEMM1>), grid, dim3(256), 0, s, g); break;
-    case 3: hipLaunchKernelGGL((gemm_bf16_stream<NG, 3, GEMM1>), grid, dim3(256), 0, s, g); break;
-    default: hipLaunchKernelGGL((gemm_bf16_stream<NG, 4, GEMM1>), grid, dim3(256), 0, s, g); break;
+  const int K = GEMM1 ? g.H : g.I;
+  // one workgroup per CU, at most one per (row tile, column block) unit
+  const long units = static_cast<long>(g.max_rows / 16) * ((GEMM1 ? g.I : g.H) / NC);
+  const dim3 grid(static_cast<unsigned>(std::max(1L, std::min<long>(stream_grid(), units))));
+#define MOE_STREAM_CASE(NP, JP) \
+  hipLaunchKernelGGL((gemm_bf16_stream<NG, NP, JP, GEMM1>), grid, dim3(256), 0, s, g)
+  const int qb = K / 2;  // bytes of a row per wave
+  if (qb % 512 == 0) {   // 512-byte pieces
+    switch (qb / 512) {
+      case 1: MOE_STREAM_CASE(1, 8); break;
+      case 2: MOE_STREAM_CASE(2, 8); break;
+      case 3: MOE_STREAM_CASE(3, 8); break;
+      default: MOE_STREAM_CASE(4, 8); break;
+    }
+  } else {  // one piece: the quarter is 64 * JP bytes
+    switch (qb / 64) {
+      case 1: MOE_STREAM_CASE(1, 1); break;
+      case 2: MOE_STREAM_CASE(1, 2); break;
+      case 3: MOE_STREAM_CASE(1, 3); break;
+      case 4: MOE_STREAM_CASE(1, 4); break;
+      case 5: MOE_STREAM_CASE(1, 5); break;
+      case 6: MOE_STREAM_CASE(1, 6); break;
+      case 7: MOE_STREAM_CASE(1, 7); break;
+      case 9: MOE_STREAM_CASE(1, 9); break;
+      case 10: MOE_STREAM_CASE(1, 10); break;
+      case 11: MOE_STREAM_CASE(1, 11); break;
+      case 12: MOE_STREAM_CASE(1, 12); break;
+      case 13: MOE_STREAM_CASE(1, 13); break;
+      case 14: MOE_STREAM_CASE(1, 14); break;
+      default: MOE_STREAM_CASE(1, 15); break;
+    }
   }
+#undef MOE_STREAM_CASE
   return hipGetLastError();
 }
-// K = 1024 * NP, NP <= 4 (each wave's quarter of a row is whole 512-byte
-// pieces); other decode shapes take the skinny kernel
-bool stream_fits(int K, int N, int nc) { return MOE_STREAM && K % 1024 == 0 && K <= 4096 && N % nc == 0; }
+// Streamed when each wave's quarter of a row is whole 512-byte pieces (K a
+// multiple of 1024, up to 4096) or one piece under 1 KB (K < 2048)
+bool stream_fits(int K, int N, int nc) {
+  return MOE_STREAM && ((K % 1024 == 0 && K <= 4096) || K < 2048) && N % nc == 0;
+}
 
 hipError_t launch_gemm1_bf16(const GroupedGemm& g, hipStream_t s) {
   if (bf16_use_skinny(g.T, g.top_k, g.E) && stream_fits(g.H, g.I, MOE_STREAM_NG1 / 2 * 16))

@@ -54,12 +54,15 @@ def test_minimum_k(dev, T):
     _check(synth.tiny_config(1, T=T, H=128, I=128, E=4, top_k=2))
 
 
-@pytest.mark.parametrize("H,I", [(1024, 1024), (2048, 3072), (3072, 2048), (4096, 4096)])
+@pytest.mark.parametrize("H,I", [(1024, 1024), (2048, 3072), (3072, 2048), (4096, 4096),
+                                 (640, 1920), (1920, 640), (896, 1664), (1664, 896),
+                                 (1152, 1536), (1536, 1152), (1280, 1792), (1792, 1280)])
 def test_streamed_decode_kernel(dev, H, I):
-    # decode-sized batches (<= 32 rows per expert on average) with K a
-    # multiple of 1024 up to 4096 take the streamed kernel in both products:
-    # one to four 512-byte pieces per wave and row; T = 37 leaves ragged
-    # 16-row tiles, E = 9 an odd expert count
+    # decode-sized batches (<= 32 rows per expert on average) take the
+    # streamed kernel in both products when K is a multiple of 1024 up to
+    # 4096 (one to four 512-byte pieces per wave and row) or below 2048 (one
+    # piece of K/2 bytes): every piece width from 320 to 960 bytes appears
+    # here; T = 37 leaves ragged 16-row tiles, E = 9 an odd expert count
     _check(synth.tiny_config(2, T=37, H=H, I=I, E=9, top_k=3))
 
 
