@@ -55,7 +55,7 @@ DESCR = {
 
 
 # sources that define the GEMM1 kernels (the roofline's dominant kernel)
-GEMM_SOURCES = ("common.hpp", "launch.hpp", "dispatch.hip", "gemm_bf16.hip", "gemm_tiled.hip")
+GEMM_SOURCES = ("common.hpp", "launch.hpp", "lds_dma.hpp", "dispatch.hip", "gemm_bf16.hip", "gemm_tiled.hip")
 
 
 def kernel_source_hash() -> str:
@@ -137,7 +137,8 @@ def cpu_baseline(cfg, inputs, budget_s: float):
 
 def gemm1_kernel_match(name: str) -> bool:
     """True for the GEMM1 (+SiLU*up) kernel of any format / variant."""
-    return ("gemm_bf16_skinny<" in name and "true>" in name) or \
+    decode = ("gemm_bf16_skinny<", "gemm_bf16_stream<", "gemm_w8a16_skinny<")
+    return (any(k in name for k in decode) and "true>" in name) or \
            ("moe_gemm_tiled<" in name and ", true," in name)
 
 
