@@ -14,6 +14,10 @@ states no formula for the layer, so every step below is the plain definition
 of the operation, written out in float64 with library primitives (sort,
 bincount, matmul, exp) and no blocking or fusion:
 
+  router    l[t,e] = sum_h x[t,h] Wr[e,h] on the exact bf16 values (the
+            optional router GEMM in front of the gate; its kernel
+            accumulates in fp32, so the tests run this gate on the
+            kernel's own fp32 logits and bound the logits separately).
   gate      key_e = l_e (+ b_e)            softmax scoring
             key_e = sigmoid(l_e) + b_e      sigmoid scoring (b: selection only)
             top-k by key, descending, equal keys -> lower expert index first;
@@ -144,6 +148,13 @@ def dequant_weight(wfmt: str, w: np.ndarray, scale) -> np.ndarray:
 
 
 # ============================================================ the layer
+def router_logits(hidden_bits, w_router_bits):
+    """Router GEMM in front of the MoE Gate (the step that feeds Fig. 1's gate
+    node): float64 [T,E] = x Wr^T on the exact values of bf16 hidden [T,H]
+    and bf16 router weights [E,H]."""
+    return bf16_to_f64(hidden_bits) @ bf16_to_f64(w_router_bits).T
+
+
 def gate(logits, sel_bias, top_k, mode="softmax", renormalize=True, routed_scale=1.0):
     """MoE Gate (Fig. 1): returns expert ids int32 [T,k] in descending-key
     order (equal keys -> lower index first) and float64 weights [T,k]."""

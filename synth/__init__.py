@@ -8,4 +8,5 @@ from .moe_inputs import (  # noqa: F401
     make_routing_inputs,
     to_device,
     make_expert_weights,
+    make_router_weights,
 )

@@ -19,6 +19,7 @@ Value recipe (the five workloads, plus a decode step on fp8 weights):
       - "zipf:<s>"      b_e = -s * ln(rank_e), rank_e a seeded permutation
                         of 1..E, so exp(b_e) follows a Zipf(s) law (skew).
   * sel_bias (sigmoid scoring only) ~ N(0, std^2): used for selection only.
+  * w_router (only for the fused router + gate) bf16 [E, H] ~ N(0, 1/H).
   (Weight spreads are variances, N(0, 1/fan_in) = LeCun init; the bias
   spreads are standard deviations.)
   * W1[E, 2I, H], W2[E, H, I] ~ N(0, 1/fan_in) in fp32 (fan_in = H for W1,
@@ -47,7 +48,7 @@ from dataclasses import dataclass, replace
 import numpy as np
 import torch
 
-TID_HIDDEN, TID_LOGITS, TID_LOGIT_BIAS, TID_W1, TID_W2, TID_SEL_BIAS = range(6)
+TID_HIDDEN, TID_LOGITS, TID_LOGIT_BIAS, TID_W1, TID_W2, TID_SEL_BIAS, TID_ROUTER = range(7)
 HIDDEN_BLOCK = 64  # tokens per hidden-state substream
 
 
@@ -168,6 +169,14 @@ def make_routing_inputs(cfg: MoeConfig, threads=None) -> dict:
         std = np.float32(cfg.sel_bias_std)
         sel_bias = (_rng(cfg.seed, TID_SEL_BIAS).standard_normal(E, dtype=np.float32) * std).astype(np.float32)
     return {"hidden": hidden, "logits": np.ascontiguousarray(logits), "sel_bias": sel_bias}
+
+
+def make_router_weights(cfg: MoeConfig) -> np.ndarray:
+    """Router weights for the fused router + gate: bf16 bits [E, H] drawn
+    N(0, 1/H) (LeCun), so with N(0, 1) hidden rows the logits are about
+    N(0, 1) like the workloads' direct logits."""
+    w = _rng(cfg.seed, TID_ROUTER).standard_normal((cfg.E, cfg.H), dtype=np.float32)
+    return _bf16_bits(w * np.float32(1.0 / np.sqrt(cfg.H)))
 
 
 # ---------------------------------------------------------------- weight storage
