@@ -174,6 +174,9 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=2, choices=sorted(DESCR))
+    ap.add_argument("--router", action="store_true",
+                    help="compute the logits in-layer from a router weight [E,H] (router GEMM fused "
+                         "with the gate); the FLOP count stays that of the experts")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="host-time budget of the oracle baseline (0 disables it)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -212,13 +215,17 @@ def main():
     t0 = time.perf_counter()
     inputs = synth.make_inputs(cfg)
     d = synth.to_device(inputs)
+    w_router = None
+    if args.router:
+        w_router = synth.to_device({"w": synth.make_router_weights(cfg)})["w"]
     gen_s = time.perf_counter() - t0
     out = torch.empty((cfg.T, cfg.H), dtype=torch.float32, device="cuda")
     margs = moe.make_args(cfg.T, cfg.H, cfg.E, cfg.I, cfg.top_k, mode=cfg.mode,
                           renormalize=cfg.renormalize, routed_scale=cfg.routed_scale,
-                          wfmt=cfg.wfmt, out_dtype="f32", hidden=d["hidden"], logits=d["logits"],
+                          wfmt=cfg.wfmt, out_dtype="f32", hidden=d["hidden"],
+                          logits=None if args.router else d["logits"],
                           w1=d["w1"], w2=d["w2"], w1_scale=d["w1_scale"], w2_scale=d["w2_scale"],
-                          sel_bias=d["sel_bias"], out=out)
+                          sel_bias=d["sel_bias"], out=out, w_router=w_router)
     ws = torch.empty(moe.moe_workspace_bytes(margs), dtype=torch.uint8, device="cuda")
     layout = moe.moe_workspace_layout(margs)
     stream = torch.cuda.current_stream()
@@ -313,7 +320,7 @@ def main():
         "vs_baseline": None,
         "dtype": dtype,
         "data": "synthetic (seeded; value recipe in DESIGN.md)",
-        "config": {"workload": DESCR[args.config], "T": T, "H": H, "E": cfg.E, "I": I,
+        "config": {"workload": DESCR[args.config] + (", logits from a fused router GEMM (bf16 [E,H])" if args.router else ""), "T": T, "H": H, "E": cfg.E, "I": I,
                    "top_k": cfg.top_k, "wfmt": cfg.wfmt, "active_experts": n_active,
                    "max_rows_per_expert": int(counts.max()), "block_m": layout["block_m"]},
         "us_per_layer": ms * 1e3,

@@ -108,6 +108,25 @@ moe_status moe_gate_topk(const float* logits, const float* sel_bias, int T, int 
                          int mode, int renormalize, float routed_scale, int32_t* topk_ids,
                          float* topk_w, hipStream_t stream);
 
+/*
+ * Router GEMM fused with the gate (the step in front of the MoE Gate node,
+ * Fig. 1): logits[t,e] = sum_h hidden[t,h] * w_router[e,h], bf16 products
+ * accumulated in fp32, then exactly the selection and weights of
+ * moe_gate_topk on those fp32 logits, in one kernel.
+ *   hidden    device bf16 bits [T,H], 16-byte aligned; H % 128 == 0, H <= 65536
+ *   w_router  device bf16 bits [E,H], 16-byte aligned
+ *   logits    device fp32 [T,E] or NULL: receives the logits the selection used
+ *   other arguments and the outputs as moe_gate_topk.
+ * The fp32 accumulation order is the kernel's own: logits agree with the
+ * exact sums to within a few fp32 roundings of sum_h |hidden * w_router|.
+ * Errors: MOE_ERR_NULL, MOE_ERR_SHAPE, MOE_ERR_UNSUPPORTED, MOE_ERR_ALIGN,
+ * MOE_ERR_HIP.  T == 0 is a no-op.
+ */
+moe_status moe_router_gate_topk(const uint16_t* hidden, const uint16_t* w_router, int T, int H, int E,
+                                int top_k, int mode, int renormalize, float routed_scale,
+                                const float* sel_bias, float* logits, int32_t* topk_ids, float* topk_w,
+                                hipStream_t stream);
+
 /* Rows needed by moe_permute's sorted_ids: T*top_k + E*(block_m-1).  Host-only. */
 size_t moe_permute_capacity(int T, int top_k, int E, int block_m);
 
@@ -155,7 +174,7 @@ typedef struct moe_args {
   int32_t ofmt;             /* moe_ofmt                                       */
   const float* sel_bias;    /* device fp32 [E] or NULL                        */
   const uint16_t* hidden;   /* device bf16 [T,H]                              */
-  const float* logits;      /* device fp32 [T,E]                              */
+  const float* logits;      /* device fp32 [T,E]; NULL when w_router is set    */
   const void* w1;           /* device, [E,2I,H] in the wfmt storage (gate rows [0,I), up rows [I,2I)) */
   const void* w2;           /* device, [E,H,I] in the wfmt storage            */
   const void* w1_scale;     /* device, per wfmt (NULL for bf16)               */
@@ -163,6 +182,9 @@ typedef struct moe_args {
   void* out;                /* device [T,H], fp32 or bf16 per ofmt            */
   int32_t* topk_ids_out;    /* optional device int32 [T,top_k] copy, or NULL  */
   float* topk_w_out;        /* optional device fp32 [T,top_k] copy, or NULL   */
+  const uint16_t* w_router; /* device bf16 [E,H] or NULL: if set, the layer computes its
+                               logits from hidden (moe_router_gate_topk) and ignores `logits` */
+  float* logits_out;        /* optional device fp32 [T,E]: those logits, or NULL */
 } moe_args;
 
 /* Workspace bytes moe_forward needs for these sizes/format.  Host-only, pure. */
@@ -186,7 +208,7 @@ typedef struct moe_ws_layout {
 moe_status moe_workspace_layout(const moe_args* a, moe_ws_layout* layout);
 
 /*
- * Fused MoE layer: gate -> permute -> [fp8 activation quantisation] ->
+ * Fused MoE layer: [router GEMM] gate -> permute -> [fp8 activation quantisation] ->
  * grouped GEMM1 with fused SiLU*up epilogue -> grouped GEMM2 -> combine, all
  * enqueued on `stream`; no host synchronisation, no allocation.
  * Requirements: T >= 0; 1 <= E <= MOE_MAX_EXPERTS; 1 <= top_k <= min(E,
@@ -194,7 +216,9 @@ moe_status moe_workspace_layout(const moe_args* a, moe_ws_layout* layout);
  * aligned; ws_bytes >= moe_workspace_bytes(a); sel_bias only with a format
  * that reads it (both scoring modes do).  Padding rows of the intermediates
  * are unspecified.  T == 0 is a no-op.
- * MOE_W_FP8E4M3_B128_A16 additionally needs T * top_k <= 32 * E.
+ * MOE_W_FP8E4M3_B128_A16 additionally needs T * top_k <= 32 * E.  With
+ * w_router set the router GEMM and the gate run as one kernel (as
+ * moe_router_gate_topk) and `logits` may be NULL.
  * Errors: MOE_ERR_NULL, MOE_ERR_SHAPE, MOE_ERR_UNSUPPORTED, MOE_ERR_ALIGN,
  * MOE_ERR_WORKSPACE, MOE_ERR_HIP.
  */

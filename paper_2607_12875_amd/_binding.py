@@ -23,7 +23,7 @@ WFMT = {"bf16": 0, "fp8": 1, "int4": 2, "fp8a16": 3}
 OFMT = {"f32": 0, "bf16": 1}
 
 EXPORTED = ("moe_status_str", "moe_permute_capacity", "moe_permute_workspace_bytes",
-            "moe_gate_topk", "moe_permute", "moe_act_quant_fp8", "moe_workspace_bytes",
+            "moe_gate_topk", "moe_router_gate_topk", "moe_permute", "moe_act_quant_fp8", "moe_workspace_bytes",
             "moe_workspace_layout", "moe_forward", "moe_forward_profiled")
 NUM_STAGES = 6
 STAGES = ("gate", "permute", "act_quant", "gemm1", "gemm2", "combine")
@@ -45,6 +45,7 @@ class MoeArgs(ctypes.Structure):
         ("w1", ctypes.c_void_p), ("w2", ctypes.c_void_p),
         ("w1_scale", ctypes.c_void_p), ("w2_scale", ctypes.c_void_p),
         ("out", ctypes.c_void_p), ("topk_ids_out", ctypes.c_void_p), ("topk_w_out", ctypes.c_void_p),
+        ("w_router", ctypes.c_void_p), ("logits_out", ctypes.c_void_p),
     ]
 
 
@@ -75,6 +76,8 @@ def lib() -> ctypes.CDLL:
         L.moe_permute_workspace_bytes.argtypes = [i32, i32, i32]
         L.moe_gate_topk.restype = i32
         L.moe_gate_topk.argtypes = [vp, vp, i32, i32, i32, i32, i32, f32, vp, vp, vp]
+        L.moe_router_gate_topk.restype = i32
+        L.moe_router_gate_topk.argtypes = [vp, vp, i32, i32, i32, i32, i32, i32, f32, vp, vp, vp, vp, vp]
         L.moe_permute.restype = i32
         L.moe_permute.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, i32, vp, sz, vp]
         L.moe_act_quant_fp8.restype = i32
@@ -136,6 +139,25 @@ def moe_gate_topk(logits, top_k, mode="softmax", renormalize=True, routed_scale=
     return topk_ids, topk_w
 
 
+def moe_router_gate_topk(hidden, w_router, top_k, mode="softmax", renormalize=True, routed_scale=1.0,
+                         sel_bias=None, logits=None, topk_ids=None, topk_w=None, stream=None):
+    """Router GEMM (bf16 hidden [T,H] x w_router [E,H]^T, fp32) fused with the
+    gate: returns (topk_ids int32 [T,k], topk_w fp32 [T,k]); logits, if given
+    (fp32 [T,E]), receives the logits the selection used."""
+    _dev(hidden, w_router, sel_bias, logits)
+    T, H = hidden.shape
+    E = w_router.shape[0]
+    if topk_ids is None:
+        topk_ids = torch.empty((T, top_k), dtype=torch.int32, device=hidden.device)
+    if topk_w is None:
+        topk_w = torch.empty((T, top_k), dtype=torch.float32, device=hidden.device)
+    _check(lib().moe_router_gate_topk(_ptr(hidden), _ptr(w_router), T, H, E, top_k, SCORE[mode],
+                                      int(renormalize), float(routed_scale), _ptr(sel_bias),
+                                      _ptr(logits), _ptr(topk_ids), _ptr(topk_w), _stream(stream)),
+           "moe_router_gate_topk")
+    return topk_ids, topk_w
+
+
 def moe_permute(topk_ids, E: int, block_m: int, stream=None):
     """Permute/align: returns (expert_offsets [E+1], sorted_ids [cap], inv_pos [T*k])."""
     _dev(topk_ids)
@@ -166,11 +188,11 @@ def moe_act_quant_fp8(x, stream=None):
 def make_args(T, H, E, I, top_k, *, mode="softmax", renormalize=True, routed_scale=1.0,
               wfmt="bf16", out_dtype="f32", hidden=None, logits=None, w1=None, w2=None,
               w1_scale=None, w2_scale=None, sel_bias=None, out=None, topk_ids_out=None,
-              topk_w_out=None) -> MoeArgs:
+              topk_w_out=None, w_router=None, logits_out=None) -> MoeArgs:
     return MoeArgs(T, H, E, I, top_k, SCORE[mode], int(renormalize), float(routed_scale),
                    WFMT[wfmt], OFMT[out_dtype], _ptr(sel_bias), _ptr(hidden), _ptr(logits),
                    _ptr(w1), _ptr(w2), _ptr(w1_scale), _ptr(w2_scale), _ptr(out),
-                   _ptr(topk_ids_out), _ptr(topk_w_out))
+                   _ptr(topk_ids_out), _ptr(topk_w_out), _ptr(w_router), _ptr(logits_out))
 
 
 def moe_workspace_bytes(args: MoeArgs) -> int:
@@ -199,17 +221,20 @@ def moe_forward_profiled(args: MoeArgs, workspace, events, stream=None):
 def moe_forward(hidden, logits, w1, w2, top_k, *, mode="softmax", renormalize=True,
                 routed_scale=1.0, wfmt="bf16", sel_bias=None, w1_scale=None, w2_scale=None,
                 out_dtype="f32", out=None, workspace=None, topk_ids_out=None, topk_w_out=None,
-                stream=None):
+                w_router=None, logits_out=None, stream=None):
     """The whole layer on device tensors; returns (out [T,H], workspace).
 
     hidden bf16 [T,H]; logits fp32 [T,E]; weights in the wfmt storage:
     bf16 [E,2I,H] / [E,H,I]; fp8 uint8 codes with fp32 block scales
     [E,2I/128,H/128] / [E,H/128,I/128]; int4 int32 [E,2I,H/8] / [E,H,I/8] with
     bf16 scales [E,2I,H/128] / [E,H,I/128]; "fp8a16" (weight-only fp8, a decode
-    route) takes the fp8 storage with bf16 activations."""
-    _dev(hidden, logits, w1, w2, sel_bias, w1_scale, w2_scale, out, topk_ids_out, topk_w_out)
+    route) takes the fp8 storage with bf16 activations.  With w_router (bf16
+    [E,H]) the layer computes its own logits (pass logits=None); logits_out
+    (fp32 [T,E]) then receives them."""
+    _dev(hidden, logits, w1, w2, sel_bias, w1_scale, w2_scale, out, topk_ids_out, topk_w_out,
+         w_router, logits_out)
     T, H = hidden.shape
-    E = logits.shape[1]
+    E = (w_router if w_router is not None else logits).shape[0 if w_router is not None else 1]
     I = w2.shape[2] * (8 if wfmt == "int4" else 1)
     if out is None:
         out = torch.empty((T, H), dtype=torch.float32 if out_dtype == "f32" else torch.bfloat16,
@@ -217,7 +242,8 @@ def moe_forward(hidden, logits, w1, w2, top_k, *, mode="softmax", renormalize=Tr
     args = make_args(T, H, E, I, top_k, mode=mode, renormalize=renormalize,
                      routed_scale=routed_scale, wfmt=wfmt, out_dtype=out_dtype, hidden=hidden,
                      logits=logits, w1=w1, w2=w2, w1_scale=w1_scale, w2_scale=w2_scale,
-                     sel_bias=sel_bias, out=out, topk_ids_out=topk_ids_out, topk_w_out=topk_w_out)
+                     sel_bias=sel_bias, out=out, topk_ids_out=topk_ids_out, topk_w_out=topk_w_out,
+                     w_router=w_router, logits_out=logits_out)
     need = moe_workspace_bytes(args)
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=hidden.device)

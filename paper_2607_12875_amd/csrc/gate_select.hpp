@@ -1,0 +1,207 @@
+// Top-k selection and routing weights of one token on one 64-lane wavefront
+// (the MoE Gate node of Fig. 1), shared by the gate kernel (logits read from
+// HBM) and the router kernel (logits computed into LDS).
+//
+// Lane l owns experts l, l+64, ... (up to EPL per lane) and computes their
+// selection keys in fp64; the order is larger key first, equal keys -> lower
+// expert index.  Keys and weights are computed in fp64 so the selection is
+// decided at a precision where ids are reproducible bit for bit; weights are
+// rounded to fp32 once at the end.
+#pragma once
+#include "common.hpp"
+
+namespace moe {
+
+constexpr int MOE_GATE_MAX_K = 32;  // the ABI's top_k limit
+
+__device__ __forceinline__ void wave_argmax(double& v, int& e) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    double ov = __shfl_xor(v, off);
+    int oe = __shfl_xor(e, off);
+    if (ov > v || (ov == v && oe < e)) { v = ov; e = oe; }
+  }
+}
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+__device__ __forceinline__ double wave_max(double v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off));
+  return v;
+}
+
+// Keys (and the values the weights use) of this lane's experts.
+template <int EPL>
+__device__ __forceinline__ void gate_keys(const float* lg, const float* bias, int E, int mode, double* key,
+                                          double* lv) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const int e = lane + 64 * i;
+    if (e < E) {
+      const double l = static_cast<double>(lg[e]);
+      const double b = bias ? static_cast<double>(bias[e]) : 0.0;
+      if (mode == 0) {
+        lv[i] = l;
+        key[i] = l + b;
+      } else {
+        const double s = 1.0 / (1.0 + exp(-l));
+        lv[i] = s;
+        key[i] = s + b;
+      }
+    } else {
+      lv[i] = -INFINITY;
+      key[i] = -INFINITY;
+    }
+  }
+}
+
+// Arg-max selection: k rounds of a cross-lane arg-max over the keys held in
+// registers.  Its work per token grows with k * log2(64), not with E, so it
+// wins once there are many experts per lane.  lg: this token's E logits;
+// ids/w (and the optional copies ids2/w2): this token's k outputs.
+template <int EPL>
+__device__ __forceinline__ void gate_argmax_row(const float* lg, const float* bias, int E, int k, int mode,
+                                                int renorm, float scale, int32_t* ids, float* w, int32_t* ids2,
+                                                float* w2) {
+  const int lane = lane_id();
+  double key[EPL], lv[EPL];  // lv: logit in fp64 (softmax) or sigmoid score (sigmoid)
+  gate_keys<EPL>(lg, bias, E, mode, key, lv);
+
+  int my_id = 0;
+  double my_v = 0.0;
+  for (int j = 0; j < k; ++j) {
+    double bv = -INFINITY;
+    int be = 0x7fffffff;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i)
+      if (key[i] > bv) { bv = key[i]; be = lane + 64 * i; }  // strict: lower index kept
+    wave_argmax(bv, be);
+#pragma unroll
+    for (int i = 0; i < EPL; ++i)
+      if (lane + 64 * i == be) key[i] = -INFINITY;
+    // the owner lane broadcasts the selected expert's logit / score
+    double v = 0.0;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i)
+      if (lane + 64 * i == be) v = lv[i];
+    v = wave_sum(v);  // exactly one lane contributed
+    if (lane == j) { my_id = be; my_v = v; }
+  }
+
+  const bool sel = lane < k;
+  double wt;
+  if (mode == 0) {
+    if (renorm) {
+      const double m = wave_max(sel ? my_v : -INFINITY);
+      const double z = sel ? exp(my_v - m) : 0.0;
+      wt = z / wave_sum(z);
+    } else {
+      double m = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) m = fmax(m, lv[i]);
+      m = wave_max(m);
+      double s = 0.0;
+#pragma unroll
+      for (int i = 0; i < EPL; ++i)
+        if (lane + 64 * i < E) s += exp(lv[i] - m);
+      wt = exp(my_v - m) / wave_sum(s);
+    }
+  } else {
+    wt = renorm ? my_v / wave_sum(sel ? my_v : 0.0) : my_v;
+  }
+  wt *= static_cast<double>(scale);
+  if (sel) {
+    ids[lane] = my_id;
+    w[lane] = static_cast<float>(wt);
+    if (ids2) ids2[lane] = my_id;
+    if (w2) w2[lane] = static_cast<float>(wt);
+  }
+}
+
+// Rank selection: every key goes to LDS; lane l counts, for each key it owns,
+// the keys that beat it (larger, or equal at a lower expert index).  That
+// rank is the key's slot in descending order, so the k winners write their
+// id directly; no sequential arg-max rounds.  Keys stay fp64 throughout.
+// skey/sval: EPL*64 doubles of LDS, sel: MOE_GATE_MAX_K doubles, private to
+// this wave.  Only waves of one token may call it together (no barrier).
+template <int EPL>
+__device__ __forceinline__ void gate_rank_row(const float* lg, const float* bias, int E, int k, int mode,
+                                              int renorm, float scale, int32_t* ids, float* w, int32_t* ids2,
+                                              float* w2, double* skey, double* sval, double* sel) {
+  const int lane = lane_id();
+  double key[EPL], lv[EPL];
+  gate_keys<EPL>(lg, bias, E, mode, key, lv);
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    skey[lane + 64 * i] = key[i];
+    sval[lane + 64 * i] = lv[i];
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+  int rank[EPL];
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) rank[i] = 0;
+#pragma unroll 4
+  for (int e2 = 0; e2 < E; ++e2) {
+    const double k2 = skey[e2];  // same address in every lane: a broadcast read
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const int e = lane + 64 * i;
+      rank[i] += (k2 > key[i]) || (k2 == key[i] && e2 < e);
+    }
+  }
+  __builtin_amdgcn_wave_barrier();  // every lane is done reading the keys
+  int32_t* slot_id = reinterpret_cast<int32_t*>(skey);  // reused: id of slot j
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const int e = lane + 64 * i;
+    if (e < E && rank[i] < k) {
+      slot_id[rank[i]] = e;
+      sel[rank[i]] = lv[i];
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  if (lane >= k) return;
+
+  const double my_v = sel[lane];
+  double wt;
+  if (mode == 0) {
+    if (renorm) {
+      double m = -INFINITY;
+      for (int j = 0; j < k; ++j) m = fmax(m, sel[j]);
+      double z = 0.0;
+      for (int j = 0; j < k; ++j) z += exp(sel[j] - m);
+      wt = exp(my_v - m) / z;
+    } else {
+      double m = -INFINITY;
+      for (int e2 = 0; e2 < E; ++e2) m = fmax(m, sval[e2]);
+      double z = 0.0;
+      for (int e2 = 0; e2 < E; ++e2) z += exp(sval[e2] - m);
+      wt = exp(my_v - m) / z;
+    }
+  } else if (renorm) {
+    double z = 0.0;
+    for (int j = 0; j < k; ++j) z += sel[j];
+    wt = my_v / z;
+  } else {
+    wt = my_v;
+  }
+  wt *= static_cast<double>(scale);
+  const int my_id = slot_id[lane];
+  ids[lane] = my_id;
+  w[lane] = static_cast<float>(wt);
+  if (ids2) ids2[lane] = my_id;
+  if (w2) w2[lane] = static_cast<float>(wt);
+}
+
+}  // namespace moe

@@ -41,12 +41,13 @@ moe_status check_args(const moe_args* a) {
     return MOE_ERR_UNSUPPORTED;
   if (a->ofmt != MOE_OUT_F32 && a->ofmt != MOE_OUT_BF16) return MOE_ERR_UNSUPPORTED;
   if (a->T == 0) return MOE_OK;
-  if (!a->hidden || !a->logits || !a->w1 || !a->w2 || !a->out) return MOE_ERR_NULL;
+  if (!a->hidden || (!a->logits && !a->w_router) || !a->w1 || !a->w2 || !a->out) return MOE_ERR_NULL;
   if (a->wfmt != MOE_W_BF16 && (!a->w1_scale || !a->w2_scale)) return MOE_ERR_NULL;
   if (!aligned16(a->hidden) || !aligned16(a->w1) || !aligned16(a->w2) || !aligned16(a->out))
     return MOE_ERR_ALIGN;
   if (a->wfmt != MOE_W_BF16 && (!aligned16(a->w1_scale) || !aligned16(a->w2_scale)))
     return MOE_ERR_ALIGN;
+  if (!aligned16(a->w_router) || !aligned4(a->logits_out)) return MOE_ERR_ALIGN;
   if (!aligned4(a->logits) || !aligned4(a->sel_bias) || !aligned4(a->topk_ids_out) ||
       !aligned4(a->topk_w_out))
     return MOE_ERR_ALIGN;
@@ -138,6 +139,26 @@ moe_status moe_gate_topk(const float* logits, const float* sel_bias, int T, int 
   return MOE_OK;
 }
 
+moe_status moe_router_gate_topk(const uint16_t* hidden, const uint16_t* w_router, int T, int H, int E,
+                                int top_k, int mode, int renormalize, float routed_scale,
+                                const float* sel_bias, float* logits, int32_t* topk_ids, float* topk_w,
+                                hipStream_t stream) {
+  moe_status st = check_topk_shape(T, E, top_k);
+  if (st != MOE_OK) return st;
+  if (H < 128 || H % 128 || H > (1 << 16)) return MOE_ERR_SHAPE;
+  if (mode != MOE_SCORE_SOFTMAX && mode != MOE_SCORE_SIGMOID) return MOE_ERR_UNSUPPORTED;
+  if (renormalize != 0 && renormalize != 1) return MOE_ERR_UNSUPPORTED;
+  if (T == 0) return MOE_OK;
+  if (!hidden || !w_router || !topk_ids || !topk_w) return MOE_ERR_NULL;
+  if (!aligned16(hidden) || !aligned16(w_router)) return MOE_ERR_ALIGN;
+  if (!aligned4(logits) || !aligned4(sel_bias) || !aligned4(topk_ids) || !aligned4(topk_w))
+    return MOE_ERR_ALIGN;
+  if (moe::launch_router_gate(hidden, w_router, T, H, E, top_k, mode, renormalize, routed_scale, sel_bias,
+                              logits, topk_ids, topk_w, nullptr, nullptr, stream) != hipSuccess)
+    return MOE_ERR_HIP;
+  return MOE_OK;
+}
+
 moe_status moe_permute(const int32_t* topk_ids, int T, int top_k, int E, int block_m,
                        int32_t* expert_offsets, int32_t* sorted_ids, int32_t* inv_pos, int cap,
                        void* ws, size_t ws_bytes, hipStream_t stream) {
@@ -210,10 +231,14 @@ moe_status run_layer(const moe_args* a, void* ws, size_t ws_bytes, hipEvent_t* e
   int32_t* inv = at<int32_t>(ws, L.inv_pos);
 
   if (!mark(0)) return MOE_ERR_HIP;
-  if (moe::launch_gate_topk(a->logits, a->sel_bias, a->T, a->E, a->top_k, a->score_mode,
-                            a->renormalize, a->routed_scale, ids, wts, a->topk_ids_out,
-                            a->topk_w_out, stream) != hipSuccess)
-    return MOE_ERR_HIP;
+  const hipError_t gate_err =
+      a->w_router
+          ? moe::launch_router_gate(a->hidden, a->w_router, a->T, a->H, a->E, a->top_k, a->score_mode,
+                                    a->renormalize, a->routed_scale, a->sel_bias, a->logits_out, ids, wts,
+                                    a->topk_ids_out, a->topk_w_out, stream)
+          : moe::launch_gate_topk(a->logits, a->sel_bias, a->T, a->E, a->top_k, a->score_mode, a->renormalize,
+                                  a->routed_scale, ids, wts, a->topk_ids_out, a->topk_w_out, stream);
+  if (gate_err != hipSuccess) return MOE_ERR_HIP;
   if (!mark(1)) return MOE_ERR_HIP;
   if (moe::launch_permute(ids, a->T, a->top_k, a->E, L.block_m, offs, sorted, inv, L.cap,
                           at<void>(ws, L.permute_ws), stream) != hipSuccess)

@@ -74,6 +74,15 @@ def test_forward_argument_validation():
     a = _args()
     a.wfmt = 9
     assert _fwd(a) == 3
+    # a router weight replaces the logits input (16-byte aligned); one of the two is required
+    a = _args(logits=None)
+    assert _fwd(a) == 1
+    a.w_router = FAKE
+    assert _fwd(a, ws=None) == 5  # accepted, then no workspace
+    a.w_router = FAKE + 4
+    assert _fwd(a) == 4
+    a.w_router, a.logits_out = FAKE, FAKE + 2
+    assert _fwd(a) == 4
     # T == 0 is a no-op that touches no device memory
     assert _fwd(_args(T=0, hidden=None, logits=None, w1=None, w2=None, out=None), ws=None, nbytes=0) == 0
 
@@ -85,6 +94,14 @@ def test_gate_and_permute_validation():
     assert L.moe_gate_topk(FAKE, None, 4, 8, 2, 5, 1, 1.0, FAKE, FAKE, None) == 3
     assert L.moe_gate_topk(FAKE + 2, None, 4, 8, 2, 0, 1, 1.0, FAKE, FAKE, None) == 4
     assert L.moe_gate_topk(None, None, 0, 8, 2, 0, 1, 1.0, None, None, None) == 0
+    R = L.moe_router_gate_topk
+    assert R(FAKE, FAKE, 4, 256, 8, 9, 0, 1, 1.0, None, None, FAKE, FAKE, None) == 2   # top_k > E
+    assert R(FAKE, FAKE, 4, 200, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, None) == 2   # H % 128
+    assert R(FAKE, None, 4, 256, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, None) == 1
+    assert R(FAKE, FAKE, 4, 256, 8, 2, 3, 1, 1.0, None, None, FAKE, FAKE, None) == 3
+    assert R(FAKE + 8, FAKE, 4, 256, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, None) == 4
+    assert R(FAKE, FAKE, 4, 256, 8, 2, 0, 1, 1.0, None, FAKE + 1, FAKE, FAKE, None) == 4
+    assert R(None, None, 0, 256, 8, 2, 0, 1, 1.0, None, None, None, None, None) == 0
     cap = moe.moe_permute_capacity(10, 2, 8, 16)
     assert cap == 10 * 2 + 8 * 15
     assert L.moe_permute(FAKE, 10, 2, 8, 16, FAKE, FAKE, FAKE, cap - 1, None, 0, None) == 2
