@@ -138,6 +138,17 @@ __global__ __launch_bounds__(256) void gemm_bf16_skinny(GroupedGemm g) {
   }
 }
 
+__device__ __forceinline__ bf16x8 e4m3x8_to_bf16(uint32_t lo, uint32_t hi) {
+  bf16x8 r;
+  const auto f0 = __builtin_amdgcn_cvt_pk_f32_fp8(lo, false), f1 = __builtin_amdgcn_cvt_pk_f32_fp8(lo, true);
+  const auto f2 = __builtin_amdgcn_cvt_pk_f32_fp8(hi, false), f3 = __builtin_amdgcn_cvt_pk_f32_fp8(hi, true);
+  r[0] = static_cast<__bf16>(f0[0]); r[1] = static_cast<__bf16>(f0[1]);  // exact: e4m3 fits bf16
+  r[2] = static_cast<__bf16>(f1[0]); r[3] = static_cast<__bf16>(f1[1]);
+  r[4] = static_cast<__bf16>(f2[0]); r[5] = static_cast<__bf16>(f2[1]);
+  r[6] = static_cast<__bf16>(f3[0]); r[7] = static_cast<__bf16>(f3[1]);
+  return r;
+}
+
 // ------------------------------------------------------ streamed (decode)
 #ifndef MOE_STREAM_NS
 #define MOE_STREAM_NS 4
@@ -160,11 +171,24 @@ __global__ __launch_bounds__(256) void gemm_bf16_skinny(GroupedGemm g) {
 // (cross-wave reduction through LDS, SiLU*up or the y store) overlaps the
 // copies in flight.  A stage row sits at a stride of PC + 16 bytes, so the
 // 16 rows of a fragment read fall in distinct LDS bank groups.
+//
+// FMT 0: bf16 weights.  FMT 3: e4m3 weights with fp32 scales per 128x128
+// block (the weight-only fp8 route): each stage also copies its group's
+// block scales for the piece (one 4-byte copy per 128-wide K block) next to
+// the weights; inside a 128-wide block lane group kg takes bytes
+// [32 kg, 32 kg + 32), the four MFMAs of the block decode them exactly to
+// bf16 (the activation fragments use the same K order), and the block's
+// partial is scaled into the accumulator.
 // NG: 16-row weight groups per block (GEMM1: NG/2 gate + NG/2 up); NP
-// pieces of JP MFMAs (64 bytes each) per row and wave: K = 4 * 32 * NP * JP.
-template <int NG, int NP, int JP, bool GEMM1>
+// pieces of JP MFMAs (32 K elements each) per row and wave: K = 4 * 32 * NP * JP.
+template <int FMT, int NG, int NP, int JP, bool GEMM1>
 __global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
-  constexpr int PC = 64 * JP, ROWB = PC + 16, STAGE = 16 * ROWB;
+  constexpr bool F8 = FMT == 3;
+  constexpr int ES = F8 ? 1 : 2;                     // weight bytes per element
+  constexpr int PC = 32 * ES * JP, ROWB = PC + 16;  // piece bytes, LDS row stride
+  constexpr int STAGE = 16 * ROWB + (F8 ? 64 : 0);  // + the piece's block scales
+  constexpr int CPS = F8 ? 17 : 16;                 // copy instructions per stage
+  static_assert(!F8 || JP % 4 == 0, "fp8 pieces are whole 128-wide scale blocks");
   // stage buffers per wave: as many as LDS holds beside the reduction, up to MOE_STREAM_NS
   constexpr int NSF = (160 * 1024 - 4 * NG * 1024) / (4 * STAGE);
   constexpr int NS = NSF < MOE_STREAM_NS ? NSF : MOE_STREAM_NS;
@@ -173,6 +197,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
   constexpr int NC = GEMM1 ? NG / 2 * 16 : NG * 16;
   constexpr int NST = NG * NP;  // stages per column block
   static_assert(PC <= 1024 && (PC / 16) % 2 == 0, "row stride an odd number of 16-byte slots");
+  static_assert(STAGE % 16 == 0, "16-byte aligned stages");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[4][NS][STAGE];
   __shared__ f32x4 red[4][NG][64];
 
@@ -184,7 +209,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
   const int r16 = lane & 15, kg = lane >> 4;
   constexpr int qe = NJ * 32;  // this wave's K elements of each row
   const int k0 = wave * qe;
-  const size_t rowbytes = static_cast<size_t>(K) * 2;
+  const size_t rowbytes = static_cast<size_t>(K) * ES;
   const uint32_t sbase = lds_addr(&smem[wave][0][0]);
 
   for (long u = units * blockIdx.x / gridDim.x; u < u_end;) {
@@ -209,18 +234,22 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
     } else {
       arow = static_cast<const uint16_t*>(g.inter) + static_cast<size_t>(m0 + r16) * g.I;
     }
-    arow += k0 + 8 * kg;
+    arow += k0;
     u32x4 a[NJ];
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) a[j] = ld16(arow + 32 * j);
+    for (int j = 0; j < NJ; ++j) a[j] = ld16(arow + (F8 ? 128 * (j / 4) + 32 * kg + 8 * (j % 4) : 32 * j + 8 * kg));
     bool live[4];  // GEMM2: rows m0 + 4 kg + i that are routed rows (pads are never read)
 #pragma unroll
     for (int i = 0; i < 4; ++i) live[i] = GEMM1 || g.sorted_ids[m0 + 4 * kg + i] < g.n_routed;
     vm_wait<0>();
 
-    const uint8_t* wq = static_cast<const uint8_t*>(GEMM1 ? g.w1 : g.w2) +
-                        static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) * rowbytes + 2 * static_cast<size_t>(k0) +
-                        16 * lane;
+    const int NR = GEMM1 ? 2 * g.I : g.H;  // weight rows per expert
+    const uint8_t* wq = static_cast<const uint8_t*>(GEMM1 ? g.w1 : g.w2) + static_cast<size_t>(e) * NR * rowbytes +
+                        static_cast<size_t>(ES) * k0 + 16 * lane;
+    // fp8: scale row of the 128-row block, at this wave's first K block
+    const float* wsc = F8 ? static_cast<const float*>(GEMM1 ? g.w1_scale : g.w2_scale) +
+                                static_cast<size_t>(e) * (NR / 128) * (K / 128) + k0 / 128 + lane
+                          : nullptr;
     const int nsg = (cb1 - cb0) * NST;  // stages of this run
     // stage q of the run: block cb0 + q / NST, group gi, piece p
     auto issue = [&](int q) {
@@ -232,6 +261,9 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
       if (16 * lane < PC) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) dma16_nt(src + i * rowbytes, dst + i * ROWB);
+      }
+      if constexpr (F8) {  // the piece's JP / 4 block scales of the group's 128-row block
+        if (lane < JP / 4) dma4(wsc + static_cast<size_t>(wr / 128) * (K / 128) + p * (PC / 128), dst + 16 * ROWB);
       }
     };
 #pragma unroll
@@ -247,15 +279,33 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
         const int q = q0 + r, gi = r / NP, p = r % NP;
         // the copy NS-1 stages ahead goes into the buffer read out in stage q-1
         if (q + NS - 1 < nsg) issue(q + NS - 1);
-        // stage q has landed once at most the later stages' 16 copies each fly
-        if (NS >= 4 && q + 3 < nsg) vm_wait<48>();
-        else if (NS >= 3 && q + 2 < nsg) vm_wait<32>();
-        else if (q + 1 < nsg) vm_wait<16>();
+        // stage q has landed once at most the later stages' CPS copies each fly
+        if (NS >= 4 && q + 3 < nsg) vm_wait<3 * CPS>();
+        else if (NS >= 3 && q + 2 < nsg) vm_wait<2 * CPS>();
+        else if (q + 1 < nsg) vm_wait<CPS>();
         else vm_wait<0>();
-        const uint8_t* B = &smem[wave][0][0] + (q % NS) * STAGE + r16 * ROWB + 16 * kg;
+        const uint8_t* St = &smem[wave][0][0] + (q % NS) * STAGE;
+        if constexpr (F8) {
+          const uint8_t* B = St + r16 * ROWB + 32 * kg;
+          const float* sc = reinterpret_cast<const float*>(St + 16 * ROWB);
 #pragma unroll
-        for (int jj = 0; jj < JP; ++jj)
-          acc[gi] = mfma16x16x32(as_bf16x8(a[p * JP + jj]), as_bf16x8(ld16(B + 64 * jj)), acc[gi]);
+          for (int b = 0; b < JP / 4; ++b) {
+            const u32x4 w0 = ld16(B + 128 * b), w1 = ld16(B + 128 * b + 16);
+            f32x4 part = {};
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const u32x4& wv = u < 2 ? w0 : w1;
+              const bf16x8 bq = (u & 1) ? e4m3x8_to_bf16(wv.z, wv.w) : e4m3x8_to_bf16(wv.x, wv.y);
+              part = mfma16x16x32(as_bf16x8(a[p * JP + 4 * b + u]), bq, part);
+            }
+            acc[gi] += part * sc[b];
+          }
+        } else {
+          const uint8_t* B = St + r16 * ROWB + 16 * kg;
+#pragma unroll
+          for (int jj = 0; jj < JP; ++jj)
+            acc[gi] = mfma16x16x32(as_bf16x8(a[p * JP + jj]), as_bf16x8(ld16(B + 64 * jj)), acc[gi]);
+        }
         lds_wait();  // this stage's buffer is read out before a later copy lands in it
       }
 
@@ -310,17 +360,6 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
 // bf16 (v_cvt_pk_f32_fp8); the block's partial is scaled by the block's
 // fp32 scale and added to the accumulator.  The loads of block b+1 are in
 // flight while block b computes.
-__device__ __forceinline__ bf16x8 e4m3x8_to_bf16(uint32_t lo, uint32_t hi) {
-  bf16x8 r;
-  const auto f0 = __builtin_amdgcn_cvt_pk_f32_fp8(lo, false), f1 = __builtin_amdgcn_cvt_pk_f32_fp8(lo, true);
-  const auto f2 = __builtin_amdgcn_cvt_pk_f32_fp8(hi, false), f3 = __builtin_amdgcn_cvt_pk_f32_fp8(hi, true);
-  r[0] = static_cast<__bf16>(f0[0]); r[1] = static_cast<__bf16>(f0[1]);  // exact: e4m3 fits bf16
-  r[2] = static_cast<__bf16>(f1[0]); r[3] = static_cast<__bf16>(f1[1]);
-  r[4] = static_cast<__bf16>(f2[0]); r[5] = static_cast<__bf16>(f2[1]);
-  r[6] = static_cast<__bf16>(f3[0]); r[7] = static_cast<__bf16>(f3[1]);
-  return r;
-}
-
 template <int NSUB, bool GEMM1>
 __global__ __launch_bounds__(256) void gemm_w8a16_skinny(GroupedGemm g) {
   constexpr int BM = 16;
@@ -480,7 +519,7 @@ hipError_t launch_stream(const GroupedGemm& g, hipStream_t s) {
   const long units = static_cast<long>(g.max_rows / 16) * ((GEMM1 ? g.I : g.H) / NC);
   const dim3 grid(static_cast<unsigned>(std::max(1L, std::min<long>(stream_grid(), units))));
 #define MOE_STREAM_CASE(NP, JP) \
-  hipLaunchKernelGGL((gemm_bf16_stream<NG, NP, JP, GEMM1>), grid, dim3(256), 0, s, g)
+  hipLaunchKernelGGL((gemm_bf16_stream<0, NG, NP, JP, GEMM1>), grid, dim3(256), 0, s, g)
   const int qb = K / 2;  // bytes of a row per wave
   if (qb % 512 == 0) {   // 512-byte pieces
     switch (qb / 512) {
@@ -510,6 +549,35 @@ hipError_t launch_stream(const GroupedGemm& g, hipStream_t s) {
 #undef MOE_STREAM_CASE
   return hipGetLastError();
 }
+
+// fp8 weights (one byte per element): the wave's quarter of a row, K/4
+// bytes (whole 128-wide blocks), is one piece of up to 1 KB.  Above that
+// (K = 7168: two pieces) the 56 activation fragments a wave would hold spill
+// (measured 523 us against the skinny kernel's 385 us), so those shapes keep
+// the skinny kernel.
+template <int NG, bool GEMM1>
+hipError_t launch_stream_f8(const GroupedGemm& g, hipStream_t s) {
+  constexpr int NC = GEMM1 ? NG / 2 * 16 : NG * 16;
+  const int K = GEMM1 ? g.H : g.I;
+  const long units = static_cast<long>(g.max_rows / 16) * ((GEMM1 ? g.I : g.H) / NC);
+  const dim3 grid(static_cast<unsigned>(std::max(1L, std::min<long>(stream_grid(), units))));
+#define MOE_STREAM_CASE(JP) \
+  hipLaunchKernelGGL((gemm_bf16_stream<3, NG, 1, JP, GEMM1>), grid, dim3(256), 0, s, g)
+  switch (K / 512) {
+    case 1: MOE_STREAM_CASE(4); break;
+    case 2: MOE_STREAM_CASE(8); break;
+    case 3: MOE_STREAM_CASE(12); break;
+    case 4: MOE_STREAM_CASE(16); break;
+    case 5: MOE_STREAM_CASE(20); break;
+    case 6: MOE_STREAM_CASE(24); break;
+    case 7: MOE_STREAM_CASE(28); break;
+    default: MOE_STREAM_CASE(32); break;
+  }
+#undef MOE_STREAM_CASE
+  return hipGetLastError();
+}
+bool stream_fits_f8(int K, int N, int nc) { return MOE_STREAM && K % 512 == 0 && K <= 4096 && N % nc == 0; }
+
 // Streamed when each wave's quarter of a row is whole 512-byte pieces (K a
 // multiple of 1024, up to 4096) or one piece under 1 KB (K < 2048)
 bool stream_fits(int K, int N, int nc) {
@@ -545,12 +613,14 @@ hipError_t launch_gemm2_bf16(const GroupedGemm& g, hipStream_t s) {
 #define MOE_W8_NSUB 4
 #endif
 hipError_t launch_gemm1_w8a16(const GroupedGemm& g, hipStream_t s) {
+  if (stream_fits_f8(g.H, g.I, MOE_STREAM_NG1 / 2 * 16)) return launch_stream_f8<MOE_STREAM_NG1, true>(g, s);
   constexpr int NS = MOE_W8_NSUB;
   const dim3 grid(g.I / (NS / 2 * 16), g.max_rows / 16);
   hipLaunchKernelGGL((gemm_w8a16_skinny<NS, true>), grid, dim3(256), 0, s, g);
   return hipGetLastError();
 }
 hipError_t launch_gemm2_w8a16(const GroupedGemm& g, hipStream_t s) {
+  if (stream_fits_f8(g.I, g.H, MOE_STREAM_NG2 * 16)) return launch_stream_f8<MOE_STREAM_NG2, false>(g, s);
   constexpr int NS = MOE_W8_NSUB;
   const dim3 grid(g.H / (NS * 16), g.max_rows / 16);
   hipLaunchKernelGGL((gemm_w8a16_skinny<NS, false>), grid, dim3(256), 0, s, g);

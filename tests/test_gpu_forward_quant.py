@@ -207,6 +207,15 @@ def test_w8a16_ragged_k(dev):
     _check(synth.tiny_config(6, T=60, H=128, I=128, E=4, top_k=2))
 
 
+@pytest.mark.parametrize("H,I", [(512, 1024), (1024, 512), (2048, 3072), (4096, 1536), (5120, 2048)])
+def test_w8a16_streamed(dev, H, I):
+    # K a multiple of 512 up to 4096 takes the streamed kernel (one piece of
+    # K/4 bytes per wave and row, carrying its 128-wide block scales); K =
+    # 5120 the skinny one
+    cfg = synth.tiny_config(6, T=37, H=H, I=I, E=9, top_k=3)
+    _check(cfg, inp=_scale_blocks(synth.make_inputs(cfg), cfg.wfmt, seed=H + I))
+
+
 def test_w8a16_workload_full_size_sampled(dev):
     _check(synth.config(6), tokens=np.array([0, 5, 11, 15]))
 
