@@ -31,8 +31,10 @@ bincount, matmul, exp) and no blocking or fusion:
   combine   out[t] = sum_j w[t,j] * y[t,j].
 
 Quantisation points the kernels take are mirrored (``mirror=True``):
-  * bf16 / int4 weights, and fp8 weights with bf16 activations ("fp8a16",
-    the weight-only fp8 route): the intermediate ``a`` is rounded to fp32,
+  * bf16 / int4 weights, fp8 weights with bf16 activations ("fp8a16",
+    the weight-only fp8 route) and MXFP4 weights with bf16 activations
+    ("mxfp4": OCP MX E2M1 elements, E8M0 scale per 32 along K, two elements
+    per byte, low nibble first): the intermediate ``a`` is rounded to fp32,
     then to bf16 (round to nearest even) before the second product; the
     hidden rows enter exactly;
   * fp8: the hidden rows and the intermediate ``a`` are each quantised per
@@ -130,6 +132,33 @@ def int4_unpack(words: np.ndarray) -> np.ndarray:
     return _NIBBLES_LE16[by].view(np.int8).reshape(w.shape[:-1] + (w.shape[-1] * 8,))
 
 
+def _e2m1_value(c: np.ndarray) -> np.ndarray:
+    """Closed form of the OCP MX FP4 element E2M1: layout S.EE.M, exponent bias
+    1, E=0 encodes the subnormal M * 0.5; no infinities or NaN.  Magnitudes
+    0, 0.5, 1, 1.5, 2, 3, 4, 6."""
+    c = np.asarray(c).astype(np.int64) & 0xF
+    sign = np.where(c & 0x8, -1.0, 1.0)
+    e = (c >> 1) & 0x3
+    m = c & 0x1
+    return sign * np.where(e == 0, m * 0.5, (1.0 + m / 2.0) * np.ldexp(1.0, e - 1))
+
+
+_E2M1_TABLE = _e2m1_value(np.arange(16))
+
+
+def e8m0_value(s: np.ndarray) -> np.ndarray:
+    """OCP MX shared scale E8M0: 2^(s - 127) for s in [0, 254]; 255 is NaN."""
+    s = np.asarray(s).astype(np.int64)
+    return np.where(s == 255, np.nan, np.ldexp(1.0, s - 127))
+
+
+def mxfp4_unpack(packed: np.ndarray) -> np.ndarray:
+    """uint8 [..., K/2] -> E2M1 codes [..., K]: element 2b is the low nibble of
+    byte b, element 2b+1 its high nibble."""
+    b = np.asarray(packed).astype(np.uint8)
+    return np.stack([b & 0xF, b >> 4], axis=-1).reshape(b.shape[:-1] + (b.shape[-1] * 2,))
+
+
 def dequant_weight(wfmt: str, w: np.ndarray, scale) -> np.ndarray:
     """One expert's stored weight [N, K] (+ scales) -> exact float64 values."""
     if wfmt == "bf16":
@@ -144,6 +173,11 @@ def dequant_weight(wfmt: str, w: np.ndarray, scale) -> np.ndarray:
         N, K = q.shape
         s = bf16_to_f64(scale)                              # [N, K/128]
         return (q.reshape(N, K // QGROUP, QGROUP) * s[:, :, None]).reshape(N, K)
+    if wfmt == "mxfp4":                                 # E2M1 x E8M0 per 32 along K
+        q = _E2M1_TABLE[mxfp4_unpack(w)]                    # [N, K]
+        N, K = q.shape
+        s = e8m0_value(scale)                               # [N, K/32]
+        return (q.reshape(N, K // 32, 32) * s[:, :, None]).reshape(N, K)
     raise ValueError(f"unknown weight format {wfmt!r}")
 
 

@@ -28,6 +28,10 @@ Value recipe (the five workloads, plus a decode step on fp8 weights):
       - fp8:   per 128x128 block of [N, K]: s = max(amax, 1e-10) / 448 (fp32),
                q = e4m3fn(clamp(w / s, -448, 448)) (uint8 codes), scales fp32
                [E, N/128, K/128];
+      - mxfp4: per 32 along K (OCP MX): X = 2^(floor(log2 amax) - 2),
+               E2M1 codes of w / X (nearest, ties to even, saturated to 6),
+               two per byte low nibble first, uint8 [E, N, K/2]; E8M0 scale
+               bytes (127 + log2 X) uint8 [E, N, K/32];
       - int4:  per 128 along K: s = bf16(max(amax, 1e-10) / 7),
                q = clip(rint(w / s), -8, 7) signed two's complement nibble,
                zero point 0, packed 8 per int32 along K with element 8w+j in
@@ -63,6 +67,7 @@ class MoeConfig:
     I: int
     top_k: int
     wfmt: str = "bf16"          # "bf16" | "fp8" | "int4" | "fp8a16" (fp8 storage, bf16 activations)
+                                # | "mxfp4" (MX E2M1 + E8M0 per 32, bf16 activations)
     mode: str = "softmax"       # "softmax" | "sigmoid"
     renormalize: bool = True
     routed_scale: float = 1.0
@@ -92,6 +97,9 @@ CONFIGS = {
     # kept bf16 (the weight-only fp8 route)
     6: MoeConfig("fp8-decode", T=16, H=7168, E=256, I=2048, top_k=8, wfmt="fp8a16",
                  mode="sigmoid", routed_scale=2.5, sel_bias_std=0.1, seed=6),
+    # the same decode step with MXFP4 expert weights (bf16 activations)
+    7: MoeConfig("mxfp4-decode", T=16, H=7168, E=256, I=2048, top_k=8, wfmt="mxfp4",
+                 mode="sigmoid", routed_scale=2.5, sel_bias_std=0.1, seed=7),
 }
 
 
@@ -105,7 +113,7 @@ def tiny_config(n: int, **overrides) -> MoeConfig:
     kernels still see several tiles and a ragged tail."""
     base = CONFIGS[n]
     small = dict(T=77, H=384, E=8, I=256, top_k=min(base.top_k, 3))
-    if base.wfmt in ("fp8", "fp8a16"):
+    if base.wfmt in ("fp8", "fp8a16", "mxfp4"):
         small.update(E=16, top_k=4)
     if base.wfmt == "int4":
         small.update(E=12, top_k=4)
@@ -192,6 +200,32 @@ def _fp8_block_quant(w: np.ndarray):
     return q, s
 
 
+_E2M1_GRID = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])  # magnitude of codes 0..7
+
+
+def _mxfp4_quant(w: np.ndarray):
+    """[N,K] fp32 -> (uint8 [N,K/2] two E2M1 codes per byte, low nibble
+    first; uint8 E8M0 scales [N,K/32]).  Per 32-element block the OCP MX
+    rule: X = 2^(floor(log2 amax) - 2) (2 = the largest E2M1 exponent), the
+    elements w / X rounded to the nearest E2M1 magnitude (ties to the even
+    code) and saturated to 6.  An all-zero block takes X = 1."""
+    N, K = w.shape
+    blk = w.astype(np.float64).reshape(N, K // 32, 32)
+    amax = np.abs(blk).max(axis=2)
+    e = np.where(amax > 0, np.floor(np.log2(np.where(amax > 0, amax, 1.0))) - 2, 0).astype(np.int64)
+    e = np.clip(e, -126, 127)
+    x = blk / np.ldexp(1.0, e)[:, :, None]
+    a = np.minimum(np.abs(x), 6.0)
+    d = np.abs(a[..., None] - _E2M1_GRID)                   # [N, K/32, 32, 8]
+    idx = d.argmin(axis=-1)
+    nxt = np.minimum(idx + 1, 7)
+    tie = (np.take_along_axis(d, nxt[..., None], -1)[..., 0] == np.take_along_axis(d, idx[..., None], -1)[..., 0])
+    idx = np.where(tie & (idx % 2 == 1) & (nxt != idx), nxt, idx)
+    code = (idx | np.where(np.signbit(x) & (idx > 0), 8, 0)).astype(np.uint8).reshape(N, K)
+    packed = (code[:, 0::2] | (code[:, 1::2] << 4)).astype(np.uint8)
+    return packed, (e + 127).astype(np.uint8)
+
+
 def _int4_group_quant(w: np.ndarray):
     """[N,K] fp32 -> (int32 packed words [N,K/8], bf16-bit scales [N,K/128])."""
     N, K = w.shape
@@ -214,6 +248,8 @@ def _weight_arrays(cfg: MoeConfig, N: int, K: int, n_exp: int):
         return np.empty((n_exp, N, K), np.uint8), np.empty((n_exp, N // 128, K // 128), np.float32)
     if cfg.wfmt == "int4":
         return np.empty((n_exp, N, K // 8), np.int32), np.empty((n_exp, N, K // 128), np.uint16)
+    if cfg.wfmt == "mxfp4":
+        return np.empty((n_exp, N, K // 2), np.uint8), np.empty((n_exp, N, K // 32), np.uint8)
     raise ValueError(f"unknown weight format {cfg.wfmt!r}")
 
 
@@ -233,6 +269,8 @@ def make_expert_weights(cfg: MoeConfig, experts=None, threads=None, identical_ex
             dst[slot] = _bf16_bits(w)
         elif cfg.wfmt in ("fp8", "fp8a16"):
             dst[slot], dst_s[slot] = _fp8_block_quant(w)
+        elif cfg.wfmt == "mxfp4":
+            dst[slot], dst_s[slot] = _mxfp4_quant(w)
         else:
             dst[slot], dst_s[slot] = _int4_group_quant(w)
 

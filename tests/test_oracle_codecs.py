@@ -146,3 +146,64 @@ def test_act_quant_worked_groups():
     # every element is within half a grid step (relative 1/16) of its input
     nz = x != 0
     assert np.all(np.abs(dq[nz] - x[nz]) <= np.abs(x[nz]) / 16 + 1e-12)
+
+
+# ---------------------------------------------------------------- MXFP4 (OCP MX)
+def _e2m1_golden():
+    rows = [r for r in _rows("e2m1_ocp_table.txt") if r[0] != "e8m0"]
+    return {int(c, 16): float(v) for c, v in rows}
+
+
+def test_e2m1_decode_matches_ocp_table():
+    table = _e2m1_golden()
+    assert len(table) == 16
+    # every code in the low and in the high nibble, scale 2^0
+    for code, val in table.items():
+        packed = np.full((1, 16), code | (code << 4), np.uint8)
+        got = O.dequant_weight("mxfp4", packed, np.array([[127]], np.uint8))
+        assert np.all(got == val) and np.all(np.signbit(got) == (math.copysign(1, val) < 0)), code
+
+
+def test_e8m0_matches_table_and_torch():
+    for r in _rows("e2m1_ocp_table.txt"):
+        if r[0] != "e8m0":
+            continue
+        got = O.e8m0_value(np.array([int(r[1])]))[0]
+        assert (math.isnan(got) and r[2] == "nan") or got == float(r[2]), r
+    codes = np.arange(256, dtype=np.uint8)
+    ref = torch.from_numpy(codes).view(torch.float8_e8m0fnu).to(torch.float64).numpy()
+    ours = O.e8m0_value(codes)
+    assert np.array_equal(np.isnan(ours), np.isnan(ref)) and np.isnan(ref).sum() == 1
+    assert np.array_equal(ours[:255], ref[:255])
+
+
+def test_mxfp4_nibble_order_and_block_scales():
+    # byte 0x21: element 0 is the low nibble (code 1 = 0.5), element 1 the high (code 2 = 1.0)
+    packed = np.zeros((2, 32), np.uint8)
+    packed[0, 0] = 0x21
+    packed[1, 20] = 0xF7          # elements 40 (6.0) and 41 (-6.0), in the second block
+    scale = np.array([[127, 130], [125, 124]], np.uint8)
+    w = O.dequant_weight("mxfp4", packed, scale)
+    table = _e2m1_golden()
+    expect = np.zeros((2, 64))
+    for n in range(2):
+        for k in range(64):
+            b = int(packed[n, k // 2])
+            code = (b >> 4) if k % 2 else (b & 0xF)
+            expect[n, k] = table[code] * 2.0 ** (int(scale[n, k // 32]) - 127)
+    assert np.array_equal(w, expect)
+    assert w[0, 0] == 0.5 and w[0, 1] == 1.0 and w[1, 40] == 6.0 * 2.0 ** -3 and w[1, 41] == -6.0 * 2.0 ** -3
+
+
+def test_mxfp4_storage_encoder_roundtrip():
+    from synth import moe_inputs as M
+    rng = np.random.default_rng(5)
+    grid = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+    # blocks whose amax is exactly 4 * 2^e (so X = 2^e) with every element on the grid
+    v = rng.choice(grid, size=(3, 96)) * rng.choice([-1.0, 1.0], size=(3, 96))
+    v[:, ::32] = 4.0
+    ex = rng.integers(-6, 6, size=(3, 3))
+    w = (v.reshape(3, 3, 32) * np.ldexp(1.0, ex)[:, :, None]).reshape(3, 96).astype(np.float32)
+    packed, scale = M._mxfp4_quant(w)
+    assert np.array_equal(scale, (ex + 127).astype(np.uint8))
+    assert np.array_equal(O.dequant_weight("mxfp4", packed, scale), w.astype(np.float64))

@@ -93,7 +93,28 @@ def test_fp8_weights_bf16_activations_single_expert(mirror):
     assert np.max(np.abs(r["out"] - ref)) <= tol * rms
 
 
-@pytest.mark.parametrize("n", [1, 4, 5, 6])
+@pytest.mark.parametrize("mirror", [False, True])
+def test_mxfp4_weights_single_expert(mirror):
+    # MXFP4 weights with bf16 activations: E = 1, k = 1 is a dense SwiGLU on
+    # weights decoded here from the OCP E2M1 table and torch's E8M0 cast
+    cfg = synth.MoeConfig("dense4", T=33, H=256, E=1, I=128, top_k=1, wfmt="mxfp4", seed=13)
+    inp = synth.make_inputs(cfg)
+    r = O.forward(cfg, inp, mirror=mirror)
+    e2m1 = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0, -0.0, -0.5, -1.0, -1.5, -2.0, -3.0, -4.0, -6.0])
+
+    def deq(packed, s):
+        codes = np.stack([packed & 0xF, packed >> 4], axis=-1).reshape(packed.shape[0], -1)
+        sc = torch.from_numpy(np.ascontiguousarray(s)).view(torch.float8_e8m0fnu).to(torch.float64).numpy()
+        return e2m1[codes] * np.repeat(sc, 32, axis=1)
+
+    x = torch.from_numpy(inp["hidden"].view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    ref = _dense_torch(x, deq(inp["w1"][0], inp["w1_scale"][0]), deq(inp["w2"][0], inp["w2_scale"][0]), mirror)
+    rms = np.sqrt((ref ** 2).mean())
+    tol = 1e-12 if not mirror else 2 ** -8
+    assert np.max(np.abs(r["out"] - ref)) <= tol * rms
+
+
+@pytest.mark.parametrize("n", [1, 4, 5, 6, 7])
 def test_identical_experts_any_routing(n):
     cfg = synth.tiny_config(n)
     inp = synth.make_inputs(cfg, identical_experts=True)
@@ -104,7 +125,7 @@ def test_identical_experts_any_routing(n):
     assert np.max(np.abs(r["out"] - ref)) <= 1e-12 * np.sqrt((ref ** 2).mean())
 
 
-@pytest.mark.parametrize("n", [1, 4, 5, 6])
+@pytest.mark.parametrize("n", [1, 4, 5, 6, 7])
 def test_token_order_invariance(n):
     cfg = synth.tiny_config(n)
     inp = synth.make_inputs(cfg)
@@ -156,7 +177,7 @@ def _brute_layer(cfg, inp, mirror):
     return np.array(outs)
 
 
-@pytest.mark.parametrize("n", [1, 4, 5, 6])
+@pytest.mark.parametrize("n", [1, 4, 5, 6, 7])
 @pytest.mark.parametrize("mirror", [False, True])
 def test_brute_force_tiny(n, mirror):
     cfg = synth.tiny_config(n, T=9, H=256, I=128, E=6, top_k=3)
