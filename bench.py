@@ -40,7 +40,7 @@ sys.path.insert(0, ROOT)
 METRIC = "fused-MoE layer TFLOP/s (active FLOPs) + µs/layer; fraction of MFMA/HBM peak"
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0}
-W_BYTES = {"bf16": 2.0, "fp8": 1.0, "int4": 0.5, "fp8a16": 1.0}
+W_BYTES = {"bf16": 2.0, "fp8": 1.0, "int4": 0.5, "fp8a16": 1.0, "mxfp4": 0.5}
 DESCR = {
     1: "tiny MoE layer: T=64 H=256 E=8 I=128 top_k=2, bf16 weights, softmax top-2 renormalised",
     2: "decode-shaped MoE layer: T=16 H=4096 E=64 I=1408 top_k=6, bf16 weights, softmax top-6 renormalised",
@@ -51,6 +51,8 @@ DESCR = {
        "Zipf(1.1)-skewed softmax top-8",
     6: "weight-only fp8 decode MoE layer: T=16 H=7168 E=256 I=2048 top_k=8, e4m3 128x128 weights, "
        "bf16 activations, sigmoid+bias top-8 x2.5",
+    7: "MXFP4 decode MoE layer: T=16 H=7168 E=256 I=2048 top_k=8, OCP MX E2M1 weights with E8M0 "
+       "scales per 32, bf16 activations, sigmoid+bias top-8 x2.5",
 }
 
 
@@ -137,7 +139,7 @@ def cpu_baseline(cfg, inputs, budget_s: float):
 
 def gemm1_kernel_match(name: str) -> bool:
     """True for the GEMM1 (+SiLU*up) kernel of any format / variant."""
-    decode = ("gemm_bf16_skinny<", "gemm_bf16_stream<", "gemm_w8a16_skinny<")
+    decode = ("gemm_bf16_skinny<", "gemm_bf16_stream<", "gemm_w8a16_skinny<", "gemm_w4a16_skinny<")
     return (any(k in name for k in decode) and "true>" in name) or \
            ("moe_gemm_tiled<" in name and ", true," in name)
 
@@ -277,8 +279,8 @@ def main():
     # GEMM1 per launch: W1 of every active expert (+ its scales), hidden read
     # once, the SwiGLU intermediate written once
     w1_scale_bytes = {"bf16": 0, "fp8": 2 * I * H / (128 * 128) * 4, "int4": 2 * I * H / 128 * 2,
-                      "fp8a16": 2 * I * H / (128 * 128) * 4}[cfg.wfmt]
-    act_bytes = {"bf16": 2, "fp8": 1, "int4": 2, "fp8a16": 2}[cfg.wfmt]
+                      "fp8a16": 2 * I * H / (128 * 128) * 4, "mxfp4": 2 * I * H / 32}[cfg.wfmt]
+    act_bytes = {"bf16": 2, "fp8": 1, "int4": 2, "fp8a16": 2, "mxfp4": 2}[cfg.wfmt]
     g1_bytes = n_active * (2 * I * H * wb + w1_scale_bytes) + T * H * (1 if cfg.wfmt == "fp8" else 2) + n * I * act_bytes
     g1_flops = 2.0 * n * H * 2 * I
     g1_us = float(np.mean(g1_launch_us))
@@ -306,7 +308,7 @@ def main():
     if args.cpu_seconds > 0:
         base = cpu_baseline(cfg, inputs, args.cpu_seconds)
 
-    dtype = {"bf16": "bf16", "fp8": "fp8e4m3", "int4": "bf16", "fp8a16": "bf16"}[cfg.wfmt]
+    dtype = {"bf16": "bf16", "fp8": "fp8e4m3", "int4": "bf16", "fp8a16": "bf16", "mxfp4": "bf16"}[cfg.wfmt]
     rec = {
         "metric": METRIC,
         "value": flops / (ms * 1e-3) / 1e12,

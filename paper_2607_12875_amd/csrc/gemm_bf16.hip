@@ -153,6 +153,9 @@ __device__ __forceinline__ bf16x8 e4m3x8_to_bf16(uint32_t lo, uint32_t hi) {
 #ifndef MOE_STREAM_NS
 #define MOE_STREAM_NS 4
 #endif
+#ifndef MOE_STREAM_F4_HALF
+#define MOE_STREAM_F4_HALF 1
+#endif
 // The decode GEMMs read every weight byte once, so they are bound by how
 // fast HBM delivers the weight slab.  The skinny kernel above walks 16 rows
 // per load instruction (64 bytes of each, at the row stride); this one reads
@@ -181,16 +184,28 @@ __device__ __forceinline__ bf16x8 e4m3x8_to_bf16(uint32_t lo, uint32_t hi) {
 // partial is scaled into the accumulator.
 // NG: 16-row weight groups per block (GEMM1: NG/2 gate + NG/2 up); NP
 // pieces of JP MFMAs (32 K elements each) per row and wave: K = 4 * 32 * NP * JP.
-template <int FMT, int NG, int NP, int JP, bool GEMM1>
-__global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
-  constexpr bool F8 = FMT == 3;
-  constexpr int ES = F8 ? 1 : 2;                     // weight bytes per element
-  constexpr int PC = 32 * ES * JP, ROWB = PC + 16;  // piece bytes, LDS row stride
-  constexpr int STAGE = 16 * ROWB + (F8 ? 64 : 0);  // + the piece's block scales
-  constexpr int CPS = F8 ? 17 : 16;                 // copy instructions per stage
-  static_assert(!F8 || JP % 4 == 0, "fp8 pieces are whole 128-wide scale blocks");
+__device__ __forceinline__ u32x4 mxfp4x8_to_bf16(uint32_t w, float sc) {
+  // byte b of w holds elements 2b (low nibble) and 2b+1; each result word is
+  // the bf16 pair (element 2b, element 2b+1) -- taken as a whole word
+  u32x4 r;
+  r.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 0));
+  r.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 1));
+  r.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 2));
+  r.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 3));
+  return r;
+}
+
+template <int FMT, int NWV, int NG, int NP, int JP, bool GEMM1>
+__global__ __launch_bounds__(64 * NWV) void gemm_bf16_stream(GroupedGemm g) {
+  constexpr bool F8 = FMT == 3, F4 = FMT == 4;
+  constexpr int B32 = F8 ? 32 : (F4 ? 16 : 64);     // weight bytes per 32 elements
+  constexpr int PC = B32 * JP, ROWB = PC + 16;      // piece bytes, LDS row stride
+  constexpr int NSI = F4 ? (JP + 15) / 16 : (F8 ? 1 : 0);  // scale copy instructions per stage
+  constexpr int STAGE = 16 * ROWB + (F8 ? 64 : 0) + (F4 ? ((16 * JP + 15) / 16) * 16 : 0);
+  constexpr int CPS = 16 + NSI;                     // copy instructions per stage
+  static_assert(!(F8 || F4) || JP % 4 == 0, "pieces are whole 128-wide blocks");
   // stage buffers per wave: as many as LDS holds beside the reduction, up to MOE_STREAM_NS
-  constexpr int NSF = (160 * 1024 - 4 * NG * 1024) / (4 * STAGE);
+  constexpr int NSF = (160 * 1024 - NWV * NG * 1024) / (NWV * STAGE);
   constexpr int NS = NSF < MOE_STREAM_NS ? NSF : MOE_STREAM_NS;
   static_assert(NS >= 2, "two stage buffers per wave");
   constexpr int NJ = NP * JP;   // MFMAs over the quarter
@@ -198,8 +213,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
   constexpr int NST = NG * NP;  // stages per column block
   static_assert(PC <= 1024 && (PC / 16) % 2 == 0, "row stride an odd number of 16-byte slots");
   static_assert(STAGE % 16 == 0, "16-byte aligned stages");
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[4][NS][STAGE];
-  __shared__ f32x4 red[4][NG][64];
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[NWV][NS][STAGE];
+  __shared__ f32x4 red[NWV][NG][64];
 
   const int N = GEMM1 ? g.I : g.H, K = GEMM1 ? g.H : g.I;
   const int nb = N / NC;                                           // column blocks per row tile
@@ -209,7 +224,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
   const int r16 = lane & 15, kg = lane >> 4;
   constexpr int qe = NJ * 32;  // this wave's K elements of each row
   const int k0 = wave * qe;
-  const size_t rowbytes = static_cast<size_t>(K) * ES;
+  const size_t rowbytes = static_cast<size_t>(K) / 32 * B32;
   const uint32_t sbase = lds_addr(&smem[wave][0][0]);
 
   for (long u = units * blockIdx.x / gridDim.x; u < u_end;) {
@@ -237,7 +252,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
     arow += k0;
     u32x4 a[NJ];
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) a[j] = ld16(arow + (F8 ? 128 * (j / 4) + 32 * kg + 8 * (j % 4) : 32 * j + 8 * kg));
+    for (int j = 0; j < NJ; ++j)
+      a[j] = ld16(arow + ((F8 || F4) ? 128 * (j / 4) + 32 * kg + 8 * (j % 4) : 32 * j + 8 * kg));
     bool live[4];  // GEMM2: rows m0 + 4 kg + i that are routed rows (pads are never read)
 #pragma unroll
     for (int i = 0; i < 4; ++i) live[i] = GEMM1 || g.sorted_ids[m0 + 4 * kg + i] < g.n_routed;
@@ -245,11 +261,15 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
 
     const int NR = GEMM1 ? 2 * g.I : g.H;  // weight rows per expert
     const uint8_t* wq = static_cast<const uint8_t*>(GEMM1 ? g.w1 : g.w2) + static_cast<size_t>(e) * NR * rowbytes +
-                        static_cast<size_t>(ES) * k0 + 16 * lane;
+                        static_cast<size_t>(k0) / 32 * B32 + 16 * lane;
     // fp8: scale row of the 128-row block, at this wave's first K block
     const float* wsc = F8 ? static_cast<const float*>(GEMM1 ? g.w1_scale : g.w2_scale) +
                                 static_cast<size_t>(e) * (NR / 128) * (K / 128) + k0 / 128 + lane
                           : nullptr;
+    // MXFP4: the expert's E8M0 bytes [NR][K/32], at this wave's first 32-block
+    const uint8_t* wsc4 = F4 ? static_cast<const uint8_t*>(GEMM1 ? g.w1_scale : g.w2_scale) +
+                                   static_cast<size_t>(e) * NR * (K / 32) + k0 / 32
+                             : nullptr;
     const int nsg = (cb1 - cb0) * NST;  // stages of this run
     // stage q of the run: block cb0 + q / NST, group gi, piece p
     auto issue = [&](int q) {
@@ -264,6 +284,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
       }
       if constexpr (F8) {  // the piece's JP / 4 block scales of the group's 128-row block
         if (lane < JP / 4) dma4(wsc + static_cast<size_t>(wr / 128) * (K / 128) + p * (PC / 128), dst + 16 * ROWB);
+      }
+      if constexpr (F4) {  // the piece's JP scale bytes of each of the 16 rows, [row][JP] in LDS
+#pragma unroll
+        for (int c = 0; c < NSI; ++c) {
+          const int gi4 = 64 * c + lane, row = gi4 / (JP / 4), dw = gi4 % (JP / 4);
+          if (row < 16)
+            dma4(wsc4 + static_cast<size_t>(wr + row) * (K / 32) + p * JP + 4 * dw, dst + 16 * ROWB + 256 * c);
+        }
       }
     };
 #pragma unroll
@@ -285,7 +313,20 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
         else if (q + 1 < nsg) vm_wait<CPS>();
         else vm_wait<0>();
         const uint8_t* St = &smem[wave][0][0] + (q % NS) * STAGE;
-        if constexpr (F8) {
+        if constexpr (F4) {
+          const uint8_t* B = St + r16 * ROWB + 16 * kg;
+          const uint8_t* sc = St + 16 * ROWB + r16 * JP + kg;  // E8M0 of (row, 32-block 4 b + kg)
+#pragma unroll
+          for (int b = 0; b < JP / 4; ++b) {
+            const u32x4 wv = ld16(B + 64 * b);
+            const float scf = __uint_as_float(static_cast<uint32_t>(sc[4 * b]) << 23);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const uint32_t w = u == 0 ? wv.x : (u == 1 ? wv.y : (u == 2 ? wv.z : wv.w));
+              acc[gi] = mfma16x16x32(as_bf16x8(a[p * JP + 4 * b + u]), as_bf16x8(mxfp4x8_to_bf16(w, scf)), acc[gi]);
+            }
+          }
+        } else if constexpr (F8) {
           const uint8_t* B = St + r16 * ROWB + 32 * kg;
           const float* sc = reinterpret_cast<const float*>(St + 16 * ROWB);
 #pragma unroll
@@ -318,14 +359,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
       auto sum = [&](int gi) {
         f32x4 v = red[0][gi][lane];
 #pragma unroll
-        for (int w = 1; w < 4; ++w) v += red[w][gi][lane];
+        for (int w = 1; w < NWV; ++w) v += red[w][gi][lane];
         return v;
       };
       // D element i of a 16x16 tile is (row 4*(lane/16) + i, col lane%16)
       if (GEMM1) {
 #pragma unroll
         for (int gi = 0; gi < NG / 2; ++gi) {
-          if (gi % 4 != wave) continue;
+          if (gi % NWV != wave) continue;
           const f32x4 gt = sum(gi), up = sum(gi + NG / 2);
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
@@ -337,7 +378,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(GroupedGemm g) {
       } else {
 #pragma unroll
         for (int gi = 0; gi < NG; ++gi) {
-          if (gi % 4 != wave) continue;
+          if (gi % NWV != wave) continue;
           const f32x4 v = sum(gi);
 #pragma unroll
           for (int i = 0; i < 4; ++i)
@@ -471,6 +512,136 @@ __global__ __launch_bounds__(256) void gemm_w8a16_skinny(GroupedGemm g) {
   }
 }
 
+// ------------------------------------------------ skinny, MXFP4 weights
+// The decode kernel on MXFP4 weights (OCP MX: E2M1 codes, two per byte, low
+// nibble first; one E8M0 scale byte per 32 along K) with bf16 activations:
+// the weight-only fp8 kernel's structure (16-row tile, K split over the four
+// waves in 128-wide blocks; inside a block lane group kg takes elements
+// [32 kg, 32 kg + 32), 16 bytes of each weight row, and the matching 64
+// bytes of its activation row).  Those 32 elements share one E8M0 scale, so
+// v_cvt_scalef32_pk_bf16_fp4 decodes each code pair straight to bf16 with
+// the scale applied (exact: a code times a power of two; the instruction
+// takes the f32 scale's exponent field, which is the E8M0 byte itself).
+
+template <int NSUB, int UB, bool GEMM1>
+__global__ __launch_bounds__(256) void gemm_w4a16_skinny(GroupedGemm g) {
+  constexpr int BM = 16;
+  constexpr int BN = GEMM1 ? NSUB / 2 * 16 : NSUB * 16;
+  __shared__ f32x4 red[3][NSUB][64];
+
+  const int m0 = blockIdx.y * BM;
+  if (m0 >= g.offsets[g.E]) return;
+  const int e = find_segment(g.offsets, g.E, m0);
+  const int n0 = blockIdx.x * BN;
+  const int K = GEMM1 ? g.H : g.I;
+  const int NR = GEMM1 ? 2 * g.I : g.H;  // weight rows of one expert
+  const int lane = lane_id(), wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+
+  const uint16_t* arow;
+  if (GEMM1) {
+    const int sid = g.sorted_ids[m0 + r16];
+    const int tok = sid < g.n_routed ? sid / g.top_k : 0;
+    arow = static_cast<const uint16_t*>(g.x) + static_cast<size_t>(tok) * g.H;
+  } else {
+    arow = static_cast<const uint16_t*>(g.inter) + static_cast<size_t>(m0 + r16) * g.I;
+  }
+  arow += kg * 32;
+  const uint8_t* wbase = static_cast<const uint8_t*>(GEMM1 ? g.w1 : g.w2) + static_cast<size_t>(e) * NR * (K / 2);
+  const uint8_t* sbase = static_cast<const uint8_t*>(GEMM1 ? g.w1_scale : g.w2_scale) +
+                         static_cast<size_t>(e) * NR * (K / 32);
+  const uint8_t* brow[NSUB];
+  const uint32_t* srow[NSUB];  // the four scale bytes of each 128-wide block, one word
+#pragma unroll
+  for (int s = 0; s < NSUB; ++s) {
+    int n;
+    if (GEMM1) n = s < NSUB / 2 ? n0 + s * 16 + r16 : g.I + n0 + (s - NSUB / 2) * 16 + r16;
+    else n = n0 + s * 16 + r16;
+    brow[s] = wbase + static_cast<size_t>(n) * (K / 2) + kg * 16;
+    srow[s] = reinterpret_cast<const uint32_t*>(sbase + static_cast<size_t>(n) * (K / 32));
+  }
+
+  f32x4 acc[NSUB];
+#pragma unroll
+  for (int s = 0; s < NSUB; ++s) acc[s] = f32x4{};
+  const int nb = K / 128, lb = nb / 4, lr = nb % 4;
+  const int bbeg = wave * lb + min(wave, lr);
+  const int bend = bbeg + lb + (wave < lr ? 1 : 0);
+
+  // UB blocks per pipeline stage: a block of MXFP4 is half the bytes of an
+  // fp8 one, so two are loaded together to keep as many bytes in flight
+  u32x4 a0[UB][4], b0[UB][NSUB], a1[UB][4], b1[UB][NSUB];
+  uint32_t s0[UB][NSUB], s1[UB][NSUB];
+#define MOE_W4_LOAD(A, Bv, Sv, blk)                                                               \
+  do {                                                                                            \
+    _Pragma("unroll") for (int v = 0; v < UB; ++v) {                                            \
+      const int bb = min((blk) + v, bend - 1); /* a short last stage re-reads its last block */   \
+      _Pragma("unroll") for (int u = 0; u < 4; ++u) A[v][u] = ld16(arow + bb * 128 + u * 8);     \
+      _Pragma("unroll") for (int s = 0; s < NSUB; ++s) {                                        \
+        Bv[v][s] = ld16(brow[s] + bb * 64);                                                      \
+        Sv[v][s] = srow[s][bb];                                                                   \
+      }                                                                                           \
+    }                                                                                             \
+  } while (0)
+#define MOE_W4_MMA(A, Bv, Sv, blk)                                                                \
+  do {                                                                                            \
+    _Pragma("unroll") for (int v = 0; v < UB; ++v) {                                            \
+      if ((blk) + v >= bend) break;                                                               \
+      _Pragma("unroll") for (int s = 0; s < NSUB; ++s) {                                        \
+        const float sc = __uint_as_float(((Sv[v][s] >> (8 * kg)) & 0xFFu) << 23);                 \
+        _Pragma("unroll") for (int u = 0; u < 4; ++u) {                                         \
+          const u32x4& bw = Bv[v][s];                                                             \
+          const uint32_t w = u == 0 ? bw.x : (u == 1 ? bw.y : (u == 2 ? bw.z : bw.w));            \
+          acc[s] = mfma16x16x32(as_bf16x8(A[v][u]), as_bf16x8(mxfp4x8_to_bf16(w, sc)), acc[s]);  \
+        }                                                                                         \
+      }                                                                                           \
+    }                                                                                             \
+  } while (0)
+  int b = bbeg;
+  if (b < bend) MOE_W4_LOAD(a0, b0, s0, b);
+  for (; b + UB < bend; b += 2 * UB) {
+    MOE_W4_LOAD(a1, b1, s1, b + UB);
+    MOE_W4_MMA(a0, b0, s0, b);
+    if (b + 2 * UB < bend) MOE_W4_LOAD(a0, b0, s0, b + 2 * UB);
+    MOE_W4_MMA(a1, b1, s1, b + UB);
+  }
+  if (b < bend) MOE_W4_MMA(a0, b0, s0, b);
+#undef MOE_W4_LOAD
+#undef MOE_W4_MMA
+
+  if (wave > 0) {
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s) red[wave - 1][s][lane] = acc[s];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int s = 0; s < NSUB; ++s)
+#pragma unroll
+    for (int w = 0; w < 3; ++w) acc[s] += red[w][s][lane];
+
+  // D element i of a 16x16 tile is (row 4*(lane/16) + i, col lane%16)
+  if (GEMM1) {
+#pragma unroll
+    for (int s = 0; s < NSUB / 2; ++s)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = m0 + 4 * kg + i, col = n0 + s * 16 + r16;
+        static_cast<uint16_t*>(g.inter)[static_cast<size_t>(row) * g.I + col] =
+            f32_to_bf16(silu_mul(acc[s][i], acc[s + NSUB / 2][i]));
+      }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = m0 + 4 * kg + i;
+      if (g.sorted_ids[row] >= g.n_routed) continue;  // pad rows are never read
+#pragma unroll
+      for (int s = 0; s < NSUB; ++s)
+        static_cast<float*>(g.y)[static_cast<size_t>(row) * g.H + n0 + s * 16 + r16] = acc[s][i];
+    }
+  }
+}
+
 // ----------------------------------------------------------------- dispatch
 bool bf16_use_skinny(int T, int top_k, int E) {
   return static_cast<long>(T) * top_k <= 32L * E;  // <= 32 rows per expert on average
@@ -519,7 +690,7 @@ hipError_t launch_stream(const GroupedGemm& g, hipStream_t s) {
   const long units = static_cast<long>(g.max_rows / 16) * ((GEMM1 ? g.I : g.H) / NC);
   const dim3 grid(static_cast<unsigned>(std::max(1L, std::min<long>(stream_grid(), units))));
 #define MOE_STREAM_CASE(NP, JP) \
-  hipLaunchKernelGGL((gemm_bf16_stream<0, NG, NP, JP, GEMM1>), grid, dim3(256), 0, s, g)
+  hipLaunchKernelGGL((gemm_bf16_stream<0, 4, NG, NP, JP, GEMM1>), grid, dim3(256), 0, s, g)
   const int qb = K / 2;  // bytes of a row per wave
   if (qb % 512 == 0) {   // 512-byte pieces
     switch (qb / 512) {
@@ -562,7 +733,7 @@ hipError_t launch_stream_f8(const GroupedGemm& g, hipStream_t s) {
   const long units = static_cast<long>(g.max_rows / 16) * ((GEMM1 ? g.I : g.H) / NC);
   const dim3 grid(static_cast<unsigned>(std::max(1L, std::min<long>(stream_grid(), units))));
 #define MOE_STREAM_CASE(JP) \
-  hipLaunchKernelGGL((gemm_bf16_stream<3, NG, 1, JP, GEMM1>), grid, dim3(256), 0, s, g)
+  hipLaunchKernelGGL((gemm_bf16_stream<3, 4, NG, 1, JP, GEMM1>), grid, dim3(256), 0, s, g)
   switch (K / 512) {
     case 1: MOE_STREAM_CASE(4); break;
     case 2: MOE_STREAM_CASE(8); break;
@@ -577,6 +748,57 @@ hipError_t launch_stream_f8(const GroupedGemm& g, hipStream_t s) {
   return hipGetLastError();
 }
 bool stream_fits_f8(int K, int N, int nc) { return MOE_STREAM && K % 512 == 0 && K <= 4096 && N % nc == 0; }
+
+// MXFP4 weights (half a byte per element): one piece per wave and row, the
+// wave's K range = K / NWV elements held as activation fragments (at most
+// 32); four waves up to K = 4096, eight (K in eighths) up to 7168 (at 8192
+// eight waves' two stage buffers no longer fit LDS beside the reduction).
+template <int NG, bool GEMM1>
+hipError_t launch_stream_f4(const GroupedGemm& g, hipStream_t s) {
+  constexpr int NC = GEMM1 ? NG / 2 * 16 : NG * 16;
+  const int K = GEMM1 ? g.H : g.I;
+  const long units = static_cast<long>(g.max_rows / 16) * ((GEMM1 ? g.I : g.H) / NC);
+  const dim3 grid(static_cast<unsigned>(std::max(1L, std::min<long>(stream_grid(), units))));
+#define MOE_STREAM_CASE(NWV, JP) \
+  hipLaunchKernelGGL((gemm_bf16_stream<4, NWV, NG, 1, JP, GEMM1>), grid, dim3(64 * NWV), 0, s, g)
+  if (MOE_STREAM_F4_HALF && K <= 2048) {
+    // two waves (K in halves): pieces twice as long, twice the workgroups
+    const dim3 grid2(static_cast<unsigned>(std::max(1L, std::min<long>(2L * stream_grid(), units))));
+#define MOE_STREAM_CASE2(JP) \
+    hipLaunchKernelGGL((gemm_bf16_stream<4, 2, NG, 1, JP, GEMM1>), grid2, dim3(128), 0, s, g)
+    switch (K / 512) {
+      case 1: MOE_STREAM_CASE2(8); break;
+      case 2: MOE_STREAM_CASE2(16); break;
+      case 3: MOE_STREAM_CASE2(24); break;
+      default: MOE_STREAM_CASE2(32); break;
+    }
+#undef MOE_STREAM_CASE2
+    return hipGetLastError();
+  }
+  if (K <= 4096) {
+    switch (K / 512) {
+      case 1: MOE_STREAM_CASE(4, 4); break;
+      case 2: MOE_STREAM_CASE(4, 8); break;
+      case 3: MOE_STREAM_CASE(4, 12); break;
+      case 4: MOE_STREAM_CASE(4, 16); break;
+      case 5: MOE_STREAM_CASE(4, 20); break;
+      case 6: MOE_STREAM_CASE(4, 24); break;
+      case 7: MOE_STREAM_CASE(4, 28); break;
+      default: MOE_STREAM_CASE(4, 32); break;
+    }
+  } else {
+    switch (K / 1024) {
+      case 5: MOE_STREAM_CASE(8, 20); break;
+      case 6: MOE_STREAM_CASE(8, 24); break;
+      default: MOE_STREAM_CASE(8, 28); break;
+    }
+  }
+#undef MOE_STREAM_CASE
+  return hipGetLastError();
+}
+bool stream_fits_f4(int K, int N, int nc) {
+  return MOE_STREAM && K % 512 == 0 && K <= 7168 && (K <= 4096 || K % 1024 == 0) && N % nc == 0;
+}
 
 // Streamed when each wave's quarter of a row is whole 512-byte pieces (K a
 // multiple of 1024, up to 4096) or one piece under 1 KB (K < 2048)
@@ -617,6 +839,27 @@ hipError_t launch_gemm1_w8a16(const GroupedGemm& g, hipStream_t s) {
   constexpr int NS = MOE_W8_NSUB;
   const dim3 grid(g.I / (NS / 2 * 16), g.max_rows / 16);
   hipLaunchKernelGGL((gemm_w8a16_skinny<NS, true>), grid, dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+// MXFP4 weights (decode route; the host guarantees T*k <= 32*E)
+#ifndef MOE_W4_NSUB
+#define MOE_W4_NSUB 4
+#endif
+#ifndef MOE_W4_UB
+#define MOE_W4_UB 2
+#endif
+hipError_t launch_gemm1_w4a16(const GroupedGemm& g, hipStream_t s) {
+  if (stream_fits_f4(g.H, g.I, MOE_STREAM_NG1 / 2 * 16)) return launch_stream_f4<MOE_STREAM_NG1, true>(g, s);
+  constexpr int NS = MOE_W4_NSUB;
+  const dim3 grid(g.I / (NS / 2 * 16), g.max_rows / 16);
+  hipLaunchKernelGGL((gemm_w4a16_skinny<NS, MOE_W4_UB, true>), grid, dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+hipError_t launch_gemm2_w4a16(const GroupedGemm& g, hipStream_t s) {
+  if (stream_fits_f4(g.I, g.H, MOE_STREAM_NG2 * 16)) return launch_stream_f4<MOE_STREAM_NG2, false>(g, s);
+  constexpr int NS = MOE_W4_NSUB;
+  const dim3 grid(g.H / (NS * 16), g.max_rows / 16);
+  hipLaunchKernelGGL((gemm_w4a16_skinny<NS, MOE_W4_UB, false>), grid, dim3(256), 0, s, g);
   return hipGetLastError();
 }
 hipError_t launch_gemm2_w8a16(const GroupedGemm& g, hipStream_t s) {

@@ -6,7 +6,7 @@ import torch
 import paper_2607_12875_amd as moe
 import synth
 
-TOL = {"bf16": 2e-2, "fp8": 6e-2, "int4": 8e-2, "fp8a16": 2e-2}   # max|err| <= TOL * rms(oracle out)
+TOL = {"bf16": 2e-2, "fp8": 6e-2, "int4": 8e-2, "fp8a16": 2e-2, "mxfp4": 2e-2}   # max|err| <= TOL * rms(oracle out)
 
 
 def require_gpu():

@@ -179,15 +179,17 @@ def _scale_blocks(inp, wfmt, seed=1):
     rng = np.random.default_rng(seed)
     out = dict(inp)
     for k in ("w1_scale", "w2_scale"):
-        f = 2.0 ** rng.integers(-3, 4, size=inp[k].shape)
+        d = rng.integers(-3, 4, size=inp[k].shape)
         if wfmt == "int4":      # bf16 bits
-            out[k] = O.f32_to_bf16_rne((O.bf16_to_f64(inp[k]) * f).astype(np.float32))
+            out[k] = O.f32_to_bf16_rne((O.bf16_to_f64(inp[k]) * 2.0 ** d).astype(np.float32))
+        elif wfmt == "mxfp4":   # E8M0 exponent bytes
+            out[k] = (inp[k].astype(np.int64) + d).astype(np.uint8)
         else:                   # fp32
-            out[k] = (inp[k] * f).astype(np.float32)
+            out[k] = (inp[k] * 2.0 ** d).astype(np.float32)
     return out
 
 
-@pytest.mark.parametrize("wcfg", [4, 5, 6])
+@pytest.mark.parametrize("wcfg", [4, 5, 6, 7])
 def test_block_scales_vary(dev, wcfg):
     cfg = synth.tiny_config(wcfg, T=100, H=512, I=1024 if wcfg == 4 else 256, E=8, top_k=2)
     _check(cfg, inp=_scale_blocks(synth.make_inputs(cfg), cfg.wfmt))
@@ -226,3 +228,36 @@ def test_w8a16_large_batch_rejected(dev):
     with pytest.raises(moe.MoeError) as ei:
         run_forward(cfg, inp)
     assert ei.value.status == 3   # MOE_ERR_UNSUPPORTED
+
+
+# ---- MXFP4 weights (OCP MX E2M1 + E8M0 per 32), bf16 activations: a decode route
+@pytest.mark.parametrize("T", [1, 5, 16, 33, 128])
+def test_mxfp4_small(dev, T):
+    # T = 128: T * top_k = 512 = 32 * E, the largest batch the route accepts
+    _check(synth.tiny_config(7, T=T, H=512, I=256, E=16, top_k=4))
+
+
+def test_mxfp4_ragged_and_minimum_k(dev):
+    # H = I = 384: three 128-wide blocks over four waves; H = I = 128: one
+    _check(synth.tiny_config(7, T=40, H=384, I=384, E=8, top_k=3))
+    _check(synth.tiny_config(7, T=60, H=128, I=128, E=4, top_k=2))
+
+
+@pytest.mark.parametrize("H,I", [(512, 1024), (1536, 2048), (3072, 2560), (4096, 512), (5120, 1536), (7168, 3584)])
+def test_mxfp4_streamed(dev, H, I):
+    # K a multiple of 512: the streamed kernel splits K over two waves up to
+    # 2048, four up to 4096 and eight up to 7168; every piece carries its
+    # rows' E8M0 bytes (randomised here by up to 2^+-3)
+    cfg = synth.tiny_config(7, T=37, H=H, I=I, E=9, top_k=3)
+    _check(cfg, inp=_scale_blocks(synth.make_inputs(cfg), cfg.wfmt, seed=H + I))
+
+
+def test_mxfp4_workload_full_size_sampled(dev):
+    _check(synth.config(7), tokens=np.array([0, 6, 9, 15]))
+
+
+def test_mxfp4_large_batch_rejected(dev):
+    cfg = synth.tiny_config(7, T=129, H=256, I=128, E=16, top_k=4)
+    with pytest.raises(moe.MoeError) as ei:
+        run_forward(cfg, synth.make_inputs(cfg))
+    assert ei.value.status == 3
