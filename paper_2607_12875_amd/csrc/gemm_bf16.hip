@@ -153,6 +153,9 @@ __device__ __forceinline__ bf16x8 e4m3x8_to_bf16(uint32_t lo, uint32_t hi) {
 #ifndef MOE_STREAM_NS
 #define MOE_STREAM_NS 4
 #endif
+#ifndef MOE_STREAM_OCC
+#define MOE_STREAM_OCC 1  // workgroups per CU the stage buffers are sized for
+#endif
 #ifndef MOE_STREAM_F4_HALF
 #define MOE_STREAM_F4_HALF 1
 #endif
@@ -205,7 +208,9 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_stream(GroupedGemm g) {
   constexpr int CPS = 16 + NSI;                     // copy instructions per stage
   static_assert(!(F8 || F4) || JP % 4 == 0, "pieces are whole 128-wide blocks");
   // stage buffers per wave: as many as LDS holds beside the reduction, up to MOE_STREAM_NS
-  constexpr int NSF = (160 * 1024 - NWV * NG * 1024) / (NWV * STAGE);
+  constexpr int RED = (NWV - 1) * NG * 1024;  // bytes of the reduction buffer
+  constexpr int NSO = (160 * 1024 / MOE_STREAM_OCC - RED) / (NWV * STAGE);
+  constexpr int NSF = NSO >= 2 ? NSO : (160 * 1024 - RED) / (NWV * STAGE);
   constexpr int NS = NSF < MOE_STREAM_NS ? NSF : MOE_STREAM_NS;
   static_assert(NS >= 2, "two stage buffers per wave");
   constexpr int NJ = NP * JP;   // MFMAs over the quarter
@@ -214,7 +219,7 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_stream(GroupedGemm g) {
   static_assert(PC <= 1024 && (PC / 16) % 2 == 0, "row stride an odd number of 16-byte slots");
   static_assert(STAGE % 16 == 0, "16-byte aligned stages");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NWV][NS][STAGE];
-  __shared__ f32x4 red[NWV][NG][64];
+  __shared__ f32x4 red[NWV - 1][NG][64];  // partials of waves 1.. for wave 0
 
   const int N = GEMM1 ? g.I : g.H, K = GEMM1 ? g.H : g.I;
   const int nb = N / NC;                                           // column blocks per row tile
@@ -350,23 +355,26 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_stream(GroupedGemm g) {
         lds_wait();  // this stage's buffer is read out before a later copy lands in it
       }
 
-      // reduce the four K quarters (in wave order); wave w finishes groups w, w+4, ...
+      // reduce the K slices in wave order; wave 0 finishes every group (the
+      // other waves go on with the next block's stages)
+      if (wave > 0) {
 #pragma unroll
-      for (int gi = 0; gi < NG; ++gi) red[wave][gi][lane] = acc[gi];
+        for (int gi = 0; gi < NG; ++gi) red[wave - 1][gi][lane] = acc[gi];
+      }
       lds_wait();
       bar();
       const int n0 = cb * NC;
       auto sum = [&](int gi) {
-        f32x4 v = red[0][gi][lane];
+        f32x4 v = acc[gi];
 #pragma unroll
-        for (int w = 1; w < NWV; ++w) v += red[w][gi][lane];
+        for (int w = 1; w < NWV; ++w) v += red[w - 1][gi][lane];
         return v;
       };
       // D element i of a 16x16 tile is (row 4*(lane/16) + i, col lane%16)
       if (GEMM1) {
 #pragma unroll
         for (int gi = 0; gi < NG / 2; ++gi) {
-          if (gi % NWV != wave) continue;
+          if (wave != 0) break;
           const f32x4 gt = sum(gi), up = sum(gi + NG / 2);
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
@@ -378,7 +386,7 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_stream(GroupedGemm g) {
       } else {
 #pragma unroll
         for (int gi = 0; gi < NG; ++gi) {
-          if (gi % NWV != wave) continue;
+          if (wave != 0) break;
           const f32x4 v = sum(gi);
 #pragma unroll
           for (int i = 0; i < 4; ++i)
@@ -674,7 +682,7 @@ bool bf16_use_skinny(int T, int top_k, int E) {
 #endif
 
 int stream_grid() {
-  static const int cus = [] {
+  static const int cus = MOE_STREAM_OCC * [] {
     int dev = 0, n = 0;
     if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
       n = 256;
