@@ -75,7 +75,9 @@ __device__ __forceinline__ int swz(int r) { return KB == 128 ? (r >> 1) & 7 : (r
 // (L1 waiting on L2) cannot hold up the MFMA stream behind an in-order copy
 // instruction.  NP == 0: the math waves issue the copies themselves.
 template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM, int KBT = 128, int STAGES = 3, int NP = 0>
-__global__ __launch_bounds__((WM * WN + NP) * 64) void moe_gemm_tiled(GroupedGemm g) {
+// int4 GEMM1 is held to 128 registers, which keeps two workgroups per CU.
+__global__ __launch_bounds__((WM * WN + NP) * 64) __attribute__((amdgpu_waves_per_eu(FMT == 2 && GEMM1 ? 4 : 1)))
+void moe_gemm_tiled(GroupedGemm g) {
   constexpr int NW = WM * WN, NT = (NW + NP) * 64;
   constexpr int LW = NP > 0 ? NP : NW;  // waves that issue the copies
   static_assert(NW == 4 || NW == 8, "four or eight math waves");
@@ -109,6 +111,8 @@ __global__ __launch_bounds__((WM * WN + NP) * 64) void moe_gemm_tiled(GroupedGem
   __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES][STAGE];
   __shared__ float lds_amax[FMT == 1 && GEMM1 ? WN : 1][FMT == 1 && GEMM1 ? BM : 1];
   __shared__ int lds_off[MOE_MAX_EXPERTS_DEV + 1];  // expert_offsets, read once per workgroup
+  // GEMM1 copy waves: the next tile's row ids, one slot per copy wave
+  __shared__ int lds_sid[GEMM1 && NP > 0 ? NP : 1][GEMM1 && NP > 0 ? BM : 1];
 
   const int tid = threadIdx.x, lane = lane_id(), wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -133,43 +137,76 @@ __global__ __launch_bounds__((WM * WN + NP) * 64) void moe_gemm_tiled(GroupedGem
   const int t_end = min(total, (xcd + 1) * chunk);
   const uint32_t smem0 = lds_addr(&smem[0][0]);
 
-  for (int t = xcd * chunk + slot; t < t_end; t += per_xcd) {
-    // Logical tile order: expert by expert; inside expert e (row tiles
-    // [base, base+cnt)) chunks of at most GM row tiles, each chunk swept
-    // column tile by column tile with its row tiles adjacent.  Workgroups
-    // running together then share one expert's weight slab and a few row tiles.
-    const int e = find_segment(lds_off, g.E, (t / n_tiles_n) * BM);
+  // Logical tile order: expert by expert; inside expert e (row tiles
+  // [base, base+cnt)) chunks of at most GM row tiles, each chunk swept
+  // column tile by column tile with its row tiles adjacent.  Workgroups
+  // running together then share one expert's weight slab and a few row tiles.
+  auto coords = [&](int t, int& e, int& m0, int& n0) {
+    e = find_segment(lds_off, g.E, (t / n_tiles_n) * BM);
     const int base = lds_off[e] / BM, cnt = (lds_off[e + 1] - lds_off[e]) / BM;
     const int local = t - base * n_tiles_n;
     const int c = local / (GM * n_tiles_n), within = local % (GM * n_tiles_n);
     const int sz = min(GM, cnt - c * GM);
     const int mt = base + c * GM + within % sz, nt = within / sz;
-    const int m0 = mt * BM, n0 = nt * NC;
-    __syncthreads();  // the previous tile's last stages are no longer read
+    m0 = mt * BM;
+    n0 = nt * NC;
+  };
 
-    // ---- per-lane DMA sources.  Instruction i of copy wave lw fills the 1 KB
+  constexpr int NSL = SC > 0 ? SC : 1;
+  struct Src {
+    const uint8_t* a[A_CH];  // A rows
+    const uint8_t* b[B_CH];  // B rows
+    const uint8_t* s[NSL];   // scale words
+    int ss[NSL];             // scale advance per step
+  };
+  // staged: the tile's BM row ids are in this copy wave's lds_sid slot (else
+  // they are read from sorted_ids)
+  auto sources = [&](int e, int m0, int n0, Src& src, bool staged) {
+    // per-lane DMA sources of the tile.  Instruction i of copy wave lw fills the 1 KB
     // block (i*LW + lw) of a stage: 8 rows of A / of fp8-bf16 B (lane -> row
     // l/8, 16-byte slot l%8) or 32 rows of int4 B (row l/2, slot l%2).  Slot s
     // of row r holds the row's chunk s ^ swz<KB>(r), the XOR swizzle the
     // fragment reads undo.
-    const uint8_t* a_src[A_CH];
+    // GEMM1 gathers its A rows by token: every row id this lane needs (A rows,
+    // fp8 row scales) is requested before the first is used, so the tile
+    // pays one memory round trip.  Pad rows (id n_routed) read the last
+    // token instead; their products are never read.
+    int sid[A_CH + NSL];
+    if constexpr (GEMM1) {
+#pragma unroll
+      for (int i = 0; i < A_CH; ++i) {
+        const int r = (i * LW + lw) * RPI + lane / LPR;
+        if constexpr (NP > 0) sid[i] = staged ? lds_sid[lw][r] : g.sorted_ids[m0 + r];
+        else sid[i] = g.sorted_ids[m0 + r];
+      }
+#pragma unroll
+      for (int k = 0; k < NSL; ++k) {
+        const int r = (lw + k * LW) * 64 + lane;
+        int v = 0;
+        if (FMT == 1 && lw + k * LW < BM / 64) {
+          if constexpr (NP > 0) v = staged ? lds_sid[lw][r] : g.sorted_ids[m0 + r];
+          else v = g.sorted_ids[m0 + r];
+        }
+        sid[A_CH + k] = v;
+      }
+    }
+    auto token = [&](int v) {
+      return static_cast<size_t>(static_cast<unsigned>(min(v, g.n_routed - 1)) / static_cast<unsigned>(g.top_k));
+    };
 #pragma unroll
     for (int i = 0; i < A_CH; ++i) {
       const int r = (i * LW + lw) * RPI + lane / LPR;
       const uint8_t* row;
       if (GEMM1) {
-        const int sid = g.sorted_ids[m0 + r];
-        const int tok = sid < g.n_routed ? sid / g.top_k : 0;
-        row = static_cast<const uint8_t*>(g.x) + static_cast<size_t>(tok) * g.H * (FMT == 1 ? 1 : 2);
+        row = static_cast<const uint8_t*>(g.x) + token(sid[i]) * g.H * (FMT == 1 ? 1 : 2);
       } else {
         row = static_cast<const uint8_t*>(g.inter) + static_cast<size_t>(m0 + r) * g.I * (FMT == 1 ? 1 : 2);
       }
-      a_src[i] = row + (((lane % LPR) ^ swz<KB>(r)) << 4);
+      src.a[i] = row + (((lane % LPR) ^ swz<KB>(r)) << 4);
     }
     const size_t w_row_bytes = FMT == 0 ? K * 2 : (FMT == 1 ? K : K / 2);
     const uint8_t* wbase = static_cast<const uint8_t*>(GEMM1 ? g.w1 : g.w2) +
                            static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) * w_row_bytes;
-    const uint8_t* b_src[B_CH];
 #pragma unroll
     for (int i = 0; i < B_CH; ++i) {
       const int blk = i * LW + lw;
@@ -178,38 +215,33 @@ __global__ __launch_bounds__((WM * WN + NP) * 64) void moe_gemm_tiled(GroupedGem
       int n;
       if (GEMM1) n = r < NC ? n0 + r : g.I + n0 + (r - NC);
       else n = n0 + r;
-      b_src[i] = wbase + static_cast<size_t>(n) * w_row_bytes + (sl << 4);
+      src.b[i] = wbase + static_cast<size_t>(n) * w_row_bytes + (sl << 4);
     }
     // scale DMA sources of this lane, one per slot lw + k*LW (advanced by one
     // K block / half group per step); slots without a scale role load a
     // harmless dummy
-    constexpr int NSL = SC > 0 ? SC : 1;
-    const uint8_t* s_src[NSL];
-    int s_step[NSL];
 #pragma unroll
     for (int k = 0; k < NSL; ++k) {
       const int sl = lw + k * LW;
-      s_src[k] = a_src[0];
-      s_step[k] = 0;
+      src.s[k] = src.a[0];
+      src.ss[k] = 0;
       if constexpr (FMT == 1) {
         if (sl < BM / 64) {
           const int r = sl * 64 + lane;
           if (GEMM1) {
-            const int sid = g.sorted_ids[m0 + r];
-            const int tok = sid < g.n_routed ? sid / g.top_k : 0;
-            s_src[k] = reinterpret_cast<const uint8_t*>(g.x_scale + static_cast<size_t>(tok) * (g.H / 128));
+            src.s[k] = reinterpret_cast<const uint8_t*>(g.x_scale + token(sid[A_CH + k]) * (g.H / 128));
           } else {
-            s_src[k] = reinterpret_cast<const uint8_t*>(g.inter_scale + static_cast<size_t>(m0 + r) * (g.I / 128));
+            src.s[k] = reinterpret_cast<const uint8_t*>(g.inter_scale + static_cast<size_t>(m0 + r) * (g.I / 128));
           }
-          s_step[k] = 4;
+          src.ss[k] = 4;
         } else if (sl == BM / 64) {
           // lane l: block row of W (GEMM1: l odd -> up half, even -> gate half;
           // GEMM2: block row n0/128 + l % (BNW/128))
           const float* wsc = static_cast<const float*>(GEMM1 ? g.w1_scale : g.w2_scale) +
                              static_cast<size_t>(e) * ((GEMM1 ? 2 * g.I : g.H) / 128) * (K / 128);
           const int br = GEMM1 ? ((lane & 1) ? (g.I + n0) / 128 : n0 / 128) : n0 / 128 + lane % (BNW / 128);
-          s_src[k] = reinterpret_cast<const uint8_t*>(wsc + static_cast<size_t>(br) * (K / 128));
-          s_step[k] = 4;
+          src.s[k] = reinterpret_cast<const uint8_t*>(wsc + static_cast<size_t>(br) * (K / 128));
+          src.ss[k] = 4;
         }
       } else if constexpr (FMT == 2) {
         if (sl < BNW / 64) {
@@ -217,41 +249,124 @@ __global__ __launch_bounds__((WM * WN + NP) * 64) void moe_gemm_tiled(GroupedGem
           const int n = GEMM1 ? (r < NC ? n0 + r : g.I + n0 + (r - NC)) : n0 + r;
           // bf16 scale [n][group] of K step kt sits at element n*(K/128) + kt/2;
           // the dword holding it starts at the even element below
-          s_src[k] = reinterpret_cast<const uint8_t*>(static_cast<const uint16_t*>(GEMM1 ? g.w1_scale : g.w2_scale) +
+          src.s[k] = reinterpret_cast<const uint8_t*>(static_cast<const uint16_t*>(GEMM1 ? g.w1_scale : g.w2_scale) +
                                                       (static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) + n) * (K / 128));
-          s_step[k] = 1;  // advanced per step in elements below
+          src.ss[k] = 1;  // advanced per step in elements below
         }
       }
     }
+  };
 
-    // issue stage kt (DMA q in [q0, q1) of this copy wave's A_CH + B_CH tile
-    // loads for one K step, plus the scale loads with q1 == N_DMA) into buffer kt % STAGES
-    auto issue_part = [&](int kt, int q0, int q1) {
-      const uint32_t base = smem0 + (kt % STAGES) * STAGE;
+  // issue step kt of the tile `src` describes (DMA q in [q0, q1) of this copy
+  // wave's A_CH + B_CH tile loads, plus the scale loads with q1 == N_DMA)
+  // into LDS buffer `buf`
+  auto issue_part = [&](const Src& src, int kt, int buf, int q0, int q1) {
+    const uint32_t base = smem0 + buf * STAGE;
 #pragma unroll
-      for (int i = 0; i < A_CH; ++i)
-        if (i >= q0 && i < q1) dma16(a_src[i] + kt * KB, base + (i * LW + lw) * 1024);
+    for (int i = 0; i < A_CH; ++i)
+      if (i >= q0 && i < q1) dma16(src.a[i] + kt * KB, base + (i * LW + lw) * 1024);
 #pragma unroll
-      for (int i = 0; i < B_CH; ++i)
-        if (A_CH + i >= q0 && A_CH + i < q1) dma16(b_src[i] + kt * BB, base + A_BYTES + (i * LW + lw) * 1024);
-      if (q1 < N_DMA) return;
+    for (int i = 0; i < B_CH; ++i)
+      if (A_CH + i >= q0 && A_CH + i < q1) dma16(src.b[i] + kt * BB, base + A_BYTES + (i * LW + lw) * 1024);
+    if (q1 < N_DMA) return;
 #pragma unroll
-      for (int k = 0; k < SC; ++k) {
-        const uint32_t dst = base + A_BYTES + B_BYTES + (lw + k * LW) * 256;
-        if constexpr (FMT == 1) {
-          dma4(s_src[k] + kt * s_step[k], dst);
-        } else if constexpr (FMT == 2) {
-          // element offset kt/2 within the row, rounded down to an even element (4-byte aligned)
-          const uint8_t* p = s_src[k];
-          if (s_step[k]) {
-            const uintptr_t a = reinterpret_cast<uintptr_t>(s_src[k]) + (kt >> 1) * 2;
-            p = reinterpret_cast<const uint8_t*>(a & ~static_cast<uintptr_t>(3));
-          }
-          dma4(p, dst);
+    for (int k = 0; k < SC; ++k) {
+      const uint32_t dst = base + A_BYTES + B_BYTES + (lw + k * LW) * 256;
+      if constexpr (FMT == 1) {
+        dma4(src.s[k] + kt * src.ss[k], dst);
+      } else if constexpr (FMT == 2) {
+        // element offset kt/2 within the row, rounded down to an even element (4-byte aligned)
+        const uint8_t* p = src.s[k];
+        if (src.ss[k]) {
+          const uintptr_t a = reinterpret_cast<uintptr_t>(src.s[k]) + (kt >> 1) * 2;
+          p = reinterpret_cast<const uint8_t*>(a & ~static_cast<uintptr_t>(3));
         }
+        dma4(p, dst);
       }
-    };
-    auto issue = [&](int kt) { issue_part(kt, 0, N_DMA); };
+    }
+  };
+  auto issue = [&](const Src& src, int kt, int buf) { issue_part(src, kt, buf, 0, N_DMA); };
+  // this copy wave's loads for a step have landed once at most `ahead`
+  // later steps (N_DMA loads each) are still in flight
+  auto wait_ahead = [&](int ahead) {
+    if constexpr (STAGES >= 6) { if (ahead >= 4) { vm_wait<4 * N_DMA>(); return; } }
+    if constexpr (STAGES >= 5) { if (ahead == 3) { vm_wait<3 * N_DMA>(); return; } }
+    if constexpr (STAGES >= 4) { if (ahead == 2) { vm_wait<2 * N_DMA>(); return; } }
+    if constexpr (STAGES >= 3) { if (ahead == 1) { vm_wait<N_DMA>(); return; } }
+    vm_wait<0>();
+  };
+
+  // K steps are numbered across this workgroup's tiles, and step s of the
+  // sequence lives in LDS buffer s % STAGES; `sb` is the buffer of a tile's
+  // step 0.  STAGES-1 steps are loaded ahead: step s+STAGES-1 goes into the
+  // buffer read in step s-1, issued once the barrier of step s shows every
+  // wave is past it.  With copy waves the next tile's first STAGES-1 steps
+  // are issued right after the barrier of the current tile's last step (their
+  // buffers were read in earlier steps), so they load during that step and
+  // the epilogue; without, each tile starts with a barrier and the math
+  // waves load its first steps themselves.
+  const int t0 = xcd * chunk + slot;
+  Src cur;
+  if constexpr (NP > 0) {
+    if (!is_math) {
+      // copy waves: one barrier per step, the same sequence as the math waves
+      if (t0 < t_end) {
+        int e, m0, n0;
+        coords(t0, e, m0, n0);
+        sources(e, m0, n0, cur, false);
+#pragma unroll
+        for (int q = 0; q < STAGES - 1; ++q)
+          if (q < nk) issue(cur, q, q);
+      }
+      // the next tile's sources are computed in step kc; its row ids (GEMM1),
+      // copied to this wave's LDS slot ahead of step STAGES-1's loads, have
+      // landed by then: in-order completion, and the wait of step kt covers
+      // every load issued before step kt+1 (all of them in the last step)
+      const int kc = min(STAGES - 2, nk - 1);
+      for (int t = t0, sb = 0; t < t_end; t += per_xcd, sb = (sb + nk) % STAGES) {
+        const int tn = t + per_xcd;
+        const bool next = tn < t_end;
+        Src nxt;
+        int en = 0, m0n = 0, n0n = 0;
+        if (next) {
+          coords(tn, en, m0n, n0n);
+          if constexpr (GEMM1) {
+#pragma unroll
+            for (int q = 0; q < BM / 64; ++q) dma4(g.sorted_ids + m0n + q * 64 + lane, lds_addr(&lds_sid[lw][q * 64]));
+          }
+        }
+        for (int kt = 0; kt < nk; ++kt) {
+          wait_ahead(min(STAGES - 2, nk - 1 - kt));
+          bar();
+          const int j = kt + STAGES - 1;
+          if (j < nk) issue(cur, j, (sb + j) % STAGES);
+          if (next && kt == kc) sources(en, m0n, n0n, nxt, true);
+          if (next && kt == nk - 1) {
+#pragma unroll
+            for (int q = 0; q < STAGES - 1; ++q)
+              if (q < nk) issue(nxt, q, (sb + nk + q) % STAGES);
+          }
+        }
+        if constexpr (FMT == 1 && GEMM1) {  // the two barriers of the requant epilogue
+          bar();
+          bar();
+        }
+        if (next) cur = nxt;
+      }
+      return;
+    }
+  }
+
+  for (int t = t0, sb = 0; t < t_end; t += per_xcd, sb = (sb + nk) % STAGES) {
+    int e, m0, n0;
+    coords(t, e, m0, n0);
+    if constexpr (NP == 0) {
+      __syncthreads();  // the previous tile's buffers are no longer read
+      sources(e, m0, n0, cur, false);
+#pragma unroll
+      for (int q = 0; q < STAGES - 1; ++q)
+        if (q < nk) issue(cur, q, (sb + q) % STAGES);
+    }
 
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -263,37 +378,6 @@ __global__ __launch_bounds__((WM * WN + NP) * 64) void moe_gemm_tiled(GroupedGem
 #define brow(j) (GEMM1 ? ((j) < TN / 2 ? wn * (WTN / 2) + (j) * 32 : NC + wn * (WTN / 2) + ((j) - TN / 2) * 32) \
                        : wn * WTN + (j) * 32)
 
-    // STAGES-1 steps are loaded ahead; step kt+STAGES-1 goes into the buffer
-    // read in step kt-1, once the barrier shows every wave is past it.
-    // stage kt has landed in this copy wave once at most `ahead` later stages fly
-    auto wait_landed = [&](int kt) {
-      const int ahead = min(STAGES - 2, nk - 1 - kt);  // stages issued after kt
-      if constexpr (STAGES >= 6) { if (ahead >= 4) { vm_wait<4 * N_DMA>(); return; } }
-      if constexpr (STAGES >= 5) { if (ahead == 3) { vm_wait<3 * N_DMA>(); return; } }
-      if constexpr (STAGES >= 4) { if (ahead == 2) { vm_wait<2 * N_DMA>(); return; } }
-      if constexpr (STAGES >= 3) { if (ahead == 1) { vm_wait<N_DMA>(); return; } }
-      vm_wait<0>();
-    };
-    if (is_loader) {
-#pragma unroll
-      for (int q = 0; q < STAGES - 1; ++q)
-        if (q < nk) issue(q);
-    }
-    if constexpr (NP > 0) {
-      if (!is_math) {
-        // copy waves: the same one barrier per step as the math loop below
-        for (int kt = 0; kt < nk; ++kt) {
-          wait_landed(kt);
-          bar();
-          if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
-        }
-        if constexpr (FMT == 1 && GEMM1) {  // the two barriers of the requant epilogue
-          __syncthreads();
-          __syncthreads();
-        }
-        continue;  // no epilogue
-      }
-    }
     if constexpr (NP > 0 && FMT == 0) {
       // Math waves of a split bf16 launch: fragments are read one MFMA K
       // substep ahead into a double buffer.  The barrier for stage kt+1 sits
@@ -304,7 +388,7 @@ __global__ __launch_bounds__((WM * WN + NP) * 64) void moe_gemm_tiled(GroupedGem
       static_assert(NKK % 2 == 0, "substep parity");
       bf16x8 fa[2][TM], fb[2][TN];
       auto read_frags = [&](int kt, int kk, int buf) {
-        const uint8_t* As = &smem[kt % STAGES][0];
+        const uint8_t* As = &smem[(sb + kt) % STAGES][0];
         const uint8_t* Bs = As + A_BYTES;
         const int ch = 2 * kk + kg;
 #pragma unroll
@@ -341,11 +425,11 @@ __global__ __launch_bounds__((WM * WN + NP) * 64) void moe_gemm_tiled(GroupedGem
       }
     }
     for (int kt = 0; kt < nk && !(NP > 0 && FMT == 0); ++kt) {
-      if constexpr (NP == 0) wait_landed(kt);
+      if constexpr (NP == 0) wait_ahead(min(STAGES - 2, nk - 1 - kt));
       bar();  // every stage-kt copy of every copy wave has landed
       const bool pre = NP == 0 && kt + STAGES - 1 < nk;  // this wave starts a later stage
-      if (FMT != 0 && pre) issue(kt + STAGES - 1);
-      const uint8_t* As = &smem[kt % STAGES][0];
+      if (FMT != 0 && pre) issue(cur, kt + STAGES - 1, (sb + kt + STAGES - 1) % STAGES);
+      const uint8_t* As = &smem[(sb + kt) % STAGES][0];
       const uint8_t* Bs = As + A_BYTES;
       const uint8_t* Ss = Bs + B_BYTES;
       if constexpr (FMT == 0) {
@@ -377,7 +461,7 @@ __global__ __launch_bounds__((WM * WN + NP) * 64) void moe_gemm_tiled(GroupedGem
 #pragma unroll
             for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(af[kk][i], bfr[kk][j], acc[i][j]);
           __builtin_amdgcn_sched_barrier(0);
-          if (pre) issue_part(kt + STAGES - 1, kk * PER, min((kk + 1) * PER, A_CH + B_CH));
+          if (pre) issue_part(cur, kt + STAGES - 1, (sb + kt + STAGES - 1) % STAGES, kk * PER, min((kk + 1) * PER, A_CH + B_CH));
           __builtin_amdgcn_sched_barrier(0);
         }
       } else if constexpr (FMT == 1 && NP > 0) {
