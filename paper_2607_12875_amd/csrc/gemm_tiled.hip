@@ -36,21 +36,6 @@ namespace moe {
 constexpr int kXcds = 8;
 constexpr int MOE_MAX_EXPERTS_DEV = 1024;  // the ABI's expert limit
 
-template <int FMT>
-struct FmtTraits;
-template <>
-struct FmtTraits<0> {  // bf16
-  static constexpr int KE = 64, BB = 128;
-};
-template <>
-struct FmtTraits<1> {  // fp8
-  static constexpr int KE = 128, BB = 128;
-};
-template <>
-struct FmtTraits<2> {  // int4 weights, bf16 activations
-  static constexpr int KE = 64, BB = 32;
-};
-
 // 8 signed nibbles -> 8 bf16 values q * s (s an fp32 copy of a bf16 scale).
 __device__ __forceinline__ bf16x8 dequant_int4x8(uint32_t w, float s) {
   bf16x8 r;
@@ -66,9 +51,14 @@ __device__ __forceinline__ bf16x8 dequant_int4x8(uint32_t w, float s) {
 // chunk c in slot c ^ swz<KB>(r).  For the fragment reads (32 consecutive rows,
 // lanes l and l+32 on neighbouring chunks of one row) (r >> 1) & 7 measured
 // 1.6x the LDS read throughput of r & 7 on gfx950.
-// With 64-byte rows (4 chunks) the analogous choice is (r >> 2) & 3.
+// With 64-byte rows (4 chunks) the analogous choice is (r >> 2) & 3; a
+// 256-byte row spans all 64 banks, so there the slot alone must tell 16
+// consecutive rows apart: r & 15.
 template <int KB>
-__device__ __forceinline__ int swz(int r) { return KB == 128 ? (r >> 1) & 7 : (r >> 2) & 3; }
+__device__ __forceinline__ int swz(int r) { return KB == 256 ? r & 15 : KB == 128 ? (r >> 1) & 7 : (r >> 2) & 3; }
+// int4 B rows (32 or 64 bytes: 2 or 4 chunks)
+template <int BB>
+__device__ __forceinline__ int swz_b(int r) { return BB == 32 ? (r >> 2) & 1 : (r >> 2) & 3; }
 
 // NP > 0: NP extra waves only issue the global->LDS copies and the NW math
 // waves never touch global memory in the main loop, so a stalled load queue
@@ -83,10 +73,12 @@ void moe_gemm_tiled(GroupedGemm g) {
   static_assert(NW == 4 || NW == 8, "four or eight math waves");
   static_assert(NP == 0 || NW % NP == 0, "scale slots split evenly over the copy waves");
   static_assert(NP == 0 || WM * WN == 4, "split launches have one math wave per SIMD");
-  static_assert(KBT == 128 || (KBT == 64 && FMT == 0), "64-byte steps are bf16 only");
+  static_assert(KBT == 128 || (KBT == 64 && FMT == 0) || (KBT == 256 && FMT == 2),
+                "64-byte steps are bf16 only, 256-byte steps int4 only");
   constexpr int KB = KBT;                                       // A bytes per row per step
-  constexpr int KE = FMT == 0 ? KB / 2 : FmtTraits<FMT>::KE;   // K elements per step
-  constexpr int BB = FMT == 0 ? KB : FmtTraits<FMT>::BB;       // B bytes per row per step
+  constexpr int KE = FMT == 1 ? KB : KB / 2;                          // K elements per step
+  constexpr int BB = FMT == 0 ? KB : (FMT == 1 ? KB : KB / 4);        // B bytes per row per step
+  constexpr int LPB = BB / 16;                                         // lanes per int4 B row in a copy
   constexpr int RPI = 1024 / KB, LPR = KB / 16;  // rows per DMA instruction, lanes per row
   constexpr int WTM = BM / WM, WTN = BNW / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -163,10 +155,10 @@ void moe_gemm_tiled(GroupedGemm g) {
   // they are read from sorted_ids)
   auto sources = [&](int e, int m0, int n0, Src& src, bool staged) {
     // per-lane DMA sources of the tile.  Instruction i of copy wave lw fills the 1 KB
-    // block (i*LW + lw) of a stage: 8 rows of A / of fp8-bf16 B (lane -> row
-    // l/8, 16-byte slot l%8) or 32 rows of int4 B (row l/2, slot l%2).  Slot s
-    // of row r holds the row's chunk s ^ swz<KB>(r), the XOR swizzle the
-    // fragment reads undo.
+    // block (i*LW + lw) of a stage: 1024/KB rows of A / of fp8-bf16 B (KB/16
+    // lanes per row, one 16-byte slot each) or 64/LPB rows of int4 B (LPB
+    // lanes per row).  Slot s of row r holds the row's chunk s ^ swz(r), the
+    // XOR swizzle the fragment reads undo.
     // GEMM1 gathers its A rows by token: every row id this lane needs (A rows,
     // fp8 row scales) is requested before the first is used, so the tile
     // pays one memory round trip.  Pad rows (id n_routed) read the last
@@ -210,8 +202,8 @@ void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
     for (int i = 0; i < B_CH; ++i) {
       const int blk = i * LW + lw;
-      const int r = FMT == 2 ? blk * 32 + (lane >> 1) : blk * RPI + lane / LPR;
-      const int sl = FMT == 2 ? (lane & 1) ^ ((r >> 2) & 1) : (lane % LPR) ^ swz<KB>(r);
+      const int r = FMT == 2 ? blk * (64 / LPB) + lane / LPB : blk * RPI + lane / LPR;
+      const int sl = FMT == 2 ? (lane % LPB) ^ swz_b<BB>(r) : (lane % LPR) ^ swz<KB>(r);
       int n;
       if (GEMM1) n = r < NC ? n0 + r : g.I + n0 + (r - NC);
       else n = n0 + r;
@@ -278,7 +270,7 @@ void moe_gemm_tiled(GroupedGemm g) {
         // element offset kt/2 within the row, rounded down to an even element (4-byte aligned)
         const uint8_t* p = src.s[k];
         if (src.ss[k]) {
-          const uintptr_t a = reinterpret_cast<uintptr_t>(src.s[k]) + (kt >> 1) * 2;
+          const uintptr_t a = reinterpret_cast<uintptr_t>(src.s[k]) + ((kt * KE) / 128) * 2;
           p = reinterpret_cast<const uint8_t*>(a & ~static_cast<uintptr_t>(3));
         }
         dma4(p, dst);
@@ -602,38 +594,48 @@ void moe_gemm_tiled(GroupedGemm g) {
           __builtin_amdgcn_sched_barrier(0);
         }
       } else {  // int4
-        // this lane's B words for the four 16-wide K substeps, and its scales
+        // this lane's scales, then per 64-element half of the step its B words
+        // (one word of eight nibbles per 16-wide K substep; a lane group
+        // covers KE/2 elements of the step)
+        constexpr int NKK = KE / 16, NBW = NKK / 4;
         const uint32_t* sW = reinterpret_cast<const uint32_t*>(Ss);  // one dword per tile row
-        u32x4 bw[TN];
         float sb[TN];
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
           const int r = brow(j) + l32;
-          bw[j] = ld16(Bs + r * BB + ((kg ^ ((r >> 2) & 1)) << 4));
           const int n_glob = GEMM1 ? (r < NC ? n0 + r : g.I + n0 + (r - NC)) : n0 + r;
-          const int idx = (e * (GEMM1 ? 2 * g.I : g.H) + n_glob) * (K / 128) + (kt >> 1);
+          const int idx = (e * (GEMM1 ? 2 * g.I : g.H) + n_glob) * (K / 128) + (kt * KE) / 128;
           const uint32_t d = sW[r];
           sb[j] = __uint_as_float((idx & 1) ? (d & 0xFFFF0000u) : (d << 16));
         }
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          // substep kk of lane group kg covers K elements [(4kg+kk)*8, +8) of the step
-          const int ch = 4 * kg + kk;
-          bf16x8 a[TM], b[TN];
-#pragma unroll
-          for (int i = 0; i < TM; ++i) {
-            const int r = wm * WTM + i * 32 + l32;
-            a[i] = as_bf16x8(ld16(As + r * KB + ((ch ^ swz<KB>(r)) << 4)));
-          }
+        for (int h = 0; h < NBW; ++h) {
+          u32x4 bw[TN];
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
-            const uint32_t wd = kk == 0 ? bw[j].x : (kk == 1 ? bw[j].y : (kk == 2 ? bw[j].z : bw[j].w));
-            b[j] = dequant_int4x8(wd, sb[j]);
+            const int r = brow(j) + l32;
+            bw[j] = ld16(Bs + r * BB + (((NBW * kg + h) ^ swz_b<BB>(r)) << 4));
           }
 #pragma unroll
-          for (int i = 0; i < TM; ++i)
+          for (int k4 = 0; k4 < 4; ++k4) {
+            // substep kk of lane group kg covers K elements [(NKK*kg+kk)*8, +8) of the step
+            const int kk = 4 * h + k4, ch = NKK * kg + kk;
+            bf16x8 a[TM], b[TN];
 #pragma unroll
-            for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(a[i], b[j], acc[i][j]);
+            for (int i = 0; i < TM; ++i) {
+              const int r = wm * WTM + i * 32 + l32;
+              a[i] = as_bf16x8(ld16(As + r * KB + ((ch ^ swz<KB>(r)) << 4)));
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+              const uint32_t wd = k4 == 0 ? bw[j].x : (k4 == 1 ? bw[j].y : (k4 == 2 ? bw[j].z : bw[j].w));
+              b[j] = dequant_int4x8(wd, sb[j]);
+            }
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+              for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(a[i], b[j], acc[i][j]);
+          }
         }
       }
     }
@@ -856,13 +858,20 @@ hipError_t launch_gemm2_fp8(const GroupedGemm& g, hipStream_t s) {
 #ifndef MOE_TI4_BM
 #define MOE_TI4_BM 64
 #endif
+// 128 K elements per step: 64 bytes of each int4 weight row (half a cache
+// line, where 64 elements took a quarter), 256 bytes of each activation row;
+// two stages keep two workgroups per CU
+#ifndef MOE_TI4_KB
+#define MOE_TI4_KB 256
+#define MOE_TI4_STAGES 2
+#endif
 int gemm_block_m_int4(int, int, int) { return MOE_TI4_BM; }
 hipError_t launch_gemm1_int4(const GroupedGemm& g, hipStream_t s) {
-  return launch_tiled<2, true, MOE_TI4_BM, 256, 1, 4, MOE_TGM_INT4, 128, 3, MOE_TI4_NP1>(g, s);
+  return launch_tiled<2, true, MOE_TI4_BM, 256, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP1>(g, s);
 }
 hipError_t launch_gemm2_int4(const GroupedGemm& g, hipStream_t s) {
-  if (g.H % 256) return launch_tiled<2, false, MOE_TI4_BM, 128, 1, 4, MOE_TGM_INT4, 128, 3, MOE_TI4_NP2>(g, s);
-  return launch_tiled<2, false, MOE_TI4_BM, 256, 1, 4, MOE_TGM_INT4, 128, 3, MOE_TI4_NP2>(g, s);
+  if (g.H % 256) return launch_tiled<2, false, MOE_TI4_BM, 128, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP2>(g, s);
+  return launch_tiled<2, false, MOE_TI4_BM, 256, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP2>(g, s);
 }
 
 }  // namespace moe

@@ -149,7 +149,7 @@ def test_int4_h_not_multiple_of_256(dev):
 
 @pytest.mark.parametrize("wcfg", [4, 5])
 def test_quant_minimum_k(dev, wcfg):
-    # H = I = 128: one (fp8) or two (int4) K steps per tile
+    # H = I = 128: a single K step per tile
     _check(synth.tiny_config(wcfg, T=400, H=128, I=128, E=4, top_k=2))
 
 
