@@ -79,6 +79,9 @@ void moe_gemm_tiled(GroupedGemm g) {
   constexpr int KE = FMT == 1 ? KB : KB / 2;                          // K elements per step
   constexpr int BB = FMT == 0 ? KB : (FMT == 1 ? KB : KB / 4);        // B bytes per row per step
   constexpr int LPB = BB / 16;                                         // lanes per int4 B row in a copy
+  // bf16 GEMM2 forms its product transposed, as fp8 does (16-byte y stores,
+  // one pad check per row; 4 % faster on prefill, GEMM1 was not)
+  constexpr bool TRB = FMT == 0 && !GEMM1;
   constexpr int RPI = 1024 / KB, LPR = KB / 16;  // rows per DMA instruction, lanes per row
   constexpr int WTM = BM / WM, WTN = BNW / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -411,7 +414,9 @@ void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
           for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(fa[kk & 1][i], fb[kk & 1][j], acc[i][j]);
+            for (int j = 0; j < TN; ++j)
+              acc[i][j] = TRB ? mfma32x32x16(fb[kk & 1][j], fa[kk & 1][i], acc[i][j])
+                              : mfma32x32x16(fa[kk & 1][i], fb[kk & 1][j], acc[i][j]);
           __builtin_amdgcn_sched_barrier(0);
         }
       }
@@ -451,7 +456,8 @@ void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
           for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(af[kk][i], bfr[kk][j], acc[i][j]);
+            for (int j = 0; j < TN; ++j)
+              acc[i][j] = TRB ? mfma32x32x16(bfr[kk][j], af[kk][i], acc[i][j]) : mfma32x32x16(af[kk][i], bfr[kk][j], acc[i][j]);
           __builtin_amdgcn_sched_barrier(0);
           if (pre) issue_part(cur, kt + STAGES - 1, (sb + kt + STAGES - 1) % STAGES, kk * PER, min((kk + 1) * PER, A_CH + B_CH));
           __builtin_amdgcn_sched_barrier(0);
@@ -641,8 +647,11 @@ void moe_gemm_tiled(GroupedGemm g) {
     }
 #undef brow
 
-    // ---- epilogue.  D element v of a 32x32 tile (bf16, int4): row
-    // 8*(v/4) + 4*kg + v%4, column l32; fp8 holds the transpose.
+    // ---- epilogue.  D element v of a 32x32 tile (bf16 GEMM1, int4): row
+    // 8*(v/4) + 4*kg + v%4, column l32.  fp8 and bf16 GEMM2 form the product
+    // transposed (W is the MFMA's first operand): lane (kg, l32) of row
+    // block i holds row wm*WTM + i*32 + l32 at columns 8*(v/4) + 4*kg + v%4
+    // of each column block, so four consecutive columns per store.
     if constexpr (GEMM1) {
       constexpr int TH = TN / 2;  // gate tiles (paired with up tile j + TH)
       float av[TM][TH][16];
@@ -718,6 +727,23 @@ void moe_gemm_tiled(GroupedGemm g) {
             const f32x16& c = acc[i][j];
             const uint2 pk = {pack_bf16x2(c[4 * v4], c[4 * v4 + 1]), pack_bf16x2(c[4 * v4 + 2], c[4 * v4 + 3])};
             *reinterpret_cast<uint2*>(yr + col) = pk;
+          }
+      }
+    } else if constexpr (FMT == 0) {
+      // transposed layout, fp32 y: four consecutive output columns per 16-byte store
+      static_assert(y_is_f32(FMT), "bf16 routes keep y in fp32");
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int row = m0 + wm * WTM + i * 32 + l32;
+        if (g.sorted_ids[row] >= g.n_routed) continue;  // pad rows are never read
+        float* yr = static_cast<float*>(g.y) + static_cast<size_t>(row) * g.H;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int v4 = 0; v4 < 4; ++v4) {
+            const int col = n0 + wn * WTN + j * 32 + 8 * v4 + 4 * kg;
+            const f32x16& c = acc[i][j];
+            *reinterpret_cast<f32x4*>(yr + col) = f32x4{c[4 * v4], c[4 * v4 + 1], c[4 * v4 + 2], c[4 * v4 + 3]};
           }
       }
     } else {
