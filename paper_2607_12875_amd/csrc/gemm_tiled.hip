@@ -79,9 +79,9 @@ void moe_gemm_tiled(GroupedGemm g) {
   constexpr int KE = FMT == 1 ? KB : KB / 2;                          // K elements per step
   constexpr int BB = FMT == 0 ? KB : (FMT == 1 ? KB : KB / 4);        // B bytes per row per step
   constexpr int LPB = BB / 16;                                         // lanes per int4 B row in a copy
-  // bf16 GEMM2 forms its product transposed, as fp8 does (16-byte y stores,
-  // one pad check per row; 4 % faster on prefill, GEMM1 was not)
-  constexpr bool TRB = FMT == 0 && !GEMM1;
+  // bf16 and int4 GEMM2 form their product transposed, as fp8 does (16-byte
+  // y stores, one pad check per row; bf16 prefill 4 % faster, GEMM1 was not)
+  constexpr bool TRB = FMT != 1 && !GEMM1;
   constexpr int RPI = 1024 / KB, LPR = KB / 16;  // rows per DMA instruction, lanes per row
   constexpr int WTM = BM / WM, WTN = BNW / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -640,15 +640,15 @@ void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
-              for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(a[i], b[j], acc[i][j]);
+              for (int j = 0; j < TN; ++j) acc[i][j] = TRB ? mfma32x32x16(b[j], a[i], acc[i][j]) : mfma32x32x16(a[i], b[j], acc[i][j]);
           }
         }
       }
     }
 #undef brow
 
-    // ---- epilogue.  D element v of a 32x32 tile (bf16 GEMM1, int4): row
-    // 8*(v/4) + 4*kg + v%4, column l32.  fp8 and bf16 GEMM2 form the product
+    // ---- epilogue.  D element v of a 32x32 tile (bf16 / int4 GEMM1): row
+    // 8*(v/4) + 4*kg + v%4, column l32.  fp8 and every GEMM2 form the product
     // transposed (W is the MFMA's first operand): lane (kg, l32) of row
     // block i holds row wm*WTM + i*32 + l32 at columns 8*(v/4) + 4*kg + v%4
     // of each column block, so four consecutive columns per store.
@@ -729,9 +729,9 @@ void moe_gemm_tiled(GroupedGemm g) {
             *reinterpret_cast<uint2*>(yr + col) = pk;
           }
       }
-    } else if constexpr (FMT == 0) {
+    } else {
       // transposed layout, fp32 y: four consecutive output columns per 16-byte store
-      static_assert(y_is_f32(FMT), "bf16 routes keep y in fp32");
+      static_assert(TRB && y_is_f32(FMT), "bf16 and int4 routes keep y in fp32");
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int row = m0 + wm * WTM + i * 32 + l32;
@@ -746,22 +746,6 @@ void moe_gemm_tiled(GroupedGemm g) {
             *reinterpret_cast<f32x4*>(yr + col) = f32x4{c[4 * v4], c[4 * v4 + 1], c[4 * v4 + 2], c[4 * v4 + 3]};
           }
       }
-    } else {
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int row = m0 + wm * WTM + i * 32 + 8 * (v >> 2) + 4 * kg + (v & 3);
-          if (g.sorted_ids[row] >= g.n_routed) continue;  // pad rows are never read
-#pragma unroll
-          for (int j = 0; j < TN; ++j) {
-            const int col = n0 + wn * WTN + j * 32 + l32;
-            if (y_is_f32(FMT))
-              static_cast<float*>(g.y)[static_cast<size_t>(row) * g.H + col] = acc[i][j][v];
-            else
-              static_cast<uint16_t*>(g.y)[static_cast<size_t>(row) * g.H + col] = f32_to_bf16(acc[i][j][v]);
-          }
-        }
     }
   }
 }
