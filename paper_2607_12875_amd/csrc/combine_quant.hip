@@ -7,64 +7,96 @@
 namespace moe {
 
 // out[t, h] = sum_j w[t, j] * y[inv_pos[t*k + j], h], j ascending, fp32
-// accumulation.  Each thread owns 8 consecutive columns: one 16-byte load per
-// routed row, one or two 16-byte stores.
-template <bool Y_F32, bool OUT_BF16>
+// accumulation.  Each thread owns 8 consecutive columns of one token (threads
+// laid over all T * H/8 column groups, so no workgroup is left part-empty).
+// The slots' positions and weights are read first, then every slot's row
+// piece is requested before any is summed (a row load issued behind an index
+// load would wait for all earlier row loads: the counts complete in order).
+// KC > 0: k == KC, all slots at once; KC == 0: any k, eight slots at a time
+// (slots past k re-read the last row and are not summed).  y is read and out
+// written exactly once, with non-temporal hints.
+template <bool Y_F32, bool OUT_BF16, int KC>
 __global__ __launch_bounds__(256) void combine_kernel(
     const void* __restrict__ y, const float* __restrict__ w, const int32_t* __restrict__ inv_pos,
     int T, int H, int k, void* __restrict__ out) {
-  const int t = blockIdx.y;
-  const int h = (blockIdx.x * 256 + threadIdx.x) * 8;
-  if (h >= H) return;
+  constexpr int CH = KC > 0 ? KC : 8;
+  typedef float f4 __attribute__((ext_vector_type(4)));
+  const int hg = H / 8;
+  const long idx = static_cast<long>(blockIdx.x) * 256 + threadIdx.x;
+  if (idx >= static_cast<long>(T) * hg) return;
+  const int t = static_cast<int>(idx / hg), h = static_cast<int>(idx % hg) * 8;
   float acc[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = 0.f;
-  for (int j = 0; j < k; ++j) {
-    const float wt = w[static_cast<size_t>(t) * k + j];
-    const int p = inv_pos[static_cast<size_t>(t) * k + j];
-    if (Y_F32) {
-      const float4* src = reinterpret_cast<const float4*>(static_cast<const float*>(y) +
-                                                          static_cast<size_t>(p) * H + h);
-      const float4 a = src[0], b = src[1];
-      const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  for (int j0 = 0; j0 < k; j0 += CH) {
+    float wt[CH];
+    int pos[CH];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) acc[i] = fmaf(wt, v[i], acc[i]);
-    } else {
-      const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(y) +
-                                                      static_cast<size_t>(p) * H + h);
-      const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+    for (int c = 0; c < CH; ++c) {
+      const size_t o = static_cast<size_t>(t) * k + (KC > 0 ? c : min(j0 + c, k - 1));
+      wt[c] = w[o];
+      pos[c] = inv_pos[o];
+    }
+    f4 va[CH], vb[CH];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        acc[2 * i] = fmaf(wt, __uint_as_float(u[i] << 16), acc[2 * i]);
-        acc[2 * i + 1] = fmaf(wt, __uint_as_float(u[i] & 0xFFFF0000u), acc[2 * i + 1]);
+    for (int c = 0; c < CH; ++c) {
+      const size_t p = static_cast<size_t>(pos[c]);
+      if (Y_F32) {
+        const f4* src = reinterpret_cast<const f4*>(static_cast<const float*>(y) + p * H + h);
+        va[c] = __builtin_nontemporal_load(src);
+        vb[c] = __builtin_nontemporal_load(src + 1);
+      } else {
+        va[c] = __builtin_nontemporal_load(reinterpret_cast<const f4*>(static_cast<const uint16_t*>(y) + p * H + h));
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      if (KC == 0 && j0 + c >= k) break;
+      if (Y_F32) {
+        const float v[8] = {va[c].x, va[c].y, va[c].z, va[c].w, vb[c].x, vb[c].y, vb[c].z, vb[c].w};
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] = fmaf(wt[c], v[i], acc[i]);
+      } else {
+        const uint32_t u[4] = {__float_as_uint(va[c].x), __float_as_uint(va[c].y), __float_as_uint(va[c].z),
+                               __float_as_uint(va[c].w)};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          acc[2 * i] = fmaf(wt[c], __uint_as_float(u[i] << 16), acc[2 * i]);
+          acc[2 * i + 1] = fmaf(wt[c], __uint_as_float(u[i] & 0xFFFF0000u), acc[2 * i + 1]);
+        }
       }
     }
   }
   if (OUT_BF16) {
-    uint4 o;
-    o.x = pack_bf16x2(acc[0], acc[1]);
-    o.y = pack_bf16x2(acc[2], acc[3]);
-    o.z = pack_bf16x2(acc[4], acc[5]);
-    o.w = pack_bf16x2(acc[6], acc[7]);
-    *reinterpret_cast<uint4*>(static_cast<uint16_t*>(out) + static_cast<size_t>(t) * H + h) = o;
+    const u32x4 o = {pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]), pack_bf16x2(acc[4], acc[5]),
+                     pack_bf16x2(acc[6], acc[7])};
+    __builtin_nontemporal_store(o, reinterpret_cast<u32x4*>(static_cast<uint16_t*>(out) + static_cast<size_t>(t) * H + h));
   } else {
-    float4* o = reinterpret_cast<float4*>(static_cast<float*>(out) + static_cast<size_t>(t) * H + h);
-    o[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
-    o[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+    f32x4* o = reinterpret_cast<f32x4*>(static_cast<float*>(out) + static_cast<size_t>(t) * H + h);
+    __builtin_nontemporal_store(f32x4{acc[0], acc[1], acc[2], acc[3]}, o);
+    __builtin_nontemporal_store(f32x4{acc[4], acc[5], acc[6], acc[7]}, o + 1);
   }
 }
 
 hipError_t launch_combine(const void* y, bool y_f32, const float* w, const int32_t* inv_pos, int T,
                           int H, int k, bool out_bf16, void* out, hipStream_t s) {
-  const dim3 grid((H / 8 + 255) / 256, T), block(256);
-#define MOE_COMBINE(YF, OB) \
-  hipLaunchKernelGGL((combine_kernel<YF, OB>), grid, block, 0, s, y, w, inv_pos, T, H, k, out)
+  const long n = static_cast<long>(T) * (H / 8);
+  const dim3 grid(static_cast<unsigned>((n + 255) / 256)), block(256);
+#define MOE_COMBINE_K(YF, OB, KC) \
+  hipLaunchKernelGGL((combine_kernel<YF, OB, KC>), grid, block, 0, s, y, w, inv_pos, T, H, k, out)
+#define MOE_COMBINE(YF, OB)                        \
+  do {                                             \
+    if (k == 6) MOE_COMBINE_K(YF, OB, 6);          \
+    else if (k == 8) MOE_COMBINE_K(YF, OB, 8);     \
+    else MOE_COMBINE_K(YF, OB, 0);                 \
+  } while (0)
   if (y_f32) {
     if (out_bf16) MOE_COMBINE(true, true); else MOE_COMBINE(true, false);
   } else {
     if (out_bf16) MOE_COMBINE(false, true); else MOE_COMBINE(false, false);
   }
 #undef MOE_COMBINE
+#undef MOE_COMBINE_K
   return hipGetLastError();
 }
 
