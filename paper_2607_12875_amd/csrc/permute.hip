@@ -91,10 +91,18 @@ __global__ __launch_bounds__(kPermThreads) void permute_scatter_kernel(
     if (counts == nullptr) {
       for (int w = 0; w < W; ++w) tot += __popc(bitmap[tid * W + w]);
     } else {
-      for (int cc = 0; cc < nchunks; ++cc) {
-        const int v = counts[cc * E + tid];
-        tot += v;
-        if (cc < c) pre += v;
+      // every chunk's count of expert tid, sixteen loads in flight at a time
+      // (indices clamped so the loads issue unconditionally)
+      for (int c0 = 0; c0 < nchunks; c0 += 16) {
+        int v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = counts[min(c0 + u, nchunks - 1) * E + tid];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const int cc = c0 + u;
+          if (cc < nchunks) tot += v[u];
+          if (cc < c) pre += v[u];
+        }
       }
     }
   }
