@@ -57,3 +57,10 @@ def test_hundreds_of_experts(dev):
 
 def test_top_k_equals_e(dev):
     check_forward(synth.tiny_config(1, T=120, E=6, top_k=6))
+
+
+@pytest.mark.parametrize("k", [12, 32])
+def test_many_routed_rows_per_token(dev, k):
+    # more than eight routed rows per token: the weighted sum takes the
+    # slots eight at a time, in slot order
+    check_forward(synth.tiny_config(1, T=90, E=48, top_k=k, H=256, I=128))
