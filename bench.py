@@ -17,6 +17,9 @@ Timing:
     roofline's denominator) is measured live inside the same timed region;
   * per stage: after the timed region, K further calls with events between
     all stages (a breakdown only; these events cost a few microseconds each);
+  * graph: the same layer captured once in a HIP graph and replayed K times
+    (how a serving loop would run it), reported beside ``value``, which
+    stays the stream-launched figure;
   * traffic: HBM bytes per launch from committed rocprofv3 FETCH_SIZE /
     WRITE_SIZE counters, only if the kernel sources still hash to the value
     they were taken at (else null);
@@ -266,6 +269,29 @@ def main():
     stage_us = {name: float(v * 1e3 / K) for name, v in zip(moe.STAGES, stage_sum)}
     sev.close()
 
+    # ---- the same layer captured once in a HIP graph, replayed K times
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    with torch.cuda.stream(side):
+        moe.moe_forward_args(margs, ws)
+    stream.wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        moe.moe_forward_args(margs, ws)
+    for _ in range(3):
+        graph.replay()
+    torch.cuda.synchronize()
+    gev = HipEvents(2)
+    rt.hipEventRecord(gev.ev[0], ctypes.c_void_p(stream.cuda_stream))
+    for _ in range(K):
+        graph.replay()
+    rt.hipEventRecord(gev.ev[1], ctypes.c_void_p(stream.cuda_stream))
+    torch.cuda.synchronize()
+    graph_us = gev.elapsed_ms(0, 1) * 1e3 / K
+    gev.close()
+    del graph
+
     # routing statistics of this batch (from the layer's own workspace)
     offs = ws[layout["expert_offsets"]:layout["expert_offsets"] + 4 * (cfg.E + 1)].view(torch.int32).cpu().numpy()
     ids = ws[layout["topk_ids"]:layout["topk_ids"] + 4 * cfg.n_routed].view(torch.int32).cpu().numpy()
@@ -327,6 +353,7 @@ def main():
                    "max_rows_per_expert": int(counts.max()), "block_m": layout["block_m"]},
         "us_per_layer": ms * 1e3,
         "wall_us_per_layer": wall_ms * 1e3,
+        "graph_us_per_layer": graph_us,
         "stage_us": stage_us,
         "roofline": roof,
         "cpu_baseline": base,
