@@ -63,11 +63,20 @@ DESCR = {
 GEMM_SOURCES = ("common.hpp", "launch.hpp", "lds_dma.hpp", "dispatch.hip", "gemm_bf16.hip", "gemm_tiled.hip")
 
 
+def _code_only(text: str) -> str:
+    """C++ source without comments and with whitespace runs collapsed, so an
+    edit of comments alone does not count as a kernel change."""
+    import re
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
     for p in sorted(os.path.join(ROOT, "paper_2607_12875_amd", "csrc", n) for n in GEMM_SOURCES):
-        with open(p, "rb") as f:
-            h.update(os.path.basename(p).encode() + f.read())
+        with open(p, encoding="utf-8") as f:
+            h.update(os.path.basename(p).encode() + _code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -14,17 +14,21 @@
 //        group per row.
 //  int4  A bf16; B signed int4 words decoded in registers (q * bf16 scale,
 //        rounded to bf16) right before the bf16 MFMA, never materialised.
+// Every GEMM2 also forms its product transposed (four consecutive output
+// columns per lane, so y goes out in 16-byte stores).
 //
-// Every format streams 128 bytes of each A row per K step through LDS (64
-// bf16 / 128 fp8 elements), 16-byte chunks XOR-swizzled by row so that the
-// fragment reads are bank-conflict free; B rows likewise (int4: 32 bytes).
+// Each K step streams KB bytes of every A row through LDS -- 128 (64 bf16 /
+// 128 fp8 elements), or 256 for int4 (128 elements, so each int4 weight row
+// gives 64 bytes, half a cache line) -- in 16-byte chunks XOR-swizzled by row
+// so that the fragment reads are bank-conflict free; B rows likewise.
 //
 // Scheduling is persistent and XCD-aware: the launch has a few workgroups per
 // CU; workgroups that land on one XCD (block ids congruent mod 8) own one
 // contiguous range of logical tiles, ordered expert by expert in chunks of at
 // most GM row tiles x all column tiles, so the weight slab and row tiles that
-// concurrently running workgroups share are read from HBM about once.  The number of real row tiles
-// is read on the device from expert_offsets[E] (segments are padded to BM).
+// concurrently running workgroups share are read from HBM about once.  The
+// number of real row tiles is read on the device from expert_offsets[E]
+// (segments are padded to BM).
 #include <algorithm>
 
 #include "common.hpp"
@@ -77,7 +81,7 @@ void moe_gemm_tiled(GroupedGemm g) {
                 "64-byte steps are bf16 only, 256-byte steps int4 only");
   constexpr int KB = KBT;                                       // A bytes per row per step
   constexpr int KE = FMT == 1 ? KB : KB / 2;                          // K elements per step
-  constexpr int BB = FMT == 0 ? KB : (FMT == 1 ? KB : KB / 4);        // B bytes per row per step
+  constexpr int BB = FMT == 2 ? KB / 4 : KB;                           // B bytes per row per step
   constexpr int LPB = BB / 16;                                         // lanes per int4 B row in a copy
   // bf16 and int4 GEMM2 form their product transposed, as fp8 does (16-byte
   // y stores, one pad check per row; bf16 prefill 4 % faster, GEMM1 was not)
