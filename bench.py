@@ -56,6 +56,8 @@ DESCR = {
        "bf16 activations, sigmoid+bias top-8 x2.5",
     7: "MXFP4 decode MoE layer: T=16 H=7168 E=256 I=2048 top_k=8, OCP MX E2M1 weights with E8M0 "
        "scales per 32, bf16 activations, sigmoid+bias top-8 x2.5",
+    8: "MXFP4 prefill MoE layer: T=8192 H=7168 E=256 I=2048 top_k=8, OCP MX E2M1 weights with E8M0 "
+       "scales per 32, bf16 activations, sigmoid+bias top-8 x2.5",
 }
 
 

@@ -83,15 +83,15 @@ typedef enum {
      32 routed rows per expert on average), else MOE_ERR_UNSUPPORTED: larger
      batches take MOE_W_FP8E4M3_B128. */
   MOE_W_FP8E4M3_B128_A16 = 3,
-  /* MXFP4 weights (OCP Microscaling v1.0), a decode route like
-     MOE_W_FP8E4M3_B128_A16: E2M1 codes (S.EE.M, bias 1; magnitudes 0, 0.5,
+  /* MXFP4 weights (OCP Microscaling v1.0), weight-only: E2M1 codes (S.EE.M, bias 1; magnitudes 0, 0.5,
      1, 1.5, 2, 3, 4, 6), two per byte, element k = 2b+j in bits [4j,4j+4) of
      byte b (low nibble first): w[e][n][K/2] (uint8_t); one E8M0 scale byte
      per 32 along K: scale[e][n][K/32], value 2^(s-127) (s = 255, NaN, and
      products beyond the bf16 range are unspecified); value = e2m1(q) *
      2^(s-127), decoded exactly to bf16.  Hidden rows enter as bf16, the
-     SwiGLU intermediate is rounded to bf16.  Requires T * top_k <= 32 * E,
-     else MOE_ERR_UNSUPPORTED. */
+     SwiGLU intermediate is rounded to bf16.  Any batch: up to 32 routed rows
+     per expert on average the 16-row decode kernels run, above that the
+     tiled ones (segments padded to 64 rows). */
   MOE_W_MXFP4_A16 = 4
 } moe_wfmt;
 
@@ -226,7 +226,7 @@ moe_status moe_workspace_layout(const moe_args* a, moe_ws_layout* layout);
  * aligned; ws_bytes >= moe_workspace_bytes(a); sel_bias only with a format
  * that reads it (both scoring modes do).  Padding rows of the intermediates
  * are unspecified.  T == 0 is a no-op.
- * MOE_W_FP8E4M3_B128_A16 and MOE_W_MXFP4_A16 additionally need
+ * MOE_W_FP8E4M3_B128_A16 additionally needs
  * T * top_k <= 32 * E.  With
  * w_router set the router GEMM and the gate run as one kernel (as
  * moe_router_gate_topk) and `logits` may be NULL.

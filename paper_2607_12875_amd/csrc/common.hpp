@@ -75,6 +75,21 @@ __device__ __forceinline__ float silu_mul(float g, float u) {
   return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
 }
 
+// Eight OCP MX E2M1 codes (one 32-bit word, byte b holding elements 2b in the
+// low nibble and 2b+1 in the high one) -> eight bf16 values times the block
+// scale.  v_cvt_scalef32_pk_bf16_fp4 applies its fp32 scale operand through
+// the exponent field only, so an E8M0 scale byte s is passed as float(s << 23).
+// Each result word is the bf16 pair (element 2b, element 2b+1), taken as a
+// whole word.
+__device__ __forceinline__ u32x4 mxfp4x8_to_bf16(uint32_t w, float sc) {
+  u32x4 r;
+  r.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 0));
+  r.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 1));
+  r.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 2));
+  r.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 3));
+  return r;
+}
+
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
 // Index e with off[e] <= p < off[e+1] (off non-decreasing, off[0] = 0 <= p < off[E]).

@@ -187,16 +187,6 @@ __device__ __forceinline__ bf16x8 e4m3x8_to_bf16(uint32_t lo, uint32_t hi) {
 // partial is scaled into the accumulator.
 // NG: 16-row weight groups per block (GEMM1: NG/2 gate + NG/2 up); NP
 // pieces of JP MFMAs (32 K elements each) per row and wave: K = 4 * 32 * NP * JP.
-__device__ __forceinline__ u32x4 mxfp4x8_to_bf16(uint32_t w, float sc) {
-  // byte b of w holds elements 2b (low nibble) and 2b+1; each result word is
-  // the bf16 pair (element 2b, element 2b+1) -- taken as a whole word
-  u32x4 r;
-  r.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 0));
-  r.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 1));
-  r.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 2));
-  r.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 3));
-  return r;
-}
 
 template <int FMT, int NWV, int NG, int NP, int JP, bool GEMM1>
 __global__ __launch_bounds__(64 * NWV) void gemm_bf16_stream(GroupedGemm g) {

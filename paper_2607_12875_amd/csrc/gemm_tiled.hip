@@ -14,12 +14,15 @@
 //        group per row.
 //  int4  A bf16; B signed int4 words decoded in registers (q * bf16 scale,
 //        rounded to bf16) right before the bf16 MFMA, never materialised.
+//  mxfp4 A bf16; B OCP MX E2M1 codes with an E8M0 scale per 32 elements,
+//        decoded by v_cvt_scalef32_pk_bf16_fp4 (exact: the bf16 result is the
+//        code's value times a power of two) right before the bf16 MFMA.
 // Every GEMM2 also forms its product transposed (four consecutive output
 // columns per lane, so y goes out in 16-byte stores).
 //
 // Each K step streams KB bytes of every A row through LDS -- 128 (64 bf16 /
-// 128 fp8 elements), or 256 for int4 (128 elements, so each int4 weight row
-// gives 64 bytes, half a cache line) -- in 16-byte chunks XOR-swizzled by row
+// 128 fp8 elements), or 256 for the 4-bit formats (128 elements, so each
+// weight row gives 64 bytes, half a cache line) -- in 16-byte chunks XOR-swizzled by row
 // so that the fragment reads are bank-conflict free; B rows likewise.
 //
 // Scheduling is persistent and XCD-aware: the launch has a few workgroups per
@@ -69,20 +72,21 @@ __device__ __forceinline__ int swz_b(int r) { return BB == 32 ? (r >> 2) & 1 : (
 // (L1 waiting on L2) cannot hold up the MFMA stream behind an in-order copy
 // instruction.  NP == 0: the math waves issue the copies themselves.
 template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM, int KBT = 128, int STAGES = 3, int NP = 0>
-// int4 GEMM1 is held to 128 registers, which keeps two workgroups per CU.
-__global__ __launch_bounds__((WM * WN + NP) * 64) __attribute__((amdgpu_waves_per_eu(FMT == 2 && GEMM1 ? 4 : 1)))
+// The 4-bit GEMM1s are held to 128 registers, which keeps two workgroups per CU.
+__global__ __launch_bounds__((WM * WN + NP) * 64) __attribute__((amdgpu_waves_per_eu((FMT == 2 || FMT == 4) && GEMM1 ? 4 : 1)))
 void moe_gemm_tiled(GroupedGemm g) {
   constexpr int NW = WM * WN, NT = (NW + NP) * 64;
   constexpr int LW = NP > 0 ? NP : NW;  // waves that issue the copies
   static_assert(NW == 4 || NW == 8, "four or eight math waves");
   static_assert(NP == 0 || NW % NP == 0, "scale slots split evenly over the copy waves");
   static_assert(NP == 0 || WM * WN == 4, "split launches have one math wave per SIMD");
-  static_assert(KBT == 128 || (KBT == 64 && FMT == 0) || (KBT == 256 && FMT == 2),
-                "64-byte steps are bf16 only, 256-byte steps int4 only");
+  constexpr bool F4B = FMT == 2 || FMT == 4;  // 4-bit weights (int4, MXFP4), bf16 activations
+  static_assert(KBT == 128 || (KBT == 64 && FMT == 0) || (KBT == 256 && F4B),
+                "64-byte steps are bf16 only, 256-byte steps 4-bit weights only");
   constexpr int KB = KBT;                                       // A bytes per row per step
   constexpr int KE = FMT == 1 ? KB : KB / 2;                          // K elements per step
-  constexpr int BB = FMT == 2 ? KB / 4 : KB;                           // B bytes per row per step
-  constexpr int LPB = BB / 16;                                         // lanes per int4 B row in a copy
+  constexpr int BB = F4B ? KB / 4 : KB;                                // B bytes per row per step
+  constexpr int LPB = BB / 16;                                         // lanes per 4-bit B row in a copy
   // bf16 and int4 GEMM2 form their product transposed, as fp8 does (16-byte
   // y stores, one pad check per row; bf16 prefill 4 % faster, GEMM1 was not)
   constexpr bool TRB = FMT != 1 && !GEMM1;
@@ -101,7 +105,7 @@ void moe_gemm_tiled(GroupedGemm g) {
   // B row's group scale.  Copy wave lw fills slots lw, lw + LW, ...
   constexpr int SC = FMT == 0 ? 0 : NW / LW;  // scale loads per copy wave per stage
   static_assert(FMT != 1 || BM / 64 < NW, "fp8 scale DMA layout");
-  static_assert(FMT != 2 || (NW == 4 && BNW / 64 <= NW), "int4 scale DMA layout");
+  static_assert(!F4B || (NW == 4 && BNW / 64 <= NW), "4-bit scale DMA layout");
   static_assert(STAGES >= 2 && (STAGES - 2) * (A_CH + B_CH + SC) < 64, "vmcnt range");
   constexpr int A_BYTES = BM * KB, B_BYTES = BNW * BB, S_BYTES = FMT == 0 ? 0 : NW * 256;
   constexpr int STAGE = A_BYTES + B_BYTES + S_BYTES;
@@ -209,8 +213,8 @@ void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
     for (int i = 0; i < B_CH; ++i) {
       const int blk = i * LW + lw;
-      const int r = FMT == 2 ? blk * (64 / LPB) + lane / LPB : blk * RPI + lane / LPR;
-      const int sl = FMT == 2 ? (lane % LPB) ^ swz_b<BB>(r) : (lane % LPR) ^ swz<KB>(r);
+      const int r = F4B ? blk * (64 / LPB) + lane / LPB : blk * RPI + lane / LPR;
+      const int sl = F4B ? (lane % LPB) ^ swz_b<BB>(r) : (lane % LPR) ^ swz<KB>(r);
       int n;
       if (GEMM1) n = r < NC ? n0 + r : g.I + n0 + (r - NC);
       else n = n0 + r;
@@ -252,6 +256,15 @@ void moe_gemm_tiled(GroupedGemm g) {
                                                       (static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) + n) * (K / 128));
           src.ss[k] = 1;  // advanced per step in elements below
         }
+      } else if constexpr (FMT == 4) {
+        if (sl < BNW / 64) {
+          // E8M0 bytes [n][K/32]: the four of K step kt are one dword at byte 4 kt
+          const int r = sl * 64 + lane;
+          const int n = GEMM1 ? (r < NC ? n0 + r : g.I + n0 + (r - NC)) : n0 + r;
+          src.s[k] = static_cast<const uint8_t*>(GEMM1 ? g.w1_scale : g.w2_scale) +
+                     (static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) + n) * (K / 32);
+          src.ss[k] = 4;
+        }
       }
     }
   };
@@ -271,7 +284,7 @@ void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
     for (int k = 0; k < SC; ++k) {
       const uint32_t dst = base + A_BYTES + B_BYTES + (lw + k * LW) * 256;
-      if constexpr (FMT == 1) {
+      if constexpr (FMT == 1 || FMT == 4) {
         dma4(src.s[k] + kt * src.ss[k], dst);
       } else if constexpr (FMT == 2) {
         // element offset kt/2 within the row, rounded down to an even element (4-byte aligned)
@@ -603,7 +616,7 @@ void moe_gemm_tiled(GroupedGemm g) {
           }
           __builtin_amdgcn_sched_barrier(0);
         }
-      } else {  // int4
+      } else if constexpr (FMT == 2) {
         // this lane's scales, then per 64-element half of the step its B words
         // (one word of eight nibbles per 16-wide K substep; a lane group
         // covers KE/2 elements of the step)
@@ -647,11 +660,53 @@ void moe_gemm_tiled(GroupedGemm g) {
               for (int j = 0; j < TN; ++j) acc[i][j] = TRB ? mfma32x32x16(b[j], a[i], acc[i][j]) : mfma32x32x16(a[i], b[j], acc[i][j]);
           }
         }
+      } else {  // MXFP4
+        // lane group kg covers elements [64 kg, 64 kg + 64) of the step, the
+        // 32-element blocks 2 kg and 2 kg + 1: their E8M0 bytes are bytes
+        // 2 kg and 2 kg + 1 of the row's scale dword, passed as float(s << 23)
+        constexpr int NKK = KE / 16, NBW = NKK / 4;
+        static_assert(NBW == 2, "one 16-byte chunk per 32-element block");
+        const uint32_t* sW = reinterpret_cast<const uint32_t*>(Ss);  // one dword per tile row
+        float sc[TN][NBW];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const uint32_t d = sW[brow(j) + l32];
+#pragma unroll
+          for (int h = 0; h < NBW; ++h) sc[j][h] = __uint_as_float(((d >> (8 * (NBW * kg + h))) & 0xFFu) << 23);
+        }
+#pragma unroll
+        for (int h = 0; h < NBW; ++h) {
+          u32x4 bw[TN];
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            const int r = brow(j) + l32;
+            bw[j] = ld16(Bs + r * BB + (((NBW * kg + h) ^ swz_b<BB>(r)) << 4));
+          }
+#pragma unroll
+          for (int k4 = 0; k4 < 4; ++k4) {
+            const int kk = 4 * h + k4, ch = NKK * kg + kk;
+            bf16x8 a[TM], b[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+              const int r = wm * WTM + i * 32 + l32;
+              a[i] = as_bf16x8(ld16(As + r * KB + ((ch ^ swz<KB>(r)) << 4)));
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+              const uint32_t wd = k4 == 0 ? bw[j].x : (k4 == 1 ? bw[j].y : (k4 == 2 ? bw[j].z : bw[j].w));
+              b[j] = as_bf16x8(mxfp4x8_to_bf16(wd, sc[j][h]));
+            }
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+              for (int j = 0; j < TN; ++j) acc[i][j] = TRB ? mfma32x32x16(b[j], a[i], acc[i][j]) : mfma32x32x16(a[i], b[j], acc[i][j]);
+          }
+        }
       }
     }
 #undef brow
 
-    // ---- epilogue.  D element v of a 32x32 tile (bf16 / int4 GEMM1): row
+    // ---- epilogue.  D element v of a 32x32 tile (bf16 / 4-bit GEMM1): row
     // 8*(v/4) + 4*kg + v%4, column l32.  fp8 and every GEMM2 form the product
     // transposed (W is the MFMA's first operand): lane (kg, l32) of row
     // block i holds row wm*WTM + i*32 + l32 at columns 8*(v/4) + 4*kg + v%4
@@ -882,6 +937,14 @@ hipError_t launch_gemm2_fp8(const GroupedGemm& g, hipStream_t s) {
 int gemm_block_m_int4(int, int, int) { return MOE_TI4_BM; }
 hipError_t launch_gemm1_int4(const GroupedGemm& g, hipStream_t s) {
   return launch_tiled<2, true, MOE_TI4_BM, 256, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP1>(g, s);
+}
+// MXFP4 weights on the int4 tile (same 4-bit packing, E8M0 scales per 32)
+hipError_t launch_gemm1_mxfp4_tiled(const GroupedGemm& g, hipStream_t s) {
+  return launch_tiled<4, true, MOE_TI4_BM, 256, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP1>(g, s);
+}
+hipError_t launch_gemm2_mxfp4_tiled(const GroupedGemm& g, hipStream_t s) {
+  if (g.H % 256) return launch_tiled<4, false, MOE_TI4_BM, 128, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP2>(g, s);
+  return launch_tiled<4, false, MOE_TI4_BM, 256, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP2>(g, s);
 }
 hipError_t launch_gemm2_int4(const GroupedGemm& g, hipStream_t s) {
   if (g.H % 256) return launch_tiled<2, false, MOE_TI4_BM, 128, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP2>(g, s);

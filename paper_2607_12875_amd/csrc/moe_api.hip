@@ -36,9 +36,8 @@ moe_status check_args(const moe_args* a) {
   if (a->wfmt != MOE_W_BF16 && a->wfmt != MOE_W_FP8E4M3_B128 && a->wfmt != MOE_W_INT4_G128 &&
       a->wfmt != MOE_W_FP8E4M3_B128_A16 && a->wfmt != MOE_W_MXFP4_A16)
     return MOE_ERR_UNSUPPORTED;
-  // the weight-only fp8 and MXFP4 routes are decode routes (16-row kernels only)
-  if ((a->wfmt == MOE_W_FP8E4M3_B128_A16 || a->wfmt == MOE_W_MXFP4_A16) &&
-      static_cast<long>(a->T) * a->top_k > 32L * a->E)
+  // the weight-only fp8 route is a decode route (16-row kernels only)
+  if (a->wfmt == MOE_W_FP8E4M3_B128_A16 && static_cast<long>(a->T) * a->top_k > 32L * a->E)
     return MOE_ERR_UNSUPPORTED;
   if (a->ofmt != MOE_OUT_F32 && a->ofmt != MOE_OUT_BF16) return MOE_ERR_UNSUPPORTED;
   if (a->T == 0) return MOE_OK;

@@ -100,6 +100,9 @@ CONFIGS = {
     # the same decode step with MXFP4 expert weights (bf16 activations)
     7: MoeConfig("mxfp4-decode", T=16, H=7168, E=256, I=2048, top_k=8, wfmt="mxfp4",
                  mode="sigmoid", routed_scale=2.5, sel_bias_std=0.1, seed=7),
+    # workload 4's prefill batch on MXFP4 expert weights (bf16 activations)
+    8: MoeConfig("mxfp4-prefill", T=8192, H=7168, E=256, I=2048, top_k=8, wfmt="mxfp4",
+                 mode="sigmoid", routed_scale=2.5, sel_bias_std=0.1, seed=8),
 }
 
 

@@ -64,7 +64,8 @@ def test_forward_argument_validation():
     assert _fwd(_args(T=129, E=8, top_k=2, wfmt="fp8a16")) == 3
     assert _fwd(_args(T=128, E=8, top_k=2, wfmt="fp8a16"), ws=None) == 5  # accepted, then no workspace
     assert _fwd(_args(wfmt="mxfp4", w1_scale=None)) == 1
-    assert _fwd(_args(T=129, E=8, top_k=2, wfmt="mxfp4")) == 3
+    # MXFP4 takes any batch (decode kernels up to 32 rows per expert, tiled above)
+    assert _fwd(_args(T=129, E=8, top_k=2, wfmt="mxfp4"), ws=None) == 5
     assert _fwd(_args(T=128, E=8, top_k=2, wfmt="mxfp4"), ws=None) == 5
     assert _fwd(_args(hidden=FAKE + 8)) == 4
     assert _fwd(_args(), ws=None) == 5
@@ -121,7 +122,8 @@ def test_gate_and_permute_validation():
 def test_workspace_layout_is_consistent():
     for wfmt, (T, H, E, I, k) in [("bf16", (16, 4096, 64, 1408, 6)), ("bf16", (4096, 4096, 64, 1408, 6)),
                                   ("fp8", (8192, 7168, 256, 2048, 8)), ("int4", (512, 4096, 128, 1536, 8)),
-                                  ("fp8a16", (16, 7168, 256, 2048, 8)), ("mxfp4", (16, 7168, 256, 2048, 8))]:
+                                  ("fp8a16", (16, 7168, 256, 2048, 8)), ("mxfp4", (16, 7168, 256, 2048, 8)),
+                                  ("mxfp4", (4096, 4096, 64, 1408, 6))]:
         a = B.make_args(T, H, E, I, k, wfmt=wfmt)
         L = moe.moe_workspace_layout(a)
         assert L["total"] == moe.moe_workspace_bytes(a)
@@ -129,3 +131,5 @@ def test_workspace_layout_is_consistent():
         offs = sorted(v for n, v in L.items() if n not in ("block_m", "cap", "total") and v >= 0)
         assert offs[0] == 0 and all(o % 256 == 0 for o in offs) and offs[-1] <= L["total"]
         assert (L["act_q"] >= 0) == (wfmt == "fp8")
+        if wfmt == "mxfp4":  # the decode kernels' 16-row tile, the tiled kernels' 64 above 32 rows per expert
+            assert L["block_m"] == (16 if T * k <= 32 * E else 64)

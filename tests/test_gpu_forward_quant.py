@@ -230,10 +230,11 @@ def test_w8a16_large_batch_rejected(dev):
     assert ei.value.status == 3   # MOE_ERR_UNSUPPORTED
 
 
-# ---- MXFP4 weights (OCP MX E2M1 + E8M0 per 32), bf16 activations: a decode route
+# ---- MXFP4 weights (OCP MX E2M1 + E8M0 per 32), bf16 activations: the
+# 16-row decode kernels up to 32 routed rows per expert, tiled above
 @pytest.mark.parametrize("T", [1, 5, 16, 33, 128])
 def test_mxfp4_small(dev, T):
-    # T = 128: T * top_k = 512 = 32 * E, the largest batch the route accepts
+    # T = 128: T * top_k = 512 = 32 * E, the largest batch of the decode kernels
     _check(synth.tiny_config(7, T=T, H=512, I=256, E=16, top_k=4))
 
 
@@ -256,8 +257,22 @@ def test_mxfp4_workload_full_size_sampled(dev):
     _check(synth.config(7), tokens=np.array([0, 6, 9, 15]))
 
 
-def test_mxfp4_large_batch_rejected(dev):
-    cfg = synth.tiny_config(7, T=129, H=256, I=128, E=16, top_k=4)
-    with pytest.raises(moe.MoeError) as ei:
-        run_forward(cfg, synth.make_inputs(cfg))
-    assert ei.value.status == 3
+@pytest.mark.parametrize("T", [129, 300, 1000])
+def test_mxfp4_tiled(dev, T):
+    # above 32 routed rows per expert: 64-row tiles, 128-element K steps, each
+    # weight row's four E8M0 bytes per step (randomised here by up to 2^+-3)
+    cfg = synth.tiny_config(7, T=T, H=512, I=256, E=16, top_k=4)
+    a = moe.make_args(cfg.T, cfg.H, cfg.E, cfg.I, cfg.top_k, wfmt=cfg.wfmt)
+    assert moe.moe_workspace_layout(a)["block_m"] == 64
+    _check(cfg, inp=_scale_blocks(synth.make_inputs(cfg), cfg.wfmt, seed=T))
+
+
+def test_mxfp4_tiled_ragged_and_minimum_k(dev):
+    # H = I = 384: three K steps and H % 256 != 0 (128-wide GEMM2 tiles);
+    # H = I = 128: a single K step
+    _check(synth.tiny_config(7, T=300, H=384, I=384, E=8, top_k=3))
+    _check(synth.tiny_config(7, T=400, H=128, I=128, E=4, top_k=2))
+
+
+def test_mxfp4_prefill_workload_full_size_sampled(dev):
+    _check(synth.config(8), tokens=np.array([0, 1, 777, 2048, 4095, 5000, 8190, 8191]))
