@@ -16,6 +16,7 @@ hipError_t launch_gemm1_w8a16(const GroupedGemm& g, hipStream_t s);
 hipError_t launch_gemm1_w4a16(const GroupedGemm& g, hipStream_t s);
 hipError_t launch_gemm2_w4a16(const GroupedGemm& g, hipStream_t s);
 hipError_t launch_gemm2_w8a16(const GroupedGemm& g, hipStream_t s);
+int gemm_block_m_mxfp4();
 hipError_t launch_gemm1_mxfp4_tiled(const GroupedGemm& g, hipStream_t s);
 hipError_t launch_gemm2_mxfp4_tiled(const GroupedGemm& g, hipStream_t s);
 
@@ -28,7 +29,7 @@ int gemm_block_m(int wfmt, int T, int top_k, int E) {
     case 1: return gemm_block_m_fp8(T, top_k, E);
     case 2: return gemm_block_m_int4(T, top_k, E);
     case 3: return 16;  // the weight-only fp8 route runs the 16-row decode kernels only
-    case 4: return mxfp4_decode(T, top_k, E) ? 16 : gemm_block_m_int4(T, top_k, E);
+    case 4: return mxfp4_decode(T, top_k, E) ? 16 : gemm_block_m_mxfp4();
     default: return gemm_block_m_bf16(T, top_k, E);
   }
 }

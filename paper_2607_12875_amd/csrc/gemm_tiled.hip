@@ -72,8 +72,8 @@ __device__ __forceinline__ int swz_b(int r) { return BB == 32 ? (r >> 2) & 1 : (
 // (L1 waiting on L2) cannot hold up the MFMA stream behind an in-order copy
 // instruction.  NP == 0: the math waves issue the copies themselves.
 template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM, int KBT = 128, int STAGES = 3, int NP = 0>
-// The 4-bit GEMM1s are held to 128 registers, which keeps two workgroups per CU.
-__global__ __launch_bounds__((WM * WN + NP) * 64) __attribute__((amdgpu_waves_per_eu((FMT == 2 || FMT == 4) && GEMM1 ? 4 : 1)))
+// The 64-row 4-bit GEMM1s are held to 128 registers, which keeps two workgroups per CU.
+__global__ __launch_bounds__((WM * WN + NP) * 64) __attribute__((amdgpu_waves_per_eu((FMT == 2 || FMT == 4) && GEMM1 && BM == 64 ? 4 : 1)))
 void moe_gemm_tiled(GroupedGemm g) {
   constexpr int NW = WM * WN, NT = (NW + NP) * 64;
   constexpr int LW = NP > 0 ? NP : NW;  // waves that issue the copies
@@ -938,13 +938,25 @@ int gemm_block_m_int4(int, int, int) { return MOE_TI4_BM; }
 hipError_t launch_gemm1_int4(const GroupedGemm& g, hipStream_t s) {
   return launch_tiled<2, true, MOE_TI4_BM, 256, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP1>(g, s);
 }
-// MXFP4 weights on the int4 tile (same 4-bit packing, E8M0 scales per 32)
+// MXFP4 weights (same 4-bit packing as int4, E8M0 scales per 32)
+#ifndef MOE_TMX_BM
+#define MOE_TMX_BM 128
+#endif
+int gemm_block_m_mxfp4() { return MOE_TMX_BM; }
 hipError_t launch_gemm1_mxfp4_tiled(const GroupedGemm& g, hipStream_t s) {
-  return launch_tiled<4, true, MOE_TI4_BM, 256, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP1>(g, s);
+  if constexpr (MOE_TMX_BM == 64)
+    return launch_tiled<4, true, 64, 256, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP1>(g, s);
+  else
+    return launch_tiled<4, true, 128, 256, 2, 2, MOE_TGM, 256, 3, 4>(g, s);
 }
 hipError_t launch_gemm2_mxfp4_tiled(const GroupedGemm& g, hipStream_t s) {
-  if (g.H % 256) return launch_tiled<4, false, MOE_TI4_BM, 128, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP2>(g, s);
-  return launch_tiled<4, false, MOE_TI4_BM, 256, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP2>(g, s);
+  if constexpr (MOE_TMX_BM == 64) {
+    if (g.H % 256) return launch_tiled<4, false, 64, 128, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP2>(g, s);
+    return launch_tiled<4, false, 64, 256, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP2>(g, s);
+  } else {
+    if (g.H % 256) return launch_tiled<4, false, 128, 128, 2, 2, MOE_TGM, 256, 3, 4>(g, s);
+    return launch_tiled<4, false, 128, 256, 2, 2, MOE_TGM, 256, 3, 4>(g, s);
+  }
 }
 hipError_t launch_gemm2_int4(const GroupedGemm& g, hipStream_t s) {
   if (g.H % 256) return launch_tiled<2, false, MOE_TI4_BM, 128, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP2>(g, s);

@@ -131,5 +131,5 @@ def test_workspace_layout_is_consistent():
         offs = sorted(v for n, v in L.items() if n not in ("block_m", "cap", "total") and v >= 0)
         assert offs[0] == 0 and all(o % 256 == 0 for o in offs) and offs[-1] <= L["total"]
         assert (L["act_q"] >= 0) == (wfmt == "fp8")
-        if wfmt == "mxfp4":  # the decode kernels' 16-row tile, the tiled kernels' 64 above 32 rows per expert
-            assert L["block_m"] == (16 if T * k <= 32 * E else 64)
+        if wfmt == "mxfp4":  # the decode kernels' 16-row tile, the tiled kernels' 128 above 32 rows per expert
+            assert L["block_m"] == (16 if T * k <= 32 * E else 128)

@@ -259,11 +259,11 @@ def test_mxfp4_workload_full_size_sampled(dev):
 
 @pytest.mark.parametrize("T", [129, 300, 1000])
 def test_mxfp4_tiled(dev, T):
-    # above 32 routed rows per expert: 64-row tiles, 128-element K steps, each
+    # above 32 routed rows per expert: 128-row tiles, 128-element K steps, each
     # weight row's four E8M0 bytes per step (randomised here by up to 2^+-3)
     cfg = synth.tiny_config(7, T=T, H=512, I=256, E=16, top_k=4)
     a = moe.make_args(cfg.T, cfg.H, cfg.E, cfg.I, cfg.top_k, wfmt=cfg.wfmt)
-    assert moe.moe_workspace_layout(a)["block_m"] == 64
+    assert moe.moe_workspace_layout(a)["block_m"] == 128
     _check(cfg, inp=_scale_blocks(synth.make_inputs(cfg), cfg.wfmt, seed=T))
 
 
