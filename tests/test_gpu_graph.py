@@ -31,7 +31,8 @@ def _args(cfg, d, out):
     synth.tiny_config(2, T=16, H=1024, I=1408, E=24, top_k=6),   # streamed decode kernels
     synth.tiny_config(1, T=600, H=512, I=384, E=8, top_k=2),     # tiled bf16 kernels
     synth.tiny_config(5, T=300, H=512, I=256, E=12, top_k=4),    # int4 route
-], ids=["decode", "tiled", "int4"])
+    synth.tiny_config(7, T=300, H=512, I=256, E=12, top_k=4),    # MXFP4, tiled
+], ids=["decode", "tiled", "int4", "mxfp4"])
 def test_graph_replays_match_eager(dev, cfg):
     print(f"graph replay {cfg}", flush=True)
     d = synth.to_device(synth.make_inputs(cfg))
