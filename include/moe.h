@@ -91,7 +91,7 @@ typedef enum {
      2^(s-127), decoded exactly to bf16.  Hidden rows enter as bf16, the
      SwiGLU intermediate is rounded to bf16.  Any batch: up to 32 routed rows
      per expert on average the 16-row decode kernels run, above that the
-     tiled ones (segments padded to 64 rows). */
+     tiled ones (segments padded to 128 rows). */
   MOE_W_MXFP4_A16 = 4
 } moe_wfmt;
 

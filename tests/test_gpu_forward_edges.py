@@ -64,3 +64,17 @@ def test_many_routed_rows_per_token(dev, k):
     # more than eight routed rows per token: the weighted sum takes the
     # slots eight at a time, in slot order
     check_forward(synth.tiny_config(1, T=90, E=48, top_k=k, H=256, I=128))
+
+
+@pytest.mark.parametrize("T", [20, 2000])
+def test_max_experts_and_top_k(dev, T):
+    # the ABI's limits E = 1024 and top_k = 32; T = 20 takes the decode
+    # kernels, T = 2000 (64000 routed rows) the tiled ones
+    check_forward(synth.tiny_config(1, T=T, E=1024, top_k=32, H=256, I=128))
+
+
+@pytest.mark.parametrize("wcfg", [1, 5])
+@pytest.mark.parametrize("T", [8, 200])
+def test_max_hidden_size(dev, wcfg, T):
+    # H = 65536, the ABI's limit: 512 (bf16 tiled) to 1024 K steps of GEMM1
+    check_forward(synth.tiny_config(wcfg, T=T, E=4, top_k=2, H=65536, I=256))
