@@ -73,7 +73,12 @@ typedef enum {
   /* signed two's-complement int4, zero point 0, 8 per int32 along K: element
      k = 8w+j sits in bits [4j,4j+4) of word w (low nibble first):
      w[e][n][K/8] (int32_t); bf16 scale per 128 along K: scale[e][n][k/128];
-     value = q * scale. */
+     value = q * scale.  Hidden rows enter as bf16 and the SwiGLU
+     intermediate is rounded to bf16.  The first product sums each 128-group
+     of codes exactly and applies the group's scale in fp32; the second
+     rounds q * scale to bf16 before its products.  A scale may be zero;
+     the nonzero scales must be normal numbers within a factor 2^64 of each
+     other along a weight row (other scales are unspecified). */
   MOE_W_INT4_G128 = 2,
   /* Weight-only fp8 (a decode route): the MOE_W_FP8E4M3_B128 storage and
      scales, but the hidden rows enter unquantised (bf16) and the SwiGLU
@@ -206,7 +211,9 @@ typedef struct moe_ws_layout {
   int64_t topk_ids, topk_w;          /* int32 / fp32 [T*top_k]                   */
   int64_t expert_offsets;            /* int32 [E+1]                              */
   int64_t sorted_ids, inv_pos;       /* int32 [cap], int32 [T*top_k]             */
-  int64_t act_q, act_s;              /* fp8: uint8 [T,H], fp32 [T,H/128]         */
+  int64_t act_q, act_s;              /* fp8: uint8 [T,H], fp32 [T,H/128]; int4:
+                                        act_s = fp32 [T,H/128] group sums of the
+                                        hidden rows (times -136)              */
   int64_t inter, inter_s;            /* bf16 [cap,I] (fp8: uint8 [cap,I], fp32 [cap,I/128]) */
   int64_t y;                         /* [cap,H] rows in sorted order: bf16 for
                                         MOE_W_FP8E4M3_B128, fp32 otherwise; pad rows unspecified */

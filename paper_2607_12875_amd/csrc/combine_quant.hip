@@ -141,4 +141,30 @@ hipError_t launch_act_quant(const uint16_t* x, int M, int K, uint8_t* q, float* 
   return hipGetLastError();
 }
 
+// Per (row, 128-column group): -136 times the fp32 sum of the group's values,
+// the term the int4 GEMM1 takes off its biased codes (136 + q).  Sixteen
+// lanes own one group, as in the quantiser above.
+__global__ __launch_bounds__(256) void group_sum_kernel(const uint16_t* __restrict__ x, int M, int K,
+                                                         float* __restrict__ out) {
+  const long idx = static_cast<long>(blockIdx.x) * 256 + threadIdx.x;  // one per 8 columns
+  const long total = static_cast<long>(M) * (K / 8);
+  const bool live = idx < total;
+  uint4 v = make_uint4(0, 0, 0, 0);
+  if (live) v = *reinterpret_cast<const uint4*>(x + idx * 8);
+  const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) sum += __uint_as_float(u[i] << 16) + __uint_as_float(u[i] & 0xFFFF0000u);
+#pragma unroll
+  for (int off = 1; off < 16; off <<= 1) sum += __shfl_xor(sum, off);
+  if (live && (threadIdx.x & 15) == 0) out[idx / 16] = -136.0f * sum;
+}
+
+hipError_t launch_group_sum(const uint16_t* x, int M, int K, float* out, hipStream_t st) {
+  const long total = static_cast<long>(M) * (K / 8);
+  const dim3 grid(static_cast<unsigned>((total + 255) / 256)), block(256);
+  hipLaunchKernelGGL(group_sum_kernel, grid, block, 0, st, x, M, K, out);
+  return hipGetLastError();
+}
+
 }  // namespace moe

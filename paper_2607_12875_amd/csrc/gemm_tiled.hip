@@ -54,6 +54,22 @@ __device__ __forceinline__ bf16x8 dequant_int4x8(uint32_t w, float s) {
   return r;
 }
 
+// 8 signed nibbles -> 8 bf16 values 136 + q, exact: the bits are 0x4300 | (q + 8)
+// (128 + (q + 8), the nibble in the low mantissa bits of 128).  Element k of
+// the word (bits [4k, 4k+4)) lands in half k % 2 of dword k / 2.  `keep` = 0
+// turns every code into q = 0.  The v_bitop3 immediate is the truth table
+// over (S0, S1, S2) = (0xF0, 0xCC, 0xAA): 0x6A = (S0 & S1) ^ S2.
+__device__ __forceinline__ bf16x8 int4x8_biased_bf16(uint32_t w, uint32_t keep) {
+  const uint32_t y = __builtin_amdgcn_bitop3_b32(w, keep, 0x88888888u, 0x6A);  // q + 8 per nibble
+  const uint32_t y4 = y >> 4;                                                  // odd nibbles moved down
+  u32x4 r;
+  r.x = (__builtin_amdgcn_perm(y4, y, 0x0c040c00u) & 0x000F000Fu) | 0x43004300u;
+  r.y = (__builtin_amdgcn_perm(y4, y, 0x0c050c01u) & 0x000F000Fu) | 0x43004300u;
+  r.z = (__builtin_amdgcn_perm(y4, y, 0x0c060c02u) & 0x000F000Fu) | 0x43004300u;
+  r.w = (__builtin_amdgcn_perm(y4, y, 0x0c070c03u) & 0x000F000Fu) | 0x43004300u;
+  return as_bf16x8(r);
+}
+
 // XOR swizzle of the 16-byte chunks of a 128-byte LDS row: row r stores its
 // chunk c in slot c ^ swz<KB>(r).  For the fragment reads (32 consecutive rows,
 // lanes l and l+32 on neighbouring chunks of one row) (r >> 1) & 7 measured
@@ -102,12 +118,15 @@ void moe_gemm_tiled(GroupedGemm g) {
   // per-stage scale block: NW slots of 256 bytes, one 4-byte DMA instruction
   // each (64 floats); fp8: slots [0, BM/64) the row scales of A, slot BM/64
   // the block scales of B; int4: slots [0, BNW/64) the bf16 pair holding each
-  // B row's group scale.  Copy wave lw fills slots lw, lw + LW, ...
-  constexpr int SC = FMT == 0 ? 0 : NW / LW;  // scale loads per copy wave per stage
+  // B row's group scale, int4 GEMM1 also slots [BNW/64, BNW/64 + BM/64) the
+  // rows' biased group sums (x_gsum).  Copy wave lw fills slots lw, lw + LW, ...
+  constexpr bool GSUM = FMT == 2 && GEMM1;
+  constexpr int SC = FMT == 0 ? 0 : (GSUM ? 2 : 1) * NW / LW;  // scale loads per copy wave per stage
   static_assert(FMT != 1 || BM / 64 < NW, "fp8 scale DMA layout");
   static_assert(!F4B || (NW == 4 && BNW / 64 <= NW), "4-bit scale DMA layout");
+  static_assert(!GSUM || (BNW / 64 + BM / 64 <= 2 * NW && STAGES == 2), "int4 group-sum DMA layout");
   static_assert(STAGES >= 2 && (STAGES - 2) * (A_CH + B_CH + SC) < 64, "vmcnt range");
-  constexpr int A_BYTES = BM * KB, B_BYTES = BNW * BB, S_BYTES = FMT == 0 ? 0 : NW * 256;
+  constexpr int A_BYTES = BM * KB, B_BYTES = BNW * BB, S_BYTES = FMT == 0 ? 0 : (GSUM ? 2 : 1) * NW * 256;
   constexpr int STAGE = A_BYTES + B_BYTES + S_BYTES;
   constexpr int N_DMA = A_CH + B_CH + SC;  // loads per copy wave per stage
 
@@ -190,6 +209,11 @@ void moe_gemm_tiled(GroupedGemm g) {
           if constexpr (NP > 0) v = staged ? lds_sid[lw][r] : g.sorted_ids[m0 + r];
           else v = g.sorted_ids[m0 + r];
         }
+        const int rg = (lw + k * LW - BNW / 64) * 64 + lane;  // group-sum slot row
+        if (GSUM && lw + k * LW >= BNW / 64 && lw + k * LW < BNW / 64 + BM / 64) {
+          if constexpr (NP > 0) v = staged ? lds_sid[lw][rg] : g.sorted_ids[m0 + rg];
+          else v = g.sorted_ids[m0 + rg];
+        }
         sid[A_CH + k] = v;
       }
     }
@@ -255,6 +279,10 @@ void moe_gemm_tiled(GroupedGemm g) {
           src.s[k] = reinterpret_cast<const uint8_t*>(static_cast<const uint16_t*>(GEMM1 ? g.w1_scale : g.w2_scale) +
                                                       (static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) + n) * (K / 128));
           src.ss[k] = 1;  // advanced per step in elements below
+        } else if (GSUM && sl < BNW / 64 + BM / 64) {
+          // row (sl - BNW/64)*64 + lane: its token's sum over K step kt's group, one float per step
+          src.s[k] = reinterpret_cast<const uint8_t*>(g.x_gsum + token(sid[A_CH + k]) * (g.H / 128));
+          src.ss[k] = 4;
         }
       } else if constexpr (FMT == 4) {
         if (sl < BNW / 64) {
@@ -283,13 +311,18 @@ void moe_gemm_tiled(GroupedGemm g) {
     if (q1 < N_DMA) return;
 #pragma unroll
     for (int k = 0; k < SC; ++k) {
+      // int4 GEMM1 (two stages, so every wait drains all loads and the
+      // per-wave load counts need not match) skips its empty slots
+      if (GSUM && src.ss[k] == 0) continue;
       const uint32_t dst = base + A_BYTES + B_BYTES + (lw + k * LW) * 256;
       if constexpr (FMT == 1 || FMT == 4) {
         dma4(src.s[k] + kt * src.ss[k], dst);
       } else if constexpr (FMT == 2) {
-        // element offset kt/2 within the row, rounded down to an even element (4-byte aligned)
-        const uint8_t* p = src.s[k];
-        if (src.ss[k]) {
+        // B scale words (ss 1): element kt*KE/128 of the row, rounded down to
+        // an even element (4-byte aligned); group sums advance one float per
+        // step (ss 4); dummies stay put (ss 0)
+        const uint8_t* p = src.s[k] + kt * src.ss[k];
+        if (src.ss[k] == 1) {
           const uintptr_t a = reinterpret_cast<uintptr_t>(src.s[k]) + ((kt * KE) / 128) * 2;
           p = reinterpret_cast<const uint8_t*>(a & ~static_cast<uintptr_t>(3));
         }
@@ -385,6 +418,9 @@ void moe_gemm_tiled(GroupedGemm g) {
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
+    float seff[TN];  // int4 GEMM1: the scale each column's accumulators are divided by (0: none yet)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) seff[j] = 0.f;
 
     // B row (within the tile) of wave tile j
 #define brow(j) (GEMM1 ? ((j) < TN / 2 ? wn * (WTN / 2) + (j) * 32 : NC + wn * (WTN / 2) + ((j) - TN / 2) * 32) \
@@ -616,7 +652,74 @@ void moe_gemm_tiled(GroupedGemm g) {
           }
           __builtin_amdgcn_sched_barrier(0);
         }
+      } else if constexpr (GSUM) {
+        // int4 GEMM1.  The codes enter the MFMA exactly, as bf16 136 + q, and
+        // the group scale is applied in fp32: acc holds the tile's sum
+        // divided by its column's current scale s, so each step first takes
+        // acc * (s_prev / s) - 136 * (the row's sum over the group) and the
+        // step's MFMAs then add sum(a * (136 + q)).  A zero scale keeps the
+        // previous one and turns the group's codes into q = 0.
+        constexpr int NKK = KE / 16, NBW = NKK / 4;
+        const uint32_t* sW = reinterpret_cast<const uint32_t*>(Ss);  // one dword per tile row
+        const float* sR = reinterpret_cast<const float*>(Ss + (BNW / 64) * 256);  // [BM] biased group sums
+        float ratio[TN];
+        uint32_t keep[TN];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int r = brow(j) + l32;
+          const int n_glob = r < NC ? n0 + r : g.I + n0 + (r - NC);
+          const int idx = (e * 2 * g.I + n_glob) * (K / 128) + (kt * KE) / 128;
+          const uint32_t d = sW[r];
+          const float sc = __uint_as_float((idx & 1) ? (d & 0xFFFF0000u) : (d << 16));
+          const bool z = sc == 0.f;
+          const float se = z ? seff[j] : sc;
+          ratio[j] = seff[j] == 0.f ? 0.f : seff[j] * __builtin_amdgcn_rcpf(se);  // 1-ulp reciprocal
+          seff[j] = se;
+          keep[j] = z ? 0u : ~0u;
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int r0 = wm * WTM + i * 32 + 4 * kg;  // value v: row r0 + 8*(v/4) + v%4
+          f32x16 rs;
+#pragma unroll
+          for (int b4 = 0; b4 < 4; ++b4) {
+            const u32x4 q = ld16(sR + r0 + 8 * b4);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) rs[4 * b4 + c] = __uint_as_float(q[c]);
+          }
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = fmaf(acc[i][j][v], ratio[j], rs[v]);
+        }
+#pragma unroll
+        for (int h = 0; h < NBW; ++h) {
+          u32x4 bw[TN];
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            const int r = brow(j) + l32;
+            bw[j] = ld16(Bs + r * BB + (((NBW * kg + h) ^ swz_b<BB>(r)) << 4));
+          }
+#pragma unroll
+          for (int k4 = 0; k4 < 4; ++k4) {
+            // substep kk of lane group kg covers K elements [(NKK*kg+kk)*8, +8) of the step
+            const int kk = 4 * h + k4, ch = NKK * kg + kk;
+            bf16x8 a[TM], b[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+              const int r = wm * WTM + i * 32 + l32;
+              a[i] = as_bf16x8(ld16(As + r * KB + ((ch ^ swz<KB>(r)) << 4)));
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) b[j] = int4x8_biased_bf16(bw[j][k4], keep[j]);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+              for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(a[i], b[j], acc[i][j]);
+          }
+        }
       } else if constexpr (FMT == 2) {
+        // int4 GEMM2: each code is decoded to bf16 q * s before the MFMA;
         // this lane's scales, then per 64-element half of the step its B words
         // (one word of eight nibbles per 16-wide K substep; a lane group
         // covers KE/2 elements of the step)
@@ -713,6 +816,14 @@ void moe_gemm_tiled(GroupedGemm g) {
     // of each column block, so four consecutive columns per store.
     if constexpr (GEMM1) {
       constexpr int TH = TN / 2;  // gate tiles (paired with up tile j + TH)
+      if constexpr (GSUM) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] *= seff[j];
+      }
       float av[TM][TH][16];
 #pragma unroll
       for (int i = 0; i < TM; ++i)

@@ -28,6 +28,8 @@ hipError_t launch_combine(const void* y, bool y_f32, const float* w, const int32
                           int H, int k, bool out_bf16, void* out, hipStream_t s);
 
 hipError_t launch_act_quant(const uint16_t* x, int M, int K, uint8_t* q, float* s, hipStream_t st);
+// out[m][g] = -136 * sum of x[m][128g, 128g + 128) in fp32 (int4 GEMM1's bias term)
+hipError_t launch_group_sum(const uint16_t* x, int M, int K, float* out, hipStream_t st);
 
 // Grouped expert GEMMs.  Rows are the permuted routed rows (sorted order),
 // grouped by expert in segments padded to a multiple of the kernel's row tile;
@@ -36,6 +38,7 @@ struct GroupedGemm {
   // first product: A rows are hidden[sorted_ids[p] / top_k] (pads read row 0)
   const void* x;              // bf16 hidden [T,H] (fp8: e4m3 codes [T,H])
   const float* x_scale;       // fp8 only: [T, H/128]
+  const float* x_gsum;        // int4 only: [T, H/128], -136 * the sum of each 128-group of a hidden row
   const int32_t* sorted_ids;  // [cap]
   const int32_t* offsets;     // [E+1]
   int T, H, E, I, top_k, n_routed, max_rows;

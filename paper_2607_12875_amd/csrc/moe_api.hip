@@ -80,7 +80,7 @@ moe_ws_layout make_layout(const moe_args* a) {
     L.inter_s = take(static_cast<size_t>(cap) * (a->I / 128) * 4);
   } else {
     L.act_q = -1;
-    L.act_s = -1;
+    L.act_s = a->wfmt == MOE_W_INT4_G128 ? take(static_cast<size_t>(a->T) * (a->H / 128) * 4) : -1;
     L.inter = take(static_cast<size_t>(cap) * a->I * 2);
     L.inter_s = -1;
   }
@@ -247,7 +247,13 @@ moe_status run_layer(const moe_args* a, void* ws, size_t ws_bytes, hipEvent_t* e
   moe::GroupedGemm g;
   g.x = a->hidden;
   g.x_scale = nullptr;
+  g.x_gsum = nullptr;
   if (!mark(2)) return MOE_ERR_HIP;
+  if (a->wfmt == MOE_W_INT4_G128) {
+    float* gs = at<float>(ws, L.act_s);
+    if (moe::launch_group_sum(a->hidden, a->T, a->H, gs, stream) != hipSuccess) return MOE_ERR_HIP;
+    g.x_gsum = gs;
+  }
   if (a->wfmt == MOE_W_FP8E4M3_B128) {
     uint8_t* q = at<uint8_t>(ws, L.act_q);
     float* s = at<float>(ws, L.act_s);

@@ -195,6 +195,26 @@ def test_block_scales_vary(dev, wcfg):
     _check(cfg, inp=_scale_blocks(synth.make_inputs(cfg), cfg.wfmt))
 
 
+def test_int4_zero_and_wide_scales(dev):
+    # int4 group scales of zero (scattered, leading runs, whole rows) and
+    # scales spread over 2^-8 .. 2^8 along one weight row: the GEMM1 applies
+    # each group's scale to its partial sums, carrying the accumulators
+    # divided by the current scale from group to group.  (Wider spreads make
+    # the output so heavy-tailed -- max|out| tens of times its rms -- that one
+    # bf16 rounding step of the intermediate exceeds the rms-relative bound.)
+    cfg = synth.tiny_config(5, T=200, H=1024, I=256, E=6, top_k=2)
+    inp = synth.make_inputs(cfg)
+    rng = np.random.default_rng(7)
+    out = dict(inp)
+    for k in ("w1_scale", "w2_scale"):
+        f = O.bf16_to_f64(inp[k]) * 2.0 ** rng.integers(-8, 9, size=inp[k].shape)
+        f[rng.random(f.shape) < 0.2] = 0.0
+        f[:, ::7, :2] = 0.0    # rows whose first groups are zero
+        f[:, 3::11, :] = 0.0   # rows with no nonzero group
+        out[k] = O.f32_to_bf16_rne(f.astype(np.float32))
+    _check(cfg, inp=out)
+
+
 # ---- weight-only fp8: e4m3 weights with their block scales, bf16 activations
 @pytest.mark.parametrize("T", [1, 5, 16, 33, 128])
 def test_w8a16_small(dev, T):
