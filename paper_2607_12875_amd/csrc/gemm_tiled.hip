@@ -668,7 +668,9 @@ void moe_gemm_tiled(GroupedGemm g) {
         for (int j = 0; j < TN; ++j) {
           const int r = brow(j) + l32;
           const int n_glob = r < NC ? n0 + r : g.I + n0 + (r - NC);
-          const int idx = (e * 2 * g.I + n_glob) * (K / 128) + (kt * KE) / 128;
+          // element index of the scale; only its parity (which half of the dword) is
+          // used, so unsigned wrap-around for the largest weight tensors is harmless
+          const unsigned idx = (static_cast<unsigned>(e) * 2u * g.I + n_glob) * (K / 128) + (kt * KE) / 128;
           const uint32_t d = sW[r];
           const float sc = __uint_as_float((idx & 1) ? (d & 0xFFFF0000u) : (d << 16));
           const bool z = sc == 0.f;
@@ -730,7 +732,7 @@ void moe_gemm_tiled(GroupedGemm g) {
         for (int j = 0; j < TN; ++j) {
           const int r = brow(j) + l32;
           const int n_glob = GEMM1 ? (r < NC ? n0 + r : g.I + n0 + (r - NC)) : n0 + r;
-          const int idx = (e * (GEMM1 ? 2 * g.I : g.H) + n_glob) * (K / 128) + (kt * KE) / 128;
+          const unsigned idx = (static_cast<unsigned>(e) * (GEMM1 ? 2 * g.I : g.H) + n_glob) * (K / 128) + (kt * KE) / 128;
           const uint32_t d = sW[r];
           sb[j] = __uint_as_float((idx & 1) ? (d & 0xFFFF0000u) : (d << 16));
         }
