@@ -195,6 +195,20 @@ def test_block_scales_vary(dev, wcfg):
     _check(cfg, inp=_scale_blocks(synth.make_inputs(cfg), cfg.wfmt))
 
 
+def test_int4_hidden_group_sums(dev):
+    # the int4 GEMM1's pre-pass: act_s holds -136 times each hidden row's sum
+    # over every 128-column group (fp32 sums of the bf16 values)
+    cfg = synth.tiny_config(5, T=37, H=640, I=256, E=6, top_k=2)
+    inp = synth.make_inputs(cfg)
+    _, ws, L, _ = run_forward(cfg, inp)
+    assert L["act_s"] >= 0 and L["act_q"] < 0
+    got = ws_view(ws, L, "act_s", torch.float32, cfg.T * cfg.H // 128).reshape(cfg.T, cfg.H // 128)
+    x = O.bf16_to_f64(inp["hidden"]).reshape(cfg.T, cfg.H // 128, 128)
+    want = -136.0 * x.sum(axis=2)
+    bound = 136.0 * np.abs(x).sum(axis=2) * 2.0 ** -20   # fp32 summation of 128 terms, with room
+    assert np.all(np.abs(got - want) <= bound)
+
+
 def test_int4_zero_and_wide_scales(dev):
     # int4 group scales of zero (scattered, leading runs, whole rows) and
     # scales spread over 2^-8 .. 2^8 along one weight row: the GEMM1 applies
