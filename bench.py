@@ -206,8 +206,8 @@ def main():
         print(json.dumps(traffic_summary(*args.traffic_summary, 1024), indent=1))
         return
     if args.gpus != 1:
-        print("bench.py: this build runs the MoE layer on one GPU only; multi-GPU "
-              "sharding is a design note, not implemented (use --gpus 1).", file=sys.stderr)
+        print("bench.py: the MoE layer runs on one GPU only; sharding it across GPUs "
+              "is described in the design notes, not implemented (use --gpus 1).", file=sys.stderr)
         sys.exit(2)
 
     import torch
