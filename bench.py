@@ -358,7 +358,7 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": dtype,
-        "data": "synthetic (seeded; value recipe in DESIGN.md)",
+        "data": "synthetic (seeded; recipe in synth/moe_inputs.py)",
         "config": {"workload": DESCR[args.config] + (", logits from a fused router GEMM (bf16 [E,H])" if args.router else ""), "T": T, "H": H, "E": cfg.E, "I": I,
                    "top_k": cfg.top_k, "wfmt": cfg.wfmt, "active_experts": n_active,
                    "max_rows_per_expert": int(counts.max()), "block_m": layout["block_m"]},

@@ -560,7 +560,7 @@ void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
         for (int b = 0; b <= TM * TN; ++b) {
           const int i = b % TM, j = b / TM;
-          const int ip = (b - 1) % TM, jp = (b - 1) / TM;  // the block folded in this round
+          const int ip = (b - 1) % TM, jp = (b - 1) / TM;  // the block folded in this iteration
           if (b < TM * TN && i == 0 && j + 1 < TN) read_b(j + 1, (j + 1) & 1);
           __builtin_amdgcn_sched_barrier(0);
           const float f = b > 0 ? fa[ip] * sb[jp] : 0.f;
