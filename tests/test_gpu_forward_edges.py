@@ -66,11 +66,13 @@ def test_many_routed_rows_per_token(dev, k):
     check_forward(synth.tiny_config(1, T=90, E=48, top_k=k, H=256, I=128))
 
 
+@pytest.mark.parametrize("wcfg", [1, 5, 7])
 @pytest.mark.parametrize("T", [20, 2000])
-def test_max_experts_and_top_k(dev, T):
-    # the ABI's limits E = 1024 and top_k = 32; T = 20 takes the decode
-    # kernels, T = 2000 (64000 routed rows) the tiled ones
-    check_forward(synth.tiny_config(1, T=T, E=1024, top_k=32, H=256, I=128))
+def test_max_experts_and_top_k(dev, wcfg, T):
+    # the ABI's limits E = 1024 and top_k = 32 (bf16, int4, MXFP4); T = 20
+    # takes the decode kernels where the format has them, T = 2000 (64000
+    # routed rows) the tiled ones
+    check_forward(synth.tiny_config(wcfg, T=T, E=1024, top_k=32, H=256, I=128))
 
 
 @pytest.mark.parametrize("wcfg", [1, 5])
