@@ -88,8 +88,8 @@ __device__ __forceinline__ int swz_b(int r) { return BB == 32 ? (r >> 2) & 1 : (
 // (L1 waiting on L2) cannot hold up the MFMA stream behind an in-order copy
 // instruction.  NP == 0: the math waves issue the copies themselves.
 template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM, int KBT = 128, int STAGES = 3, int NP = 0>
-// The 64-row 4-bit GEMM1s are held to 128 registers, which keeps two workgroups per CU.
-__global__ __launch_bounds__((WM * WN + NP) * 64) __attribute__((amdgpu_waves_per_eu((FMT == 2 || FMT == 4) && GEMM1 && BM == 64 ? 4 : 1)))
+// The 64-row 4-bit GEMMs with copy waves are held to 128 registers, which keeps two workgroups per CU.
+__global__ __launch_bounds__((WM * WN + NP) * 64) __attribute__((amdgpu_waves_per_eu((FMT == 2 || FMT == 4) && (GEMM1 || NP > 0) && BM == 64 ? 4 : 1)))
 void moe_gemm_tiled(GroupedGemm g) {
   constexpr int NW = WM * WN, NT = (NW + NP) * 64;
   constexpr int LW = NP > 0 ? NP : NW;  // waves that issue the copies
@@ -991,7 +991,7 @@ hipError_t launch_tiled(const GroupedGemm& g, hipStream_t s) {
 #define MOE_TI4_NP1 4
 #endif
 #ifndef MOE_TI4_NP2
-#define MOE_TI4_NP2 0
+#define MOE_TI4_NP2 4
 #endif
 // most row tiles of one expert swept together per column tile
 #ifndef MOE_TGM
