@@ -5,16 +5,19 @@ weighted combine) on one MI355X.
     python bench.py [--steps K] [--warmup W] [--config N]
 
 One step is one ``moe_forward`` call over one batch of synthetic inputs that
-are already resident in HBM.  The default workload is the decode-shaped layer
-(T=16, H=4096, E=64, I=1408, top_k=6, bf16 weights); ``--config`` selects one
-of the other workloads for exploration.  Prints ONE JSON line on stdout.
+are already resident in HBM.  The default workload is the largest one that
+fits one GPU, the fp8 block-quantised layer (T=8192, H=7168, E=256, I=2048,
+top_k=8); ``--config`` selects one of the other workloads.  Prints ONE JSON
+line on stdout.
 
 Timing:
   * whole layer: HIP events on the launch stream around exactly K calls,
     bracketed by device synchronisation; host wall clock reported beside it.
-    Each timed call is ``moe_forward_profiled`` with only the two events
-    around GEMM1 set, so the dominant kernel's per-launch duration (the
-    roofline's denominator) is measured live inside the same timed region;
+    Each timed call is ``moe_forward_profiled`` with an event at its start
+    (so every step's duration is known: median, p10 and p90 are reported
+    beside the mean) and the two events around GEMM1, so the dominant
+    kernel's per-launch duration (the roofline's denominator) is measured
+    live inside the same timed region;
   * per stage: after the timed region, K further calls with events between
     all stages (a breakdown only; these events cost a few microseconds each);
   * graph: the same layer captured once in a HIP graph and replayed K times
@@ -125,11 +128,9 @@ def cpu_baseline(cfg, inputs, budget_s: float):
     """Time the fp64 oracle on the host: the whole layer when it fits the
     budget, else a token sample; returns the baseline record."""
     from oracle import moe_oracle as O
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover - threadpoolctl is optional
-        cores = 1
+    # the oracle evaluates its experts on this many threads at once (one BLAS
+    # thread each)
+    cores = O.default_threads()
     tokens = None
     n_tok = cfg.T
     # the oracle dequantises every expert a token routes to: bound that work
@@ -189,7 +190,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", type=int, default=2, choices=sorted(DESCR))
+    ap.add_argument("--config", type=int, default=4, choices=sorted(DESCR))
     ap.add_argument("--router", action="store_true",
                     help="compute the logits in-layer from a router weight [E,H] (router GEMM fused "
                          "with the gate); the FLOP count stays that of the experts")
@@ -252,21 +253,23 @@ def main():
 
     # ---- whole layer: exactly K steps between two synchronisations; every
     # step brackets its GEMM1 launch with a pair of events of its own
+    # events: 0 .. K-1 the start of each step, K the end of the last, then
+    # the GEMM1 pair of each step
     K = args.steps
-    ev = HipEvents(2 + 2 * K)
+    ev = HipEvents(1 + 3 * K)
     rt = ev.rt
     rt.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
-    g1_marks = [[None, None, None, ev.ev[2 + 2 * i], ev.ev[3 + 2 * i], None, None] for i in range(K)]
+    g1_marks = [[ev.ev[i], None, None, ev.ev[K + 1 + 2 * i], ev.ev[K + 2 + 2 * i], None, None] for i in range(K)]
     torch.cuda.synchronize()
     w0 = time.perf_counter()
-    rt.hipEventRecord(ev.ev[0], ctypes.c_void_p(stream.cuda_stream))
     for i in range(K):
         moe.moe_forward_profiled(margs, ws, g1_marks[i])
-    rt.hipEventRecord(ev.ev[1], ctypes.c_void_p(stream.cuda_stream))
+    rt.hipEventRecord(ev.ev[K], ctypes.c_void_p(stream.cuda_stream))
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - w0) * 1e3 / K
-    ms = ev.elapsed_ms(0, 1) / K
-    g1_launch_us = [ev.elapsed_ms(2 + 2 * i, 3 + 2 * i) * 1e3 for i in range(K)]
+    ms = ev.elapsed_ms(0, K) / K
+    step_us = np.array([ev.elapsed_ms(i, i + 1) * 1e3 for i in range(K)])
+    g1_launch_us = [ev.elapsed_ms(K + 1 + 2 * i, K + 2 + 2 * i) * 1e3 for i in range(K)]
     ev.close()
 
     # ---- per-stage breakdown (after the timed region): events between stages
@@ -330,6 +333,7 @@ def main():
     key = f"{synth.config(args.config).name}_gemm1"
     traffic = load_traffic(key, src_hash)
     common = {"kernel": "gemm1 (+SiLU*up)", "traffic": traffic, "launch_us": g1_us,
+              "launch_us_median": float(np.median(g1_launch_us)),
               "algorithmic_bytes_per_launch": g1_bytes, "algorithmic_flops_per_launch": g1_flops,
               "roof_us": {"hbm": t_hbm * 1e6, "mfma": t_mfma * 1e6}}
     if bound == "hbm":
@@ -363,6 +367,9 @@ def main():
                    "top_k": cfg.top_k, "wfmt": cfg.wfmt, "active_experts": n_active,
                    "max_rows_per_expert": int(counts.max()), "block_m": layout["block_m"]},
         "us_per_layer": ms * 1e3,
+        "us_per_layer_median": float(np.median(step_us)),
+        "us_per_layer_p10": float(np.percentile(step_us, 10)),
+        "us_per_layer_p90": float(np.percentile(step_us, 90)),
         "wall_us_per_layer": wall_ms * 1e3,
         "graph_us_per_layer": graph_us,
         "stage_us": stage_us,

@@ -26,7 +26,11 @@
  *     error nothing is enqueued and outputs are untouched.
  *   - Calls on one stream are ordered; concurrent calls that share output or
  *     workspace buffers race.
- *   - Inputs must be finite; NaN/Inf inputs give unspecified results.
+ *   - Inputs must be finite, with one exception: a router logit or a
+ *     selection bias of -inf masks that expert (it is chosen only when a
+ *     token has fewer than top_k other experts, lowest index first, and a
+ *     masked softmax logit gets weight 0).  NaN and +inf give unspecified
+ *     results.
  */
 #ifndef MOE_H
 #define MOE_H

@@ -49,6 +49,9 @@ implementation; nothing here is "parity unpinned".
 """
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 E4M3_MAX = 448.0
@@ -290,12 +293,32 @@ def activation_operand(hidden_bits, wfmt="bf16", mirror=True):
     return x
 
 
-def forward(cfg, inputs, mirror=True, tokens=None, want_rows=False):
+def _blas_threads(n):
+    """Context that holds the BLAS library to n threads (a no-op without
+    threadpoolctl)."""
+    try:
+        from threadpoolctl import threadpool_limits
+        return threadpool_limits(limits=n, user_api="blas")
+    except ImportError:  # pragma: no cover
+        import contextlib
+        return contextlib.nullcontext()
+
+
+def default_threads() -> int:
+    """Experts the layer evaluates at once: OMP_NUM_THREADS if set, else the
+    core count, at most 16 (each one holds its dequantised weights)."""
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    n = int(env) if env.isdigit() and int(env) > 0 else (os.cpu_count() or 1)
+    return max(1, min(n, 16))
+
+
+def forward(cfg, inputs, mirror=True, tokens=None, want_rows=False, threads=None):
     """The whole layer.  ``tokens``: optional subset of token indices, in
     which case ``out`` has one row per listed token (gate and experts run for
     those tokens only).  Returns a dict with ids, w, out and, if
     ``want_rows``, the per-routed-row intermediates ``a`` and ``y`` indexed by
-    (token slot, j)."""
+    (token slot, j).  ``threads``: experts evaluated at once (default: the
+    host's core count)."""
     T, k = cfg.T, cfg.top_k
     tok = np.arange(T) if tokens is None else np.asarray(tokens, dtype=np.int64)
     ids, w = gate(inputs["logits"][tok], inputs.get("sel_bias"), k, cfg.mode,
@@ -305,15 +328,27 @@ def forward(cfg, inputs, mirror=True, tokens=None, want_rows=False):
     y = np.zeros((n * k, cfg.H))
     a_rows = np.zeros((n * k, cfg.I)) if want_rows else None
     flat = ids.reshape(-1)
-    for e in np.unique(flat):
+
+    def one_expert(e):
         rows = np.nonzero(flat == e)[0]                     # flat slots t*k+j, ascending
         w1 = dequant_weight(cfg.wfmt, inputs["w1"][e], None if inputs["w1_scale"] is None else inputs["w1_scale"][e])
         w2 = dequant_weight(cfg.wfmt, inputs["w2"][e], None if inputs["w2_scale"] is None else inputs["w2_scale"][e])
         a, ye = swiglu_expert(x[rows // k], w1, w2, cfg.wfmt, mirror)
-        y[rows] = ye
+        y[rows] = ye                                        # experts write disjoint rows
         if want_rows:
             a_rows[rows] = a
-        del w1, w2
+
+    # Experts are independent; running several at once changes no arithmetic
+    # (each one's rows, weights and products are its own).
+    experts = np.unique(flat)
+    workers = max(1, min(threads or default_threads(), experts.size))
+    if workers == 1:
+        for e in experts:
+            one_expert(e)
+    else:
+        # one BLAS thread per expert: the experts themselves fill the cores
+        with _blas_threads(1), ThreadPoolExecutor(max_workers=workers) as pool:
+            list(pool.map(one_expert, experts))
     out = (w[:, :, None] * y.reshape(n, k, cfg.H)).sum(axis=1)
     res = {"ids": ids, "w": w, "out": out}
     if want_rows:

@@ -73,6 +73,15 @@ __device__ __forceinline__ void gate_argmax_row(const float* lg, const float* bi
   double key[EPL], lv[EPL];  // lv: logit in fp64 (softmax) or sigmoid score (sigmoid)
   gate_keys<EPL>(lg, bias, E, mode, key, lv);
 
+  // taken: bit i set once expert lane + 64 i has been selected (or does not
+  // exist).  A key of -inf (a masked expert) still competes: the first
+  // untaken expert a lane sees is its candidate even at -inf, so a token with
+  // fewer than k finite keys picks its remaining experts by lowest index, as
+  // a stable sort on the keys does.
+  uint32_t taken = 0;
+#pragma unroll
+  for (int i = 0; i < EPL; ++i)
+    if (lane + 64 * i >= E) taken |= 1u << i;
   int my_id = 0;
   double my_v = 0.0;
   for (int j = 0; j < k; ++j) {
@@ -80,11 +89,14 @@ __device__ __forceinline__ void gate_argmax_row(const float* lg, const float* bi
     int be = 0x7fffffff;
 #pragma unroll
     for (int i = 0; i < EPL; ++i)
-      if (key[i] > bv) { bv = key[i]; be = lane + 64 * i; }  // strict: lower index kept
+      if (!(taken >> i & 1) && (key[i] > bv || be == 0x7fffffff)) {  // strict: lower index kept
+        bv = key[i];
+        be = lane + 64 * i;
+      }
     wave_argmax(bv, be);
 #pragma unroll
     for (int i = 0; i < EPL; ++i)
-      if (lane + 64 * i == be) key[i] = -INFINITY;
+      if (lane + 64 * i == be) taken |= 1u << i;
     // the owner lane broadcasts the selected expert's logit / score
     double v = 0.0;
 #pragma unroll

@@ -932,14 +932,18 @@ int cu_count() {
   return n;
 }
 
-// Persistent grid: as many workgroups as fit on the device at once (a
-// multiple of the XCD count), never more than the largest possible number of
-// tiles.
 template <class Kernel>
-dim3 persistent_grid(Kernel k, int threads, long max_tiles) {
+int occupancy_per_cu(Kernel k, int threads) {
   int per_cu = 1;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, threads, 0) != hipSuccess || per_cu < 1)
     per_cu = 1;
+  return per_cu;
+}
+
+// Persistent grid: as many workgroups as fit on the device at once (per_cu
+// per CU, a multiple of the XCD count), never more than the largest possible
+// number of tiles.
+dim3 persistent_grid(int per_cu, long max_tiles) {
   long n = static_cast<long>(cu_count()) * per_cu;
   n = (n + kXcds - 1) / kXcds * kXcds;
   const long cap = (max_tiles + kXcds - 1) / kXcds * kXcds;
@@ -952,7 +956,10 @@ hipError_t launch_tiled(const GroupedGemm& g, hipStream_t s) {
   constexpr int NT = (WM * WN + NP) * 64;
   const long mt = g.max_rows / BM, nt = (GEMM1 ? g.I : g.H) / NC;
   auto kern = moe_gemm_tiled<FMT, GEMM1, BM, BNW, WM, WN, GM, KBT, STAGES, NP>;
-  hipLaunchKernelGGL(kern, persistent_grid(kern, NT, mt * nt), dim3(NT), 0, s, g);
+  // workgroups per CU depend on the kernel's registers and LDS only: queried
+  // once per instantiation (thread-safe static initialisation)
+  static const int per_cu = occupancy_per_cu(kern, NT);
+  hipLaunchKernelGGL(kern, persistent_grid(per_cu, mt * nt), dim3(NT), 0, s, g);
   return hipGetLastError();
 }
 
@@ -978,9 +985,9 @@ hipError_t launch_tiled(const GroupedGemm& g, hipStream_t s) {
 #ifndef MOE_TBF_STAGES
 #define MOE_TBF_STAGES 3
 #endif
-// Copy waves beside the math waves (0: the math waves copy).  The int4
-// GEMM2 launch keeps its math waves copying: the extra waves' registers
-// would evict the second workgroup per CU it otherwise runs.
+// Copy waves beside the math waves (0: the math waves copy).  Every tiled
+// launch uses four; the 64-row int4 kernels are held to 128 registers so two
+// workgroups of eight waves still fit per CU.
 #ifndef MOE_TBF_NP1
 #define MOE_TBF_NP1 4
 #endif

@@ -10,19 +10,21 @@ namespace moe {
 // `lds + 16*l` (`lds + 4*l`); inactive lanes neither load nor write.  Issued
 // as inline asm so the compiler does not treat every later LDS read as
 // dependent on it; completion is awaited explicitly with vm_wait<N>().
-// `lds` must be uniform across the wave.
+// `lds` must be uniform across the wave.  An LDS-DMA that reads M0 needs one
+// wait state after the SALU write of M0; the hazard recognizer cannot see
+// inside inline asm, so the s_nop is written out here.
 __device__ __forceinline__ void dma16(const void* gptr, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
                "v"(gptr) : "memory", "m0");
 }
 // The same with the non-temporal hint: for data read exactly once (streamed
 // weights), so it does not displace reused lines in L2.
 __device__ __forceinline__ void dma16_nt(const void* gptr, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off nt" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off nt" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
                "v"(gptr) : "memory", "m0");
 }
 __device__ __forceinline__ void dma4(const void* gptr, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, off" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
                "v"(gptr) : "memory", "m0");
 }
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {

@@ -5,9 +5,7 @@ import numpy as np
 import pytest
 
 import synth
-from oracle import moe_oracle as O
-from tests.gpu_util import TOL, rel_err, require_gpu, run_forward, ws_view
-import torch
+from tests.gpu_util import check_forward, require_gpu, run_forward
 
 pytestmark = pytest.mark.gpu
 
@@ -18,24 +16,7 @@ def dev():
 
 
 def _check(cfg, inp=None, out_dtype="f32"):
-    print(f"forward parity {cfg}", flush=True)
-    inp = synth.make_inputs(cfg) if inp is None else inp
-    out, ws, L, _ = run_forward(cfg, inp, out_dtype)
-    ref = O.forward(cfg, inp)
-    n = cfg.T * cfg.top_k
-    ids = ws_view(ws, L, "topk_ids", torch.int32, n).reshape(cfg.T, cfg.top_k)
-    assert np.array_equal(ids, ref["ids"])
-    ro, rs, ri = O.permute(ref["ids"], cfg.E, L["block_m"])
-    assert np.array_equal(ws_view(ws, L, "expert_offsets", torch.int32, cfg.E + 1), ro)
-    assert np.array_equal(ws_view(ws, L, "sorted_ids", torch.int32, L["cap"]), rs)
-    assert np.array_equal(ws_view(ws, L, "inv_pos", torch.int32, n), ri)
-    err = rel_err(out, ref["out"])
-    print(f"  max|err|/rms = {err:.3e} (block_m={L['block_m']})", flush=True)
-    rms = np.sqrt((ref["out"] ** 2).mean())
-    # a bf16 output adds its own rounding: at most 2^-9 of each element
-    slack = 0.0 if out_dtype == "f32" else 2 ** -9 * np.abs(ref["out"]).max() / rms
-    assert err <= TOL[cfg.wfmt] + slack
-    return out, ref
+    return check_forward(cfg, inp, out_dtype)
 
 
 def test_tiny_config_full_size(dev):

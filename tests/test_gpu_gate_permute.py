@@ -57,6 +57,29 @@ def test_gate_integer_ties(dev):
     _check_gate(dev, np.zeros((5, 256), np.float32), np.zeros(256, np.float32), 8, "sigmoid", True, 2.5)
 
 
+@pytest.mark.parametrize("E,k", [(48, 6), (128, 8), (300, 12)])
+@pytest.mark.parametrize("mode", ["softmax", "sigmoid"])
+def test_gate_masked_experts(dev, E, k, mode):
+    # experts masked with -inf keys (a -inf logit in softmax mode, a -inf
+    # selection bias in sigmoid mode): rows with fewer than k finite keys pick
+    # their remaining experts by lowest index among the masked ones, as the
+    # stable order does; rank selection for E <= 64, arg-max rounds above
+    rng = np.random.default_rng(E + k)
+    T = 200
+    lg = rng.standard_normal((T, E)).astype(np.float32)
+    finite = rng.integers(1, k + 3, size=T)                  # finite keys per row
+    keep = np.argsort(rng.random((T, E)), axis=1) < finite[:, None]
+    if mode == "softmax":
+        lg[~keep] = -np.inf
+        _check_gate(dev, lg, None, k, mode, True, 1.0)
+        _check_gate(dev, lg, None, k, mode, False, 1.0)
+    else:
+        # one bias row for every token: mask the same experts in all rows
+        b = np.where(keep[0], rng.standard_normal(E) * 0.1, -np.inf).astype(np.float32)
+        _check_gate(dev, lg, b, k, mode, True, 2.5)
+        _check_gate(dev, lg, b, k, mode, False, 2.5)
+
+
 def _check_permute(dev, ids, E, block_m):
     t = torch.from_numpy(np.ascontiguousarray(ids, dtype=np.int32)).to(dev)
     off, sid, inv = moe.moe_permute(t, E, block_m)

@@ -67,10 +67,10 @@ def test_router_gate_shapes(dev, T, H, E, k, n):
 
 
 def test_router_gate_workload_shapes(dev):
-    # decode (T=16, H=4096, E=64) whole; the fp8 workload's routing (T=8192,
-    # H=7168, E=256) with oracle logits on sampled tokens, ids on all
+    # decode (T=16, H=4096, E=64) and the fp8 workload's routing (T=8192,
+    # H=7168, E=256): logits of every token against the fp64 sums
     _check_router(dev, synth.config(2))
-    _check_router(dev, synth.config(4), sample=[0, 1, 2047, 4096, 8190, 8191])
+    _check_router(dev, synth.config(4))
 
 
 @pytest.mark.parametrize("n,T", [(2, 16), (1, 300), (4, 200), (6, 16)])

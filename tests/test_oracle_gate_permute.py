@@ -69,6 +69,28 @@ def test_gate_ids_vs_brute_force(n):
     assert all(len(set(row)) == cfg.top_k for row in ids.tolist())
 
 
+def test_gate_masked_experts_vs_brute_force():
+    # -inf keys (masked experts): a row with fewer than k finite keys takes
+    # its remaining experts among the masked ones by lowest index, as the
+    # repeated scan does; masked experts get weight 0
+    rng = np.random.default_rng(11)
+    lg = rng.standard_normal((300, 40)).astype(np.float32)
+    keep = np.argsort(rng.random((300, 40)), axis=1) < rng.integers(1, 9, size=300)[:, None]
+    lg[~keep] = -np.inf
+    ids, w = O.gate(lg, None, 6, "softmax", True, 1.0)
+    for t in range(300):
+        assert ids[t].tolist() == _brute_topk(lg[t].tolist(), 6)
+    assert np.allclose(w.sum(1), 1.0, rtol=0, atol=1e-12)
+    assert np.all((w == 0) == ~np.take_along_axis(keep, ids, axis=1))
+    b = np.where(keep[0], 0.0, -np.inf).astype(np.float32)
+    lg = rng.standard_normal((300, 40)).astype(np.float32)
+    ids, w = O.gate(lg, b, 6, "sigmoid", True, 2.5)
+    assert np.allclose(w.sum(1), 2.5, rtol=0, atol=1e-12)
+    key = 1 / (1 + np.exp(-lg.astype(np.float64))) + b
+    for t in range(300):
+        assert ids[t].tolist() == _brute_topk(key[t].tolist(), 6)
+
+
 def test_gate_crafted_integer_ties():
     rng = np.random.default_rng(3)
     lg = rng.integers(-2, 3, (500, 16)).astype(np.float32)   # many exact ties
