@@ -65,7 +65,9 @@ typedef enum {
 
 /* Expert weight storage.  N x K below is [2I x H] for W1 and [H x I] for W2. */
 typedef enum {
-  /* bf16 bits, w[e][n][k] (uint16_t).  Needs H, I multiples of 128. */
+  /* bf16 bits, w[e][n][k] (uint16_t).  H and I multiples of 8 (rows stay
+     16-byte aligned); when either is not a multiple of 128 every batch runs
+     the tiled kernels (segments padded to 128 rows). */
   MOE_W_BF16 = 0,
   /* OCP fp8 e4m3fn codes (bias 7, max 448, no Inf, S.1111.111 = NaN),
      w[e][n][k] (uint8_t); fp32 scale per 128x128 block of [N,K]:
@@ -233,7 +235,9 @@ moe_status moe_workspace_layout(const moe_args* a, moe_ws_layout* layout);
  * grouped GEMM1 with fused SiLU*up epilogue -> grouped GEMM2 -> combine, all
  * enqueued on `stream`; no host synchronisation, no allocation.
  * Requirements: T >= 0; 1 <= E <= MOE_MAX_EXPERTS; 1 <= top_k <= min(E,
- * MOE_MAX_TOPK); H and I multiples of 128; every device pointer 16-byte
+ * MOE_MAX_TOPK); 8 <= H, I <= 65536, multiples of 8 for MOE_W_BF16 and of
+ * 128 for the quantised formats (with w_router, H a multiple of 128 in every
+ * format, else MOE_ERR_UNSUPPORTED); every device pointer 16-byte
  * aligned; ws_bytes >= moe_workspace_bytes(a); sel_bias only with a format
  * that reads it (both scoring modes do).  Padding rows of the intermediates
  * are unspecified.  T == 0 is a no-op.
@@ -259,6 +263,25 @@ moe_status moe_forward(const moe_args* a, void* ws, size_t ws_bytes, hipStream_t
 #define MOE_NUM_STAGES 6
 moe_status moe_forward_profiled(const moe_args* a, void* ws, size_t ws_bytes,
                                 hipEvent_t* events, hipStream_t stream);
+
+/*
+ * moe_forward without a caller workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  The layer runs exactly as moe_forward, but its
+ * intermediates live in the library's own device array of
+ * MOE_STATIC_WS_BYTES, one per GPU, which exists from the first use of the
+ * library on that GPU until the process ends.  The caller still passes
+ * every input and output in `a`.  The call allocates nothing.
+ *   a       as moe_forward; moe_workspace_bytes(a) must not exceed
+ *           MOE_STATIC_WS_BYTES, else MOE_ERR_WORKSPACE (nothing enqueued).
+ * Every call on one GPU shares that GPU's array and leaves its intermediates
+ * there (nothing in it needs to start zeroed): calls that overlap on one GPU
+ * (on different streams, or from several threads without ordering) race.
+ * Errors: those of moe_forward; MOE_ERR_HIP if the array's device address
+ * cannot be obtained.
+ */
+#define MOE_STATIC_WS_BYTES (256u << 20)
+moe_status moe_forward_static_ws(const moe_args* a, hipStream_t stream);
 
 /* Static, NUL-terminated name of a status code. */
 const char* moe_status_str(int status);

@@ -7,7 +7,7 @@ build script (``build``).
 """
 from ._binding import (  # noqa: F401
     LIB_PATH, NUM_STAGES, STAGES, MoeArgs, MoeError, lib, make_args, moe_act_quant_fp8, moe_forward,
-    moe_forward_args, moe_forward_profiled, moe_gate_topk, moe_permute, moe_permute_capacity,
+    STATIC_WS_BYTES, moe_forward_args, moe_forward_profiled, moe_forward_static_ws, moe_gate_topk, moe_permute, moe_permute_capacity,
     moe_router_gate_topk,
     moe_permute_workspace_bytes, moe_workspace_bytes, moe_workspace_layout,
 )

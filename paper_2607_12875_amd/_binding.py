@@ -24,7 +24,8 @@ OFMT = {"f32": 0, "bf16": 1}
 
 EXPORTED = ("moe_status_str", "moe_permute_capacity", "moe_permute_workspace_bytes",
             "moe_gate_topk", "moe_router_gate_topk", "moe_permute", "moe_act_quant_fp8", "moe_workspace_bytes",
-            "moe_workspace_layout", "moe_forward", "moe_forward_profiled")
+            "moe_workspace_layout", "moe_forward", "moe_forward_profiled", "moe_forward_static_ws")
+STATIC_WS_BYTES = 256 << 20  # MOE_STATIC_WS_BYTES: the library's own per-GPU workspace
 NUM_STAGES = 6
 STAGES = ("gate", "permute", "act_quant", "gemm1", "gemm2", "combine")
 
@@ -88,6 +89,8 @@ def lib() -> ctypes.CDLL:
         L.moe_workspace_layout.argtypes = [ctypes.POINTER(MoeArgs), ctypes.POINTER(MoeWsLayout)]
         L.moe_forward.restype = i32
         L.moe_forward.argtypes = [ctypes.POINTER(MoeArgs), vp, sz, vp]
+        L.moe_forward_static_ws.restype = i32
+        L.moe_forward_static_ws.argtypes = [ctypes.POINTER(MoeArgs), vp]
         L.moe_forward_profiled.restype = i32
         L.moe_forward_profiled.argtypes = [ctypes.POINTER(MoeArgs), vp, sz,
                                            ctypes.POINTER(ctypes.c_void_p), vp]
@@ -209,6 +212,13 @@ def moe_forward_args(args: MoeArgs, workspace, stream=None):
     """Run the layer on a prepared MoeArgs with a caller-owned uint8 workspace."""
     _check(lib().moe_forward(ctypes.byref(args), _ptr(workspace), workspace.numel(),
                              _stream(stream)), "moe_forward")
+
+
+def moe_forward_static_ws(args: MoeArgs, stream=None):
+    """Run the layer on a prepared MoeArgs in the library's own per-GPU
+    workspace (no workspace argument, nothing allocated); the workspace the
+    sizes need must not exceed STATIC_WS_BYTES."""
+    _check(lib().moe_forward_static_ws(ctypes.byref(args), _stream(stream)), "moe_forward_static_ws")
 
 
 def moe_forward_profiled(args: MoeArgs, workspace, events, stream=None):

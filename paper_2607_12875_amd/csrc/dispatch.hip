@@ -3,7 +3,7 @@
 
 namespace moe {
 
-int gemm_block_m_bf16(int T, int top_k, int E);
+int gemm_block_m_bf16(int T, int top_k, int E, int H, int I);
 hipError_t launch_gemm1_bf16(const GroupedGemm& g, hipStream_t s);
 hipError_t launch_gemm2_bf16(const GroupedGemm& g, hipStream_t s);
 int gemm_block_m_fp8(int T, int top_k, int E);
@@ -24,13 +24,13 @@ hipError_t launch_gemm2_mxfp4_tiled(const GroupedGemm& g, hipStream_t s);
 // average, the tiled kernels above (the row tile is the permute's padding)
 static bool mxfp4_decode(int T, int top_k, int E) { return static_cast<long>(T) * top_k <= 32L * E; }
 
-int gemm_block_m(int wfmt, int T, int top_k, int E) {
+int gemm_block_m(int wfmt, int T, int top_k, int E, int H, int I) {
   switch (wfmt) {
     case 1: return gemm_block_m_fp8(T, top_k, E);
     case 2: return gemm_block_m_int4(T, top_k, E);
     case 3: return 16;  // the weight-only fp8 route runs the 16-row decode kernels only
     case 4: return mxfp4_decode(T, top_k, E) ? 16 : gemm_block_m_mxfp4();
-    default: return gemm_block_m_bf16(T, top_k, E);
+    default: return gemm_block_m_bf16(T, top_k, E, H, I);
   }
 }
 

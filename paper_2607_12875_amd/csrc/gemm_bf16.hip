@@ -641,8 +641,11 @@ __global__ __launch_bounds__(256) void gemm_w4a16_skinny(GroupedGemm g) {
 }
 
 // ----------------------------------------------------------------- dispatch
-bool bf16_use_skinny(int T, int top_k, int E) {
-  return static_cast<long>(T) * top_k <= 32L * E;  // <= 32 rows per expert on average
+// The 16-row decode kernels: at most 32 rows per expert on average, and H, I
+// multiples of 128 (other bf16 shapes, multiples of 8, run the tiled kernels,
+// which handle a ragged last K step and column tile).
+bool bf16_use_skinny(int T, int top_k, int E, int H, int I) {
+  return static_cast<long>(T) * top_k <= 32L * E && H % 128 == 0 && I % 128 == 0;
 }
 
 // Decode tile knobs: weight subtiles of 16 rows per workgroup and k-steps of
@@ -805,9 +808,9 @@ bool stream_fits(int K, int N, int nc) {
 }
 
 hipError_t launch_gemm1_bf16(const GroupedGemm& g, hipStream_t s) {
-  if (bf16_use_skinny(g.T, g.top_k, g.E) && stream_fits(g.H, g.I, MOE_STREAM_NG1 / 2 * 16))
+  if (bf16_use_skinny(g.T, g.top_k, g.E, g.H, g.I) && stream_fits(g.H, g.I, MOE_STREAM_NG1 / 2 * 16))
     return launch_stream<MOE_STREAM_NG1, true>(g, s);
-  if (bf16_use_skinny(g.T, g.top_k, g.E)) {
+  if (bf16_use_skinny(g.T, g.top_k, g.E, g.H, g.I)) {
     constexpr int NS = MOE_SKINNY1_NSUB;
     const dim3 grid(g.I / (NS / 2 * 16), g.max_rows / 16);
     hipLaunchKernelGGL((gemm_bf16_skinny<NS, MOE_SKINNY1_UNROLL, true>), grid, dim3(256), 0, s, g);
@@ -817,9 +820,9 @@ hipError_t launch_gemm1_bf16(const GroupedGemm& g, hipStream_t s) {
 }
 
 hipError_t launch_gemm2_bf16(const GroupedGemm& g, hipStream_t s) {
-  if (bf16_use_skinny(g.T, g.top_k, g.E) && stream_fits(g.I, g.H, MOE_STREAM_NG2 * 16))
+  if (bf16_use_skinny(g.T, g.top_k, g.E, g.H, g.I) && stream_fits(g.I, g.H, MOE_STREAM_NG2 * 16))
     return launch_stream<MOE_STREAM_NG2, false>(g, s);
-  if (bf16_use_skinny(g.T, g.top_k, g.E)) {
+  if (bf16_use_skinny(g.T, g.top_k, g.E, g.H, g.I)) {
     constexpr int NS = MOE_SKINNY2_NSUB;
     const dim3 grid(g.H / (NS * 16), g.max_rows / 16);
     hipLaunchKernelGGL((gemm_bf16_skinny<NS, MOE_SKINNY2_UNROLL, false>), grid, dim3(256), 0, s, g);
@@ -868,8 +871,8 @@ hipError_t launch_gemm2_w8a16(const GroupedGemm& g, hipStream_t s) {
   return hipGetLastError();
 }
 
-int gemm_block_m_bf16(int T, int top_k, int E) {
-  return bf16_use_skinny(T, top_k, E) ? 16 : bf16_tiled_block_m();
+int gemm_block_m_bf16(int T, int top_k, int E, int H, int I) {
+  return bf16_use_skinny(T, top_k, E, H, I) ? 16 : bf16_tiled_block_m();
 }
 
 }  // namespace moe

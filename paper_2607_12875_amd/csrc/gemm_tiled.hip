@@ -43,6 +43,11 @@ namespace moe {
 constexpr int kXcds = 8;
 constexpr int MOE_MAX_EXPERTS_DEV = 1024;  // the ABI's expert limit
 
+// Sixteen zero bytes: the source of every bf16 copy chunk that lies past the
+// end of K (K a multiple of 8 but not of the 64-element step), so a ragged
+// last step multiplies zeros and reads nothing beyond a row.
+__device__ __align__(16) const uint8_t kZeroChunk[16] = {};
+
 // 8 signed nibbles -> 8 bf16 values q * s (s an fp32 copy of a bf16 scale).
 __device__ __forceinline__ bf16x8 dequant_int4x8(uint32_t w, float s) {
   bf16x8 r;
@@ -145,8 +150,11 @@ void moe_gemm_tiled(GroupedGemm g) {
   const int l32 = lane & 31, kg = lane >> 5;
   const int K = GEMM1 ? g.H : g.I;
   const int N = GEMM1 ? g.I : g.H;       // output columns of the product
-  const int nk = K / KE;
-  const int n_tiles_n = N / NC;
+  // bf16 only: K and N multiples of 8 -- a ragged last K step (zero chunks)
+  // and a ragged last column tile (weight rows clamped, stores masked); the
+  // quantised formats have K and N multiples of 128
+  const int nk = (K + KE - 1) / KE;
+  const int n_tiles_n = (N + NC - 1) / NC;
   for (int i = tid; i <= g.E; i += NT) lds_off[i] = g.offsets[i];
   __syncthreads();
   const int n_tiles_m = lds_off[g.E] / BM;
@@ -239,9 +247,11 @@ void moe_gemm_tiled(GroupedGemm g) {
       const int blk = i * LW + lw;
       const int r = F4B ? blk * (64 / LPB) + lane / LPB : blk * RPI + lane / LPR;
       const int sl = F4B ? (lane % LPB) ^ swz_b<BB>(r) : (lane % LPR) ^ swz<KB>(r);
+      // weight rows past N (a ragged last column tile) read the last row:
+      // their columns are never stored
       int n;
-      if (GEMM1) n = r < NC ? n0 + r : g.I + n0 + (r - NC);
-      else n = n0 + r;
+      if (GEMM1) n = r < NC ? min(n0 + r, g.I - 1) : g.I + min(n0 + (r - NC), g.I - 1);
+      else n = min(n0 + r, g.H - 1);
       src.b[i] = wbase + static_cast<size_t>(n) * w_row_bytes + (sl << 4);
     }
     // scale DMA sources of this lane, one per slot lw + k*LW (advanced by one
@@ -300,14 +310,27 @@ void moe_gemm_tiled(GroupedGemm g) {
   // issue step kt of the tile `src` describes (DMA q in [q0, q1) of this copy
   // wave's A_CH + B_CH tile loads, plus the scale loads with q1 == N_DMA)
   // into LDS buffer `buf`
+  // bf16 ragged K: in the last step a lane whose 8-element chunk starts at
+  // or past K copies the zero chunk instead (A row chunk (lane % LPR) ^ swz(r),
+  // r the row the instruction's lane covers; the bf16 B rows likewise)
+  const bool k_ragged = FMT == 0 && K % KE != 0;
+  auto tail_src = [&](const uint8_t* p, int blk, int kt) {
+    if (FMT == 0 && k_ragged && kt == nk - 1) {
+      const int r = blk * RPI + lane / LPR;
+      const int c = (lane % LPR) ^ swz<KB>(r);
+      if (kt * KE + 8 * c >= K) return static_cast<const uint8_t*>(kZeroChunk);
+    }
+    return p;
+  };
   auto issue_part = [&](const Src& src, int kt, int buf, int q0, int q1) {
     const uint32_t base = smem0 + buf * STAGE;
 #pragma unroll
     for (int i = 0; i < A_CH; ++i)
-      if (i >= q0 && i < q1) dma16(src.a[i] + kt * KB, base + (i * LW + lw) * 1024);
+      if (i >= q0 && i < q1) dma16(tail_src(src.a[i] + kt * KB, i * LW + lw, kt), base + (i * LW + lw) * 1024);
 #pragma unroll
     for (int i = 0; i < B_CH; ++i)
-      if (A_CH + i >= q0 && A_CH + i < q1) dma16(src.b[i] + kt * BB, base + A_BYTES + (i * LW + lw) * 1024);
+      if (A_CH + i >= q0 && A_CH + i < q1)
+        dma16(tail_src(src.b[i] + kt * BB, i * LW + lw, kt), base + A_BYTES + (i * LW + lw) * 1024);
     if (q1 < N_DMA) return;
 #pragma unroll
     for (int k = 0; k < SC; ++k) {
@@ -881,7 +904,7 @@ void moe_gemm_tiled(GroupedGemm g) {
             for (int v = 0; v < 16; ++v) {
               const int row = m0 + wm * WTM + i * 32 + 8 * (v >> 2) + 4 * kg + (v & 3);
               const int col = n0 + wn * (WTN / 2) + j * 32 + l32;
-              o[static_cast<size_t>(row) * g.I + col] = f32_to_bf16(av[i][j][v]);
+              if (col < g.I) o[static_cast<size_t>(row) * g.I + col] = f32_to_bf16(av[i][j][v]);
             }
       }
     } else if constexpr (FMT == 1) {
@@ -915,7 +938,8 @@ void moe_gemm_tiled(GroupedGemm g) {
           for (int v4 = 0; v4 < 4; ++v4) {
             const int col = n0 + wn * WTN + j * 32 + 8 * v4 + 4 * kg;
             const f32x16& c = acc[i][j];
-            *reinterpret_cast<f32x4*>(yr + col) = f32x4{c[4 * v4], c[4 * v4 + 1], c[4 * v4 + 2], c[4 * v4 + 3]};
+            if (col < g.H)  // four columns, all in or all out (H % 4 == 0)
+              *reinterpret_cast<f32x4*>(yr + col) = f32x4{c[4 * v4], c[4 * v4 + 1], c[4 * v4 + 2], c[4 * v4 + 3]};
           }
       }
     }
@@ -954,7 +978,7 @@ template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM, int KBT 
 hipError_t launch_tiled(const GroupedGemm& g, hipStream_t s) {
   constexpr int NC = GEMM1 ? BNW / 2 : BNW;
   constexpr int NT = (WM * WN + NP) * 64;
-  const long mt = g.max_rows / BM, nt = (GEMM1 ? g.I : g.H) / NC;
+  const long mt = g.max_rows / BM, nt = ((GEMM1 ? g.I : g.H) + NC - 1) / NC;
   auto kern = moe_gemm_tiled<FMT, GEMM1, BM, BNW, WM, WN, GM, KBT, STAGES, NP>;
   // workgroups per CU depend on the kernel's registers and LDS only: queried
   // once per instantiation (thread-safe static initialisation)

@@ -5,7 +5,11 @@
 // for the MoE Gate -> Fused MoE -> Weight Sum skeleton (Fig. 1, Fig. 3).
 // Every check runs before the first launch (quantised dispatch fails early on
 // an incompatible request, the guard rule of Sec. 6.2 / Table 3); nothing here
-// allocates, synchronises or keeps state.
+// allocates or synchronises.  The only state is the per-device address of the
+// static workspace moe_forward_static_ws runs in.
+#include <atomic>
+#include <mutex>
+
 #include "../../include/moe.h"
 #include "launch.hpp"
 
@@ -25,12 +29,21 @@ moe_status check_topk_shape(long T, int E, int top_k) {
   return MOE_OK;
 }
 
+// H and I: multiples of 8 for bf16 weights, of 128 for the quantised formats
+// (their scale blocks and groups are 128 wide along K, 128 rows for fp8),
+// at most 65536.
+moe_status check_hi(const moe_args* a) {
+  const int q = a->wfmt == MOE_W_BF16 ? 8 : 128;
+  if (a->H < q || a->I < q || a->H % q || a->I % q) return MOE_ERR_SHAPE;
+  if (a->H > (1 << 16) || a->I > (1 << 16)) return MOE_ERR_SHAPE;
+  return MOE_OK;
+}
+
 moe_status check_args(const moe_args* a) {
   if (!a) return MOE_ERR_NULL;
   moe_status st = check_topk_shape(a->T, a->E, a->top_k);
   if (st != MOE_OK) return st;
-  if (a->H < 128 || a->I < 128 || a->H % 128 || a->I % 128) return MOE_ERR_SHAPE;
-  if (a->H > (1 << 16) || a->I > (1 << 16)) return MOE_ERR_SHAPE;
+  if (check_hi(a) != MOE_OK) return MOE_ERR_SHAPE;
   if (a->score_mode != MOE_SCORE_SOFTMAX && a->score_mode != MOE_SCORE_SIGMOID) return MOE_ERR_UNSUPPORTED;
   if (a->renormalize != 0 && a->renormalize != 1) return MOE_ERR_UNSUPPORTED;
   if (a->wfmt != MOE_W_BF16 && a->wfmt != MOE_W_FP8E4M3_B128 && a->wfmt != MOE_W_INT4_G128 &&
@@ -40,6 +53,8 @@ moe_status check_args(const moe_args* a) {
   if (a->wfmt == MOE_W_FP8E4M3_B128_A16 && static_cast<long>(a->T) * a->top_k > 32L * a->E)
     return MOE_ERR_UNSUPPORTED;
   if (a->ofmt != MOE_OUT_F32 && a->ofmt != MOE_OUT_BF16) return MOE_ERR_UNSUPPORTED;
+  // the fused router GEMM steps through H 128 elements at a time
+  if (a->w_router && a->H % 128) return MOE_ERR_UNSUPPORTED;
   if (a->T == 0) return MOE_OK;
   if (!a->hidden || (!a->logits && !a->w_router) || !a->w1 || !a->w2 || !a->out) return MOE_ERR_NULL;
   if (a->wfmt != MOE_W_BF16 && (!a->w1_scale || !a->w2_scale)) return MOE_ERR_NULL;
@@ -58,7 +73,7 @@ moe_status check_args(const moe_args* a) {
 moe_ws_layout make_layout(const moe_args* a) {
   moe_ws_layout L;
   const long n = static_cast<long>(a->T) * a->top_k;
-  const int bm = moe::gemm_block_m(a->wfmt, a->T, a->top_k, a->E);
+  const int bm = moe::gemm_block_m(a->wfmt, a->T, a->top_k, a->E, a->H, a->I);
   const long cap = n + static_cast<long>(a->E) * (bm - 1);
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -192,7 +207,7 @@ moe_status moe_act_quant_fp8(const uint16_t* x, int M, int K, uint8_t* q, float*
 
 size_t moe_workspace_bytes(const moe_args* a) {
   if (!a || check_topk_shape(a->T, a->E, a->top_k) != MOE_OK) return 0;
-  if (a->H < 128 || a->I < 128 || a->H % 128 || a->I % 128) return 0;
+  if (check_hi(a) != MOE_OK) return 0;
   return static_cast<size_t>(make_layout(a).total);
 }
 
@@ -200,7 +215,7 @@ moe_status moe_workspace_layout(const moe_args* a, moe_ws_layout* layout) {
   if (!a || !layout) return MOE_ERR_NULL;
   moe_status st = check_topk_shape(a->T, a->E, a->top_k);
   if (st != MOE_OK) return st;
-  if (a->H < 128 || a->I < 128 || a->H % 128 || a->I % 128) return MOE_ERR_SHAPE;
+  if (check_hi(a) != MOE_OK) return MOE_ERR_SHAPE;
   *layout = make_layout(a);
   return MOE_OK;
 }
@@ -291,10 +306,52 @@ moe_status run_layer(const moe_args* a, void* ws, size_t ws_bytes, hipEvent_t* e
 
 }  // namespace
 
+// The library's own workspace for moe_forward_static_ws: one array per GPU,
+// created when the code object is loaded on that GPU and held until the
+// process ends.  In host code `scratch` names a host-side stand-in, never the
+// device memory: its device address is looked up once per device and only
+// that address is used.
+static __device__ __align__(256) uint8_t scratch[MOE_STATIC_WS_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// Device address of this device's `scratch` (nullptr on failure).
+void* scratch_on_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (p) return p;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+  if (!p) {
+    void* q = nullptr;
+    if (hipGetSymbolAddress(&q, HIP_SYMBOL(scratch)) != hipSuccess || !q) return nullptr;
+    p = q;
+    g_scratch_ptr[dev].store(p, std::memory_order_release);
+  }
+  return p;
+}
+
+}  // namespace
+
 extern "C" {
 
 moe_status moe_forward(const moe_args* a, void* ws, size_t ws_bytes, hipStream_t stream) {
   return run_layer(a, ws, ws_bytes, nullptr, stream);
+}
+
+moe_status moe_forward_static_ws(const moe_args* a, hipStream_t stream) {
+  moe_status st = check_args(a);
+  if (st != MOE_OK) return st;
+  if (a->T == 0) return MOE_OK;
+  if (static_cast<size_t>(make_layout(a).total) > MOE_STATIC_WS_BYTES) return MOE_ERR_WORKSPACE;
+  void* ws = scratch_on_current_device();
+  if (!ws) return MOE_ERR_HIP;
+  return run_layer(a, ws, MOE_STATIC_WS_BYTES, nullptr, stream);
 }
 
 moe_status moe_forward_profiled(const moe_args* a, void* ws, size_t ws_bytes,

@@ -53,8 +53,11 @@ def test_forward_argument_validation():
     assert _fwd(_args(top_k=0)) == 2
     assert _fwd(_args(E=0)) == 2
     assert _fwd(_args(E=2000, top_k=2)) == 2
-    assert _fwd(_args(H=200)) == 2
+    assert _fwd(_args(H=196)) == 2                      # bf16: H, I multiples of 8
     assert _fwd(_args(I=100)) == 2
+    assert _fwd(_args(H=200, wfmt="fp8")) == 2          # quantised formats: multiples of 128
+    assert _fwd(_args(I=200, wfmt="int4")) == 2
+    assert _fwd(_args(H=0)) == 2
     assert _fwd(_args(T=-1)) == 2
     assert _fwd(_args(hidden=None)) == 1
     assert _fwd(_args(out=None)) == 1
@@ -133,3 +136,37 @@ def test_workspace_layout_is_consistent():
         assert (L["act_q"] >= 0) == (wfmt == "fp8")
         if wfmt == "mxfp4":  # the decode kernels' 16-row tile, the tiled kernels' 128 above 32 rows per expert
             assert L["block_m"] == (16 if T * k <= 32 * E else 128)
+
+
+def test_static_workspace_entry_point_validation():
+    L = moe.lib()
+    st = lambda a: L.moe_forward_static_ws(ctypes.byref(a), None)  # noqa: E731
+    assert st(_args(top_k=9)) == B.MOE_ERR_SHAPE
+    assert st(_args(hidden=None)) == B.MOE_ERR_NULL
+    big = _args(T=4096, H=4096, E=64, I=1408, top_k=6)   # 599 MiB > the static workspace
+    assert moe.moe_workspace_bytes(big) > B.STATIC_WS_BYTES
+    assert st(big) == B.MOE_ERR_WORKSPACE
+    assert st(_args(T=0)) == B.MOE_OK
+
+
+def test_static_workspace_size_matches_header():
+    src = open(os.path.join(ROOT, "include", "moe.h")).read()
+    m = re.search(r"#define MOE_STATIC_WS_BYTES \((\d+)u << (\d+)\)", src)
+    assert m and int(m.group(1)) << int(m.group(2)) == B.STATIC_WS_BYTES
+
+
+def test_bf16_shapes_multiple_of_8_accepted():
+    # bf16 weights take any H, I that are multiples of 8 (the tiled kernels
+    # mask the ragged K step and column tile); the quantised formats keep 128
+    for H, I in ((392, 200), (4104, 1416), (8, 8)):
+        a = _args(H=H, I=I, T=4)
+        assert moe.moe_workspace_bytes(a) > 0
+        L = moe.moe_workspace_layout(a)
+        assert L["block_m"] == 128      # never the 16-row decode kernels
+        for wfmt in ("fp8", "int4", "fp8a16", "mxfp4"):
+            assert moe.moe_workspace_bytes(_args(H=H, I=I, T=4, wfmt=wfmt)) == 0
+    # a fused router needs H % 128 == 0
+    a = _args(H=392, I=200)
+    a.logits = None
+    a.w_router = FAKE
+    assert _fwd(a) == B.MOE_ERR_UNSUPPORTED

@@ -78,3 +78,13 @@ def test_token_order_permutes_output(dev):
     a, _, _, _ = run_forward(cfg, inp)
     b, _, _, _ = run_forward(cfg, dict(inp, hidden=inp["hidden"][perm], logits=inp["logits"][perm]))
     assert np.array_equal(b, a[perm])
+
+
+@pytest.mark.parametrize("H,I", [(392, 200), (4104, 1416), (8, 8), (136, 1032)])
+@pytest.mark.parametrize("T", [5, 300])
+def test_shapes_multiple_of_8(dev, H, I, T):
+    # bf16 H and I multiples of 8 but not of 128: every batch runs the tiled
+    # kernels with a ragged last K step (zero chunks past K) and a ragged last
+    # column tile (masked stores); T = 5 would take the decode kernels at
+    # 128-aligned shapes
+    _check(synth.tiny_config(1, T=T, H=H, I=I, E=6, top_k=2))
