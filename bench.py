@@ -46,7 +46,7 @@ sys.path.insert(0, ROOT)
 METRIC = "fused-MoE layer TFLOP/s (active FLOPs) + µs/layer; fraction of MFMA/HBM peak"
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0}
-W_BYTES = {"bf16": 2.0, "fp8": 1.0, "int4": 0.5, "fp8a16": 1.0, "mxfp4": 0.5}
+W_BYTES = {"bf16": 2.0, "fp8": 1.0, "int4": 0.5, "fp8a16": 1.0, "mxfp4": 0.5, "mxfp4x8": 0.5}
 DESCR = {
     1: "tiny MoE layer: T=64 H=256 E=8 I=128 top_k=2, bf16 weights, softmax top-2 renormalised",
     2: "decode-shaped MoE layer: T=16 H=4096 E=64 I=1408 top_k=6, bf16 weights, softmax top-6 renormalised",
@@ -61,6 +61,8 @@ DESCR = {
        "scales per 32, bf16 activations, sigmoid+bias top-8 x2.5",
     8: "MXFP4 prefill MoE layer: T=8192 H=7168 E=256 I=2048 top_k=8, OCP MX E2M1 weights with E8M0 "
        "scales per 32, bf16 activations, sigmoid+bias top-8 x2.5",
+    9: "MXFP4 x MXFP8 prefill MoE layer: T=8192 H=7168 E=256 I=2048 top_k=8, OCP MX E2M1 weights and "
+       "in-layer MXFP8 (e4m3, E8M0 per 32) activations, sigmoid+bias top-8 x2.5",
 }
 
 
@@ -319,13 +321,19 @@ def main():
     # GEMM1 per launch: W1 of every active expert (+ its scales), hidden read
     # once, the SwiGLU intermediate written once
     w1_scale_bytes = {"bf16": 0, "fp8": 2 * I * H / (128 * 128) * 4, "int4": 2 * I * H / 128 * 2,
-                      "fp8a16": 2 * I * H / (128 * 128) * 4, "mxfp4": 2 * I * H / 32}[cfg.wfmt]
-    act_bytes = {"bf16": 2, "fp8": 1, "int4": 2, "fp8a16": 2, "mxfp4": 2}[cfg.wfmt]
-    g1_bytes = n_active * (2 * I * H * wb + w1_scale_bytes) + T * H * (1 if cfg.wfmt == "fp8" else 2) + n * I * act_bytes
+                      "fp8a16": 2 * I * H / (128 * 128) * 4, "mxfp4": 2 * I * H / 32,
+                      "mxfp4x8": 2 * I * H / 32}[cfg.wfmt]
+    # bytes per element of the activation rows GEMM1 reads and of the
+    # intermediate it writes (with their scales)
+    act_bytes = {"bf16": 2, "fp8": 1 + 4 / 128, "int4": 2, "fp8a16": 2, "mxfp4": 2,
+                 "mxfp4x8": 1 + 1 / 32}[cfg.wfmt]
+    g1_bytes = n_active * (2 * I * H * wb + w1_scale_bytes) + T * H * act_bytes + n * I * act_bytes
     g1_flops = 2.0 * n * H * 2 * I
     g1_us = float(np.mean(g1_launch_us))
     # the roof that binds GEMM1: the larger of bytes / HBM peak and flops / MFMA peak
-    mfma_peak = PEAK_TFLOPS["fp8" if cfg.wfmt == "fp8" else "bf16"]
+    # the matrix rate the products run at: fp8 for e4m3 activations (the
+    # fp8 x fp4 instruction issues at the fp8 rate), bf16 otherwise
+    mfma_peak = PEAK_TFLOPS["fp8" if cfg.wfmt in ("fp8", "mxfp4x8") else "bf16"]
     t_hbm = g1_bytes / (PEAK_HBM_GBS * 1e9)
     t_mfma = g1_flops / (mfma_peak * 1e12)
     bound = "hbm" if t_hbm >= t_mfma else "mfma"
@@ -349,7 +357,8 @@ def main():
     if args.cpu_seconds > 0:
         base = cpu_baseline(cfg, inputs, args.cpu_seconds)
 
-    dtype = {"bf16": "bf16", "fp8": "fp8e4m3", "int4": "bf16", "fp8a16": "bf16", "mxfp4": "bf16"}[cfg.wfmt]
+    dtype = {"bf16": "bf16", "fp8": "fp8e4m3", "int4": "bf16", "fp8a16": "bf16", "mxfp4": "bf16",
+             "mxfp4x8": "mxfp8e4m3 x mxfp4e2m1"}[cfg.wfmt]
     rec = {
         "metric": METRIC,
         "value": flops / (ms * 1e-3) / 1e12,

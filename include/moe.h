@@ -103,7 +103,18 @@ typedef enum {
      SwiGLU intermediate is rounded to bf16.  Any batch: up to 32 routed rows
      per expert on average the 16-row decode kernels run, above that the
      tiled ones (segments padded to 128 rows). */
-  MOE_W_MXFP4_A16 = 4
+  MOE_W_MXFP4_A16 = 4,
+  /* MXFP4 weights with MXFP8 activations (OCP Microscaling v1.0 on both
+     sides of each product): the MOE_W_MXFP4_A16 weight storage and scales;
+     the hidden rows are quantised in-layer per (row, 32 columns) to e4m3
+     elements with a shared E8M0 scale X = 2^(floor(log2 amax) - 8) (8: the
+     exponent of e4m3's largest power of two; the E8M0 byte is clamped to
+     [0, 254], an all-zero block takes 2^-127), elements RNE(x / X) saturated
+     to +-448; the SwiGLU intermediate (fp32) is quantised the same way per
+     (row, 32 of I).  Both products run on the block-scaled matrix
+     instruction, which applies the E8M0 scales itself.  Any batch size
+     (segments padded to 128 rows). */
+  MOE_W_MXFP4_MXFP8 = 5
 } moe_wfmt;
 
 typedef enum { MOE_OUT_F32 = 0, MOE_OUT_BF16 = 1 } moe_ofmt;
@@ -217,12 +228,15 @@ typedef struct moe_ws_layout {
   int64_t topk_ids, topk_w;          /* int32 / fp32 [T*top_k]                   */
   int64_t expert_offsets;            /* int32 [E+1]                              */
   int64_t sorted_ids, inv_pos;       /* int32 [cap], int32 [T*top_k]             */
-  int64_t act_q, act_s;              /* fp8: uint8 [T,H], fp32 [T,H/128]; int4:
-                                        act_s = fp32 [T,H/128] group sums of the
-                                        hidden rows (times -136)              */
-  int64_t inter, inter_s;            /* bf16 [cap,I] (fp8: uint8 [cap,I], fp32 [cap,I/128]) */
+  int64_t act_q, act_s;              /* fp8: uint8 [T,H], fp32 [T,H/128]; MXFP8:
+                                        uint8 [T,H] e4m3, uint8 [T,H/32] E8M0;
+                                        int4: act_s = fp32 [T,H/128] group sums
+                                        of the hidden rows (times -136)       */
+  int64_t inter, inter_s;            /* bf16 [cap,I] (fp8: uint8 [cap,I], fp32 [cap,I/128];
+                                        MXFP8: uint8 [cap,I], uint8 [cap,I/32] E8M0) */
   int64_t y;                         /* [cap,H] rows in sorted order: bf16 for
-                                        MOE_W_FP8E4M3_B128, fp32 otherwise; pad rows unspecified */
+                                        MOE_W_FP8E4M3_B128 and MOE_W_MXFP4_MXFP8,
+                                        fp32 otherwise; pad rows unspecified */
   int64_t permute_ws;                /* moe_permute scratch                      */
   int32_t block_m, cap;              /* padding granule and sorted_ids length   */
   int64_t total;                     /* == moe_workspace_bytes                  */

@@ -6,5 +6,5 @@ import this package; the HIP library and its binding never do.
 from .moe_oracle import (  # noqa: F401
     bf16_to_f64, f32_to_bf16_rne, e4m3_decode, e4m3_encode, int4_unpack,
     dequant_weight, gate, permute, permute_capacity, act_quant_fp8,
-    act_dequant_fp8, swiglu_expert, activation_operand, forward,
+    act_dequant_fp8, act_quant_mxfp8, act_dequant_mxfp8, swiglu_expert, activation_operand, forward,
 )

@@ -40,7 +40,13 @@ Quantisation points the kernels take are mirrored (``mirror=True``):
   * fp8: the hidden rows and the intermediate ``a`` are each quantised per
     (row, 128-column group): s = fp32(max(amax, 1e-10) / 448) with an IEEE
     fp32 divide, q = e4m3fn(RNE(fp32(x / s))) saturated to +-448, and the
-    product then uses q * s.
+    product then uses q * s;
+  * MXFP4 weights with MXFP8 activations ("mxfp4x8"): the MXFP4 weight
+    storage above, and the hidden rows and the intermediate ``a`` (rounded
+    to fp32) quantised per (row, 32-column block) by the OCP MX rule: shared
+    scale X = 2^(floor(log2 amax) - 8) kept as an E8M0 byte (8 is the
+    exponent of e4m3's largest power of two, 256), elements e4m3(RNE(x / X))
+    saturated to +-448; the products use q * X.
 With ``mirror=False`` the layer is evaluated on the unquantised operands.
 
 Every function here is pinned by the CPU tests (tests/test_oracle_*.py)
@@ -56,6 +62,8 @@ import numpy as np
 
 E4M3_MAX = 448.0
 QGROUP = 128  # quantisation group along K (activations, int4 weights, fp8 blocks)
+MX_BLOCK = 32  # OCP MX block: elements sharing one E8M0 scale
+E4M3_EMAX = 8  # exponent of the largest power of two an e4m3 element holds (256)
 
 
 # ============================================================ storage decoding
@@ -176,7 +184,7 @@ def dequant_weight(wfmt: str, w: np.ndarray, scale) -> np.ndarray:
         N, K = q.shape
         s = bf16_to_f64(scale)                              # [N, K/128]
         return (q.reshape(N, K // QGROUP, QGROUP) * s[:, :, None]).reshape(N, K)
-    if wfmt == "mxfp4":                                 # E2M1 x E8M0 per 32 along K
+    if wfmt in ("mxfp4", "mxfp4x8"):                    # E2M1 x E8M0 per 32 along K
         q = _E2M1_TABLE[mxfp4_unpack(w)]                    # [N, K]
         N, K = q.shape
         s = e8m0_value(scale)                               # [N, K/32]
@@ -266,10 +274,35 @@ def act_dequant_fp8(codes, scales):
     return (e4m3_decode(codes).reshape(M, K // QGROUP, QGROUP) * s[:, :, None]).reshape(M, K)
 
 
+def act_quant_mxfp8(x32: np.ndarray):
+    """Per (row, 32-column block) OCP MX quantisation of fp32 rows [M, K] to
+    e4m3 elements with a shared E8M0 scale: X = 2^(floor(log2 amax) - 8),
+    its byte 127 + log2 X clamped to [0, 254] (an all-zero block: byte 0);
+    q = e4m3(RNE(x / X)) saturated to +-448.  Returns codes uint8 [M, K] and
+    scale bytes uint8 [M, K/32]."""
+    x = np.ascontiguousarray(x32, dtype=np.float32).astype(np.float64)
+    M, K = x.shape
+    blk = x.reshape(M, K // MX_BLOCK, MX_BLOCK)
+    amax = np.abs(blk).max(axis=2)
+    _, ex = np.frexp(amax)                    # amax = f * 2^ex, f in [0.5, 1): floor(log2 amax) = ex - 1
+    e = np.where(amax > 0, ex - 1 - E4M3_EMAX, -127)
+    e = np.clip(e, -127, 127)
+    q = e4m3_encode(blk / np.ldexp(1.0, e)[:, :, None])   # exact scaling, then RNE + saturation
+    return q.reshape(M, K), (e + 127).astype(np.uint8)
+
+
+def act_dequant_mxfp8(codes, scale_bytes):
+    M, K = codes.shape
+    s = e8m0_value(scale_bytes)
+    return (e4m3_decode(codes).reshape(M, K // MX_BLOCK, MX_BLOCK) * s[:, :, None]).reshape(M, K)
+
+
 def _round_intermediate(a: np.ndarray, wfmt: str) -> np.ndarray:
     a32 = a.astype(np.float32)
     if wfmt == "fp8":
         return act_dequant_fp8(*act_quant_fp8(a32))
+    if wfmt == "mxfp4x8":
+        return act_dequant_mxfp8(*act_quant_mxfp8(a32))
     return bf16_to_f64(f32_to_bf16_rne(a32))
 
 
@@ -290,6 +323,8 @@ def activation_operand(hidden_bits, wfmt="bf16", mirror=True):
     x = bf16_to_f64(hidden_bits)
     if wfmt == "fp8" and mirror:
         return act_dequant_fp8(*act_quant_fp8(x.astype(np.float32)))
+    if wfmt == "mxfp4x8" and mirror:
+        return act_dequant_mxfp8(*act_quant_mxfp8(x.astype(np.float32)))
     return x
 
 

@@ -19,7 +19,7 @@ MOE_ERR_NULL, MOE_ERR_SHAPE, MOE_ERR_UNSUPPORTED, MOE_ERR_ALIGN, MOE_ERR_WORKSPA
 STATUS_NAMES = {0: "MOE_OK", 1: "MOE_ERR_NULL", 2: "MOE_ERR_SHAPE", 3: "MOE_ERR_UNSUPPORTED",
                 4: "MOE_ERR_ALIGN", 5: "MOE_ERR_WORKSPACE", 6: "MOE_ERR_HIP"}
 SCORE = {"softmax": 0, "sigmoid": 1}
-WFMT = {"bf16": 0, "fp8": 1, "int4": 2, "fp8a16": 3, "mxfp4": 4}
+WFMT = {"bf16": 0, "fp8": 1, "int4": 2, "fp8a16": 3, "mxfp4": 4, "mxfp4x8": 5}
 OFMT = {"f32": 0, "bf16": 1}
 
 EXPORTED = ("moe_status_str", "moe_permute_capacity", "moe_permute_workspace_bytes",
@@ -238,16 +238,17 @@ def moe_forward(hidden, logits, w1, w2, top_k, *, mode="softmax", renormalize=Tr
     bf16 [E,2I,H] / [E,H,I]; fp8 uint8 codes with fp32 block scales
     [E,2I/128,H/128] / [E,H/128,I/128]; int4 int32 [E,2I,H/8] / [E,H,I/8] with
     bf16 scales [E,2I,H/128] / [E,H,I/128]; "fp8a16" (weight-only fp8, a decode
-    route) takes the fp8 storage with bf16 activations; "mxfp4" (a decode route)
-    uint8 [E,2I,H/2] / [E,H,I/2] two E2M1 codes per byte with uint8 E8M0
-    scales [E,2I,H/32] / [E,H,I/32].  With w_router (bf16
+    route) takes the fp8 storage with bf16 activations; "mxfp4" uint8
+    [E,2I,H/2] / [E,H,I/2] two E2M1 codes per byte with uint8 E8M0 scales
+    [E,2I,H/32] / [E,H,I/32] (bf16 activations); "mxfp4x8" the same storage
+    with MXFP8 activations quantised in-layer.  With w_router (bf16
     [E,H]) the layer computes its own logits (pass logits=None); logits_out
     (fp32 [T,E]) then receives them."""
     _dev(hidden, logits, w1, w2, sel_bias, w1_scale, w2_scale, out, topk_ids_out, topk_w_out,
          w_router, logits_out)
     T, H = hidden.shape
     E = (w_router if w_router is not None else logits).shape[0 if w_router is not None else 1]
-    I = w2.shape[2] * {"int4": 8, "mxfp4": 2}.get(wfmt, 1)
+    I = w2.shape[2] * {"int4": 8, "mxfp4": 2, "mxfp4x8": 2}.get(wfmt, 1)
     if out is None:
         out = torch.empty((T, H), dtype=torch.float32 if out_dtype == "f32" else torch.bfloat16,
                           device=hidden.device)

@@ -141,6 +141,50 @@ hipError_t launch_act_quant(const uint16_t* x, int M, int K, uint8_t* q, float* 
   return hipGetLastError();
 }
 
+// Per (row, 32-column block), the OCP MX rule for e4m3 elements: the shared
+// scale X = 2^(floor(log2 amax) - 8) is kept as its E8M0 byte, which is the
+// fp32 exponent field of amax minus 8, floored at 0 (an all-zero or tiny block
+// takes 2^-127); elements e4m3(RNE(x / X)) saturated to +-448, where x / X is
+// the exact product x * 2^(127 - byte).  Four lanes own one block.
+__global__ __launch_bounds__(256) void act_quant_mx_kernel(
+    const uint16_t* __restrict__ x, int M, int K, uint8_t* __restrict__ q, uint8_t* __restrict__ sx) {
+  const long idx = static_cast<long>(blockIdx.x) * 256 + threadIdx.x;  // one per 8 columns
+  const long total = static_cast<long>(M) * (K / 8);
+  const bool live = idx < total;  // uniform over each block's four lanes (K % 32 == 0)
+  uint4 v = make_uint4(0, 0, 0, 0);
+  if (live) v = *reinterpret_cast<const uint4*>(x + idx * 8);
+  const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+  float f[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __uint_as_float(u[i] << 16);
+    f[2 * i + 1] = __uint_as_float(u[i] & 0xFFFF0000u);
+  }
+  float amax = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(f[i]));
+  amax = fmaxf(amax, __shfl_xor(amax, 1));
+  amax = fmaxf(amax, __shfl_xor(amax, 2));
+  if (!live) return;
+  const uint32_t byte = mx_e8m0_of_amax(amax);
+  const float mul = __uint_as_float((254u - byte) << 23);  // 2^(127 - byte), a normal fp32
+  uint32_t lo = 0, hi = 0;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    lo |= f32x2_to_e4m3(sat_e4m3(f[2 * i] * mul), sat_e4m3(f[2 * i + 1] * mul)) << (16 * i);
+    hi |= f32x2_to_e4m3(sat_e4m3(f[4 + 2 * i] * mul), sat_e4m3(f[5 + 2 * i] * mul)) << (16 * i);
+  }
+  *reinterpret_cast<uint2*>(q + idx * 8) = make_uint2(lo, hi);
+  if ((threadIdx.x & 3) == 0) sx[idx / 4] = static_cast<uint8_t>(byte);
+}
+
+hipError_t launch_act_quant_mx(const uint16_t* x, int M, int K, uint8_t* q, uint8_t* sx, hipStream_t st) {
+  const long total = static_cast<long>(M) * (K / 8);
+  const dim3 grid(static_cast<unsigned>((total + 255) / 256)), block(256);
+  hipLaunchKernelGGL(act_quant_mx_kernel, grid, block, 0, st, x, M, K, q, sx);
+  return hipGetLastError();
+}
+
 // Per (row, 128-column group): -136 times the fp32 sum of the group's values,
 // the term the int4 GEMM1 takes off its biased codes (136 + q).  Sixteen
 // lanes own one group, as in the quantiser above.

@@ -9,6 +9,7 @@ namespace moe {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x2 __attribute__((ext_vector_type(2)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));  // native 16-byte vector (HIP's uint4 is a struct)
@@ -88,6 +89,30 @@ __device__ __forceinline__ u32x4 mxfp4x8_to_bf16(uint32_t w, float sc) {
   r.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 2));
   r.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 3));
   return r;
+}
+
+// E8M0 byte of the OCP MX scale X = 2^(floor(log2 amax) - 8) for e4m3
+// elements (8: the exponent of e4m3's largest power of two), from the fp32
+// exponent field of amax >= 0, floored at byte 0 (2^-127); amax = 0 and
+// subnormal amax give 0.
+__device__ __forceinline__ uint32_t mx_e8m0_of_amax(float amax) {
+  const int ef = static_cast<int>(__float_as_uint(amax) >> 23);
+  return static_cast<uint32_t>(ef > 8 ? ef - 8 : 0);
+}
+
+// D(32x32, fp32) += A(32x64, OCP MX E2M1) * B(64x32, OCP MX e4m3), both
+// with E8M0 block scales per 32 k applied by the instruction (layout measured
+// on gfx950 with an in-bounds probe on random data).  Lane l serves row /
+// column (l % 32); lane group g = l / 32 supplies the scale of K block g
+// (byte OS of sa / sb, biased by 127) for both operands.  A (E2M1, a.s0..s3;
+// a.s4..s7 unused): the lane's 32 nibbles are block g (element 2b in the low
+// nibble of byte b).  B (e4m3): the lane's bytes 0..15 are elements
+// [16 g, 16 g + 16) of block 0, bytes 16..31 the same elements of block 1.
+// D element v: row 8*(v/4) + 4*(l/32) + v%4, column l % 32.
+template <int OS>
+__device__ __forceinline__ f32x16 mfma32x32x64_f4f8(const i32x8& a, const i32x8& b, int sa, int sb,
+                                                     const f32x16& c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 4, 0, OS, sa, OS, sb);
 }
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }

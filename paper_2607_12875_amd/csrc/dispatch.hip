@@ -19,6 +19,8 @@ hipError_t launch_gemm2_w8a16(const GroupedGemm& g, hipStream_t s);
 int gemm_block_m_mxfp4();
 hipError_t launch_gemm1_mxfp4_tiled(const GroupedGemm& g, hipStream_t s);
 hipError_t launch_gemm2_mxfp4_tiled(const GroupedGemm& g, hipStream_t s);
+hipError_t launch_gemm1_mx8(const GroupedGemm& g, hipStream_t s);
+hipError_t launch_gemm2_mx8(const GroupedGemm& g, hipStream_t s);
 
 // MXFP4 takes the 16-row decode kernels up to 32 routed rows per expert on
 // average, the tiled kernels above (the row tile is the permute's padding)
@@ -30,6 +32,7 @@ int gemm_block_m(int wfmt, int T, int top_k, int E, int H, int I) {
     case 2: return gemm_block_m_int4(T, top_k, E);
     case 3: return 16;  // the weight-only fp8 route runs the 16-row decode kernels only
     case 4: return mxfp4_decode(T, top_k, E) ? 16 : gemm_block_m_mxfp4();
+    case 5: return 128;  // MXFP4 x MXFP8: the tiled kernels at every batch size
     default: return gemm_block_m_bf16(T, top_k, E, H, I);
   }
 }
@@ -40,6 +43,7 @@ hipError_t launch_gemm1(int wfmt, const GroupedGemm& g, hipStream_t s) {
     case 2: return launch_gemm1_int4(g, s);
     case 3: return launch_gemm1_w8a16(g, s);
     case 4: return mxfp4_decode(g.T, g.top_k, g.E) ? launch_gemm1_w4a16(g, s) : launch_gemm1_mxfp4_tiled(g, s);
+    case 5: return launch_gemm1_mx8(g, s);
     default: return launch_gemm1_bf16(g, s);
   }
 }
@@ -50,6 +54,7 @@ hipError_t launch_gemm2(int wfmt, const GroupedGemm& g, hipStream_t s) {
     case 2: return launch_gemm2_int4(g, s);
     case 3: return launch_gemm2_w8a16(g, s);
     case 4: return mxfp4_decode(g.T, g.top_k, g.E) ? launch_gemm2_w4a16(g, s) : launch_gemm2_mxfp4_tiled(g, s);
+    case 5: return launch_gemm2_mx8(g, s);
     default: return launch_gemm2_bf16(g, s);
   }
 }

@@ -102,15 +102,18 @@ void moe_gemm_tiled(GroupedGemm g) {
   static_assert(NP == 0 || NW % NP == 0, "scale slots split evenly over the copy waves");
   static_assert(NP == 0 || WM * WN == 4, "split launches have one math wave per SIMD");
   constexpr bool F4B = FMT == 2 || FMT == 4;  // 4-bit weights (int4, MXFP4), bf16 activations
+  constexpr bool MX8 = FMT == 5;              // MXFP4 weights, MXFP8 activations
+  constexpr bool A8 = FMT == 1 || MX8;        // one-byte (e4m3) activations
+  constexpr bool B4 = F4B || MX8;             // 4-bit weight rows
   static_assert(KBT == 128 || (KBT == 64 && FMT == 0) || (KBT == 256 && F4B),
-                "64-byte steps are bf16 only, 256-byte steps 4-bit weights only");
+                "64-byte steps are bf16 only, 256-byte steps 4-bit weights with bf16 activations only");
   constexpr int KB = KBT;                                       // A bytes per row per step
-  constexpr int KE = FMT == 1 ? KB : KB / 2;                          // K elements per step
-  constexpr int BB = F4B ? KB / 4 : KB;                                // B bytes per row per step
+  constexpr int KE = A8 ? KB : KB / 2;                                 // K elements per step
+  constexpr int BB = B4 ? KE / 2 : KB;                                 // B bytes per row per step
   constexpr int LPB = BB / 16;                                         // lanes per 4-bit B row in a copy
   // bf16 and int4 GEMM2 form their product transposed, as fp8 does (16-byte
   // y stores, one pad check per row; bf16 prefill 4 % faster, GEMM1 was not)
-  constexpr bool TRB = FMT != 1 && !GEMM1;
+  constexpr bool TRB = !A8 && !GEMM1;
   constexpr int RPI = 1024 / KB, LPR = KB / 16;  // rows per DMA instruction, lanes per row
   constexpr int WTM = BM / WM, WTN = BNW / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -120,18 +123,23 @@ void moe_gemm_tiled(GroupedGemm g) {
   static_assert(A_CH >= 1 && B_CH >= 1 && A_CH * LW * 1024 == BM * KB && B_CH * LW * 1024 == BNW * BB, "");
   static_assert(!GEMM1 || TN % 2 == 0, "gate/up pairs");
   static_assert(FMT != 1 || !GEMM1 || NC == 128, "fp8 requant needs one 128-column group per tile");
+  static_assert(!MX8 || (NP > 0 && WM * WN == 4 && KB == 128), "MXFP8: four math waves beside copy waves");
   // per-stage scale block: NW slots of 256 bytes, one 4-byte DMA instruction
   // each (64 floats); fp8: slots [0, BM/64) the row scales of A, slot BM/64
   // the block scales of B; int4: slots [0, BNW/64) the bf16 pair holding each
   // B row's group scale, int4 GEMM1 also slots [BNW/64, BNW/64 + BM/64) the
   // rows' biased group sums (x_gsum).  Copy wave lw fills slots lw, lw + LW, ...
+  // MXFP8: slots [0, BM/64) the E8M0 dwords of the A rows (four 32-element
+  // blocks per step), then BNW/64 slots of the B rows' E8M0 dwords; slots
+  // past those load a harmless dummy.
   constexpr bool GSUM = FMT == 2 && GEMM1;
-  constexpr int SC = FMT == 0 ? 0 : (GSUM ? 2 : 1) * NW / LW;  // scale loads per copy wave per stage
+  constexpr int NSLOT = FMT == 0 ? 0 : (MX8 ? (BM + BNW) / 64 : (GSUM ? 2 : 1) * NW);
+  constexpr int SC = (NSLOT + LW - 1) / LW;  // scale loads per copy wave per stage
   static_assert(FMT != 1 || BM / 64 < NW, "fp8 scale DMA layout");
   static_assert(!F4B || (NW == 4 && BNW / 64 <= NW), "4-bit scale DMA layout");
   static_assert(!GSUM || (BNW / 64 + BM / 64 <= 2 * NW && STAGES == 2), "int4 group-sum DMA layout");
   static_assert(STAGES >= 2 && (STAGES - 2) * (A_CH + B_CH + SC) < 64, "vmcnt range");
-  constexpr int A_BYTES = BM * KB, B_BYTES = BNW * BB, S_BYTES = FMT == 0 ? 0 : (GSUM ? 2 : 1) * NW * 256;
+  constexpr int A_BYTES = BM * KB, B_BYTES = BNW * BB, S_BYTES = SC * LW * 256;
   constexpr int STAGE = A_BYTES + B_BYTES + S_BYTES;
   constexpr int N_DMA = A_CH + B_CH + SC;  // loads per copy wave per stage
 
@@ -213,7 +221,7 @@ void moe_gemm_tiled(GroupedGemm g) {
       for (int k = 0; k < NSL; ++k) {
         const int r = (lw + k * LW) * 64 + lane;
         int v = 0;
-        if (FMT == 1 && lw + k * LW < BM / 64) {
+        if (A8 && lw + k * LW < BM / 64) {
           if constexpr (NP > 0) v = staged ? lds_sid[lw][r] : g.sorted_ids[m0 + r];
           else v = g.sorted_ids[m0 + r];
         }
@@ -233,9 +241,9 @@ void moe_gemm_tiled(GroupedGemm g) {
       const int r = (i * LW + lw) * RPI + lane / LPR;
       const uint8_t* row;
       if (GEMM1) {
-        row = static_cast<const uint8_t*>(g.x) + token(sid[i]) * g.H * (FMT == 1 ? 1 : 2);
+        row = static_cast<const uint8_t*>(g.x) + token(sid[i]) * g.H * (A8 ? 1 : 2);
       } else {
-        row = static_cast<const uint8_t*>(g.inter) + static_cast<size_t>(m0 + r) * g.I * (FMT == 1 ? 1 : 2);
+        row = static_cast<const uint8_t*>(g.inter) + static_cast<size_t>(m0 + r) * g.I * (A8 ? 1 : 2);
       }
       src.a[i] = row + (((lane % LPR) ^ swz<KB>(r)) << 4);
     }
@@ -245,8 +253,8 @@ void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
     for (int i = 0; i < B_CH; ++i) {
       const int blk = i * LW + lw;
-      const int r = F4B ? blk * (64 / LPB) + lane / LPB : blk * RPI + lane / LPR;
-      const int sl = F4B ? (lane % LPB) ^ swz_b<BB>(r) : (lane % LPR) ^ swz<KB>(r);
+      const int r = B4 ? blk * (64 / LPB) + lane / LPB : blk * RPI + lane / LPR;
+      const int sl = B4 ? (lane % LPB) ^ swz_b<BB>(r) : (lane % LPR) ^ swz<KB>(r);
       // weight rows past N (a ragged last column tile) read the last row:
       // their columns are never stored
       int n;
@@ -294,6 +302,20 @@ void moe_gemm_tiled(GroupedGemm g) {
           src.s[k] = reinterpret_cast<const uint8_t*>(g.x_gsum + token(sid[A_CH + k]) * (g.H / 128));
           src.ss[k] = 4;
         }
+      } else if constexpr (MX8) {
+        if (sl < BM / 64) {
+          // A row (sl*64 + lane): its E8M0 bytes [K/32], the four of step kt one dword
+          const int r = sl * 64 + lane;
+          if (GEMM1) src.s[k] = g.x_mx + token(sid[A_CH + k]) * (g.H / 32);
+          else src.s[k] = g.inter_mx + static_cast<size_t>(m0 + r) * (g.I / 32);
+          src.ss[k] = 4;
+        } else if (sl < BM / 64 + BNW / 64) {
+          const int r = (sl - BM / 64) * 64 + lane;
+          const int n = GEMM1 ? (r < NC ? n0 + r : g.I + n0 + (r - NC)) : n0 + r;
+          src.s[k] = static_cast<const uint8_t*>(GEMM1 ? g.w1_scale : g.w2_scale) +
+                     (static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) + n) * (K / 32);
+          src.ss[k] = 4;
+        }
       } else if constexpr (FMT == 4) {
         if (sl < BNW / 64) {
           // E8M0 bytes [n][K/32]: the four of K step kt are one dword at byte 4 kt
@@ -338,7 +360,7 @@ void moe_gemm_tiled(GroupedGemm g) {
       // per-wave load counts need not match) skips its empty slots
       if (GSUM && src.ss[k] == 0) continue;
       const uint32_t dst = base + A_BYTES + B_BYTES + (lw + k * LW) * 256;
-      if constexpr (FMT == 1 || FMT == 4) {
+      if constexpr (FMT == 1 || FMT == 4 || MX8) {
         dma4(src.s[k] + kt * src.ss[k], dst);
       } else if constexpr (FMT == 2) {
         // B scale words (ss 1): element kt*KE/128 of the row, rounded down to
@@ -788,6 +810,51 @@ void moe_gemm_tiled(GroupedGemm g) {
               for (int j = 0; j < TN; ++j) acc[i][j] = TRB ? mfma32x32x16(b[j], a[i], acc[i][j]) : mfma32x32x16(a[i], b[j], acc[i][j]);
           }
         }
+      } else if constexpr (MX8) {
+        // MXFP4 weights x MXFP8 activations, formed transposed like fp8 (the
+        // weight fragment is the first operand).  MFMA kk of the step covers
+        // K [64 kk, 64 kk + 64) in two 32-element scale blocks, and lane
+        // group kg supplies block kg's E8M0 byte for both operands (byte
+        // 2 kk + kg of each row's step dword; the instruction applies the
+        // scales itself, so the products accumulate in place: no rescale on
+        // the VALU).  Weights: lane group kg holds block kg, 16 bytes (chunk
+        // 2 kk + kg of the 64-byte row).  Activations: the e4m3 operand
+        // interleaves the blocks in 16-element halves -- lane group kg holds
+        // elements [16 kg, +16) of block 0, then of block 1, i.e. chunks
+        // 4 kk + kg and 4 kk + 2 + kg of the 128-byte row.
+        i32x8 af[2][TM], bq[2][TN];
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+          for (int i = 0; i < TM; ++i) {
+            const int r = wm * WTM + i * 32 + l32;
+            const i32x4 lo = __builtin_bit_cast(i32x4, ld16(As + r * KB + (((4 * kk + kg) ^ swz<KB>(r)) << 4)));
+            const i32x4 hi = __builtin_bit_cast(i32x4, ld16(As + r * KB + (((4 * kk + 2 + kg) ^ swz<KB>(r)) << 4)));
+            af[kk][i] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          }
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            const int r = brow(j) + l32;
+            const i32x4 q = __builtin_bit_cast(i32x4, ld16(Bs + r * BB + (((2 * kk + kg) ^ swz_b<BB>(r)) << 4)));
+            bq[kk][j] = __builtin_shufflevector(q, q, 0, 1, 2, 3, 0, 1, 2, 3);  // upper half unused
+          }
+        }
+        const uint32_t* sA = reinterpret_cast<const uint32_t*>(Ss);                    // [BM]
+        const uint32_t* sB = reinterpret_cast<const uint32_t*>(Ss + (BM / 64) * 256);  // [BNW]
+        int da[TM], db[TN];  // the row's step dword moved down by kg bytes: byte 2 kk is block 2 kk + kg
+#pragma unroll
+        for (int i = 0; i < TM; ++i) da[i] = static_cast<int>(sA[wm * WTM + i * 32 + l32] >> (8 * kg));
+#pragma unroll
+        for (int j = 0; j < TN; ++j) db[j] = static_cast<int>(sB[brow(j) + l32] >> (8 * kg));
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x64_f4f8<0>(bq[0][j], af[0][i], db[j], da[i], acc[i][j]);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x64_f4f8<2>(bq[1][j], af[1][i], db[j], da[i], acc[i][j]);
       } else {  // MXFP4
         // lane group kg covers elements [64 kg, 64 kg + 64) of the step, the
         // 32-element blocks 2 kg and 2 kg + 1: their E8M0 bytes are bytes
@@ -894,6 +961,33 @@ void moe_gemm_tiled(GroupedGemm g) {
           if (wn == 0 && kg == 0) g.inter_scale[row * (g.I / 128) + n0 / 128] = sc;
         }
         __syncthreads();  // lds_amax is reused by the next tile
+      } else if constexpr (MX8) {
+        // transposed layout as fp8; the OCP MX block is one 32-column gate
+        // block j of the row: amax over the lane's 16 values and the other
+        // k-group lane's, then the E8M0 byte and the exact power-of-two scaling
+        uint8_t* q = static_cast<uint8_t*>(g.inter);
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const size_t row = static_cast<size_t>(m0 + wm * WTM + i * 32 + l32);
+#pragma unroll
+          for (int j = 0; j < TH; ++j) {
+            float m = 0.f;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) m = fmaxf(m, fabsf(av[i][j][v]));
+            m = fmaxf(m, __shfl_xor(m, 32));
+            const uint32_t byte = mx_e8m0_of_amax(m);
+            const float mul = __uint_as_float((254u - byte) << 23);
+            const int cb = n0 + wn * (WTN / 2) + j * 32;  // the block's first column
+#pragma unroll
+            for (int v4 = 0; v4 < 4; ++v4) {
+              const float* a4 = &av[i][j][4 * v4];
+              const uint32_t codes = f32x2_to_e4m3(sat_e4m3(a4[0] * mul), sat_e4m3(a4[1] * mul)) |
+                                     (f32x2_to_e4m3(sat_e4m3(a4[2] * mul), sat_e4m3(a4[3] * mul)) << 16);
+              *reinterpret_cast<uint32_t*>(q + row * g.I + cb + 8 * v4 + 4 * kg) = codes;
+            }
+            if (kg == 0) g.inter_mx[row * (g.I / 32) + cb / 32] = static_cast<uint8_t>(byte);
+          }
+        }
       } else {
         uint16_t* o = static_cast<uint16_t*>(g.inter);
 #pragma unroll
@@ -907,7 +1001,7 @@ void moe_gemm_tiled(GroupedGemm g) {
               if (col < g.I) o[static_cast<size_t>(row) * g.I + col] = f32_to_bf16(av[i][j][v]);
             }
       }
-    } else if constexpr (FMT == 1) {
+    } else if constexpr (A8) {
       // transposed layout: four consecutive output columns per 8-byte store
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
@@ -1101,6 +1195,20 @@ hipError_t launch_gemm2_mxfp4_tiled(const GroupedGemm& g, hipStream_t s) {
     if (g.H % 256) return launch_tiled<4, false, 128, 128, 2, 2, MOE_TGM, 256, 3, 4>(g, s);
     return launch_tiled<4, false, 128, 256, 2, 2, MOE_TGM, 256, 3, 4>(g, s);
   }
+}
+// MXFP4 weights x MXFP8 activations: the fp8 tile (128 x 256, four math
+// waves beside four copy waves), 128-element K steps (128 bytes of each
+// activation row, 64 of each weight row, and one E8M0 dword per row of
+// either), four stages
+#ifndef MOE_TM8_STAGES
+#define MOE_TM8_STAGES 4
+#endif
+hipError_t launch_gemm1_mx8(const GroupedGemm& g, hipStream_t s) {
+  return launch_tiled<5, true, 128, 256, 2, 2, MOE_TGM, 128, MOE_TM8_STAGES, 4>(g, s);
+}
+hipError_t launch_gemm2_mx8(const GroupedGemm& g, hipStream_t s) {
+  if (g.H % 256) return launch_tiled<5, false, 128, 128, 2, 2, MOE_TGM, 128, MOE_TM8_STAGES, 4>(g, s);
+  return launch_tiled<5, false, 128, 256, 2, 2, MOE_TGM, 128, MOE_TM8_STAGES, 4>(g, s);
 }
 hipError_t launch_gemm2_int4(const GroupedGemm& g, hipStream_t s) {
   if (g.H % 256) return launch_tiled<2, false, MOE_TI4_BM, 128, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP2>(g, s);

@@ -28,6 +28,8 @@ hipError_t launch_combine(const void* y, bool y_f32, const float* w, const int32
                           int H, int k, bool out_bf16, void* out, hipStream_t s);
 
 hipError_t launch_act_quant(const uint16_t* x, int M, int K, uint8_t* q, float* s, hipStream_t st);
+// OCP MX e4m3 per (row, 32 columns): codes q [M,K] and E8M0 bytes sx [M,K/32]
+hipError_t launch_act_quant_mx(const uint16_t* x, int M, int K, uint8_t* q, uint8_t* sx, hipStream_t st);
 // out[m][g] = -136 * sum of x[m][128g, 128g + 128) in fp32 (int4 GEMM1's bias term)
 hipError_t launch_group_sum(const uint16_t* x, int M, int K, float* out, hipStream_t st);
 
@@ -36,8 +38,9 @@ hipError_t launch_group_sum(const uint16_t* x, int M, int K, float* out, hipStre
 // `offsets` is the permute's expert_offsets[E+1], `max_rows` the capacity.
 struct GroupedGemm {
   // first product: A rows are hidden[sorted_ids[p] / top_k] (pads read row 0)
-  const void* x;              // bf16 hidden [T,H] (fp8: e4m3 codes [T,H])
+  const void* x;              // bf16 hidden [T,H] (fp8, MXFP8: e4m3 codes [T,H])
   const float* x_scale;       // fp8 only: [T, H/128]
+  const uint8_t* x_mx;        // MXFP8 only: E8M0 bytes [T, H/32]
   const float* x_gsum;        // int4 only: [T, H/128], -136 * the sum of each 128-group of a hidden row
   const int32_t* sorted_ids;  // [cap]
   const int32_t* offsets;     // [E+1]
@@ -46,16 +49,17 @@ struct GroupedGemm {
   const void* w1_scale;
   const void* w2;             // [E, H, I]
   const void* w2_scale;
-  void* inter;                // [cap, I] bf16 (fp8: e4m3 codes)
+  void* inter;                // [cap, I] bf16 (fp8, MXFP8: e4m3 codes)
   float* inter_scale;         // fp8 only: [cap, I/128]
+  uint8_t* inter_mx;          // MXFP8 only: E8M0 bytes [cap, I/32]
   void* y;                    // [cap, H]: fp32 for bf16 weights, bf16 otherwise
 };
 
-// y is kept in fp32 for bf16 and int4 weights (a bf16 rounding of every
+// y is kept in fp32 for bf16-activation routes (a bf16 rounding of every
 // routed row would take most of the bf16 2e-2 output tolerance) and in bf16
-// for fp8, whose 1.9 GB fp32 round trip at 8192 tokens would cost more than
-// the whole error budget it buys back.
-__host__ __device__ constexpr bool y_is_f32(int wfmt) { return wfmt != 1; }
+// for the fp8-activation ones (fp8, MXFP4 x MXFP8), whose 1.9 GB fp32 round
+// trip at 8192 tokens would cost more than the error budget it buys back.
+__host__ __device__ constexpr bool y_is_f32(int wfmt) { return wfmt != 1 && wfmt != 5; }
 
 // Row tile (padding granule) the kernels for this format/shape use.
 int gemm_block_m(int wfmt, int T, int top_k, int E, int H, int I);

@@ -47,7 +47,7 @@ moe_status check_args(const moe_args* a) {
   if (a->score_mode != MOE_SCORE_SOFTMAX && a->score_mode != MOE_SCORE_SIGMOID) return MOE_ERR_UNSUPPORTED;
   if (a->renormalize != 0 && a->renormalize != 1) return MOE_ERR_UNSUPPORTED;
   if (a->wfmt != MOE_W_BF16 && a->wfmt != MOE_W_FP8E4M3_B128 && a->wfmt != MOE_W_INT4_G128 &&
-      a->wfmt != MOE_W_FP8E4M3_B128_A16 && a->wfmt != MOE_W_MXFP4_A16)
+      a->wfmt != MOE_W_FP8E4M3_B128_A16 && a->wfmt != MOE_W_MXFP4_A16 && a->wfmt != MOE_W_MXFP4_MXFP8)
     return MOE_ERR_UNSUPPORTED;
   // the weight-only fp8 route is a decode route (16-row kernels only)
   if (a->wfmt == MOE_W_FP8E4M3_B128_A16 && static_cast<long>(a->T) * a->top_k > 32L * a->E)
@@ -93,6 +93,11 @@ moe_ws_layout make_layout(const moe_args* a) {
     L.act_s = take(static_cast<size_t>(a->T) * (a->H / 128) * 4);
     L.inter = take(static_cast<size_t>(cap) * a->I);
     L.inter_s = take(static_cast<size_t>(cap) * (a->I / 128) * 4);
+  } else if (a->wfmt == MOE_W_MXFP4_MXFP8) {
+    L.act_q = take(static_cast<size_t>(a->T) * a->H);
+    L.act_s = take(static_cast<size_t>(a->T) * (a->H / 32));
+    L.inter = take(static_cast<size_t>(cap) * a->I);
+    L.inter_s = take(static_cast<size_t>(cap) * (a->I / 32));
   } else {
     L.act_q = -1;
     L.act_s = a->wfmt == MOE_W_INT4_G128 ? take(static_cast<size_t>(a->T) * (a->H / 128) * 4) : -1;
@@ -262,6 +267,7 @@ moe_status run_layer(const moe_args* a, void* ws, size_t ws_bytes, hipEvent_t* e
   moe::GroupedGemm g;
   g.x = a->hidden;
   g.x_scale = nullptr;
+  g.x_mx = nullptr;
   g.x_gsum = nullptr;
   if (!mark(2)) return MOE_ERR_HIP;
   if (a->wfmt == MOE_W_INT4_G128) {
@@ -275,6 +281,13 @@ moe_status run_layer(const moe_args* a, void* ws, size_t ws_bytes, hipEvent_t* e
     if (moe::launch_act_quant(a->hidden, a->T, a->H, q, s, stream) != hipSuccess) return MOE_ERR_HIP;
     g.x = q;
     g.x_scale = s;
+  }
+  if (a->wfmt == MOE_W_MXFP4_MXFP8) {
+    uint8_t* q = at<uint8_t>(ws, L.act_q);
+    uint8_t* sx = at<uint8_t>(ws, L.act_s);
+    if (moe::launch_act_quant_mx(a->hidden, a->T, a->H, q, sx, stream) != hipSuccess) return MOE_ERR_HIP;
+    g.x = q;
+    g.x_mx = sx;
   }
   g.sorted_ids = sorted;
   g.offsets = offs;
@@ -290,7 +303,8 @@ moe_status run_layer(const moe_args* a, void* ws, size_t ws_bytes, hipEvent_t* e
   g.w2 = a->w2;
   g.w2_scale = a->w2_scale;
   g.inter = at<void>(ws, L.inter);
-  g.inter_scale = L.inter_s >= 0 ? at<float>(ws, L.inter_s) : nullptr;
+  g.inter_scale = L.inter_s >= 0 && a->wfmt == MOE_W_FP8E4M3_B128 ? at<float>(ws, L.inter_s) : nullptr;
+  g.inter_mx = L.inter_s >= 0 && a->wfmt == MOE_W_MXFP4_MXFP8 ? at<uint8_t>(ws, L.inter_s) : nullptr;
   g.y = at<void>(ws, L.y);
   if (!mark(3)) return MOE_ERR_HIP;
   if (moe::launch_gemm1(a->wfmt, g, stream) != hipSuccess) return MOE_ERR_HIP;

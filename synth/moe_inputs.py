@@ -68,6 +68,7 @@ class MoeConfig:
     top_k: int
     wfmt: str = "bf16"          # "bf16" | "fp8" | "int4" | "fp8a16" (fp8 storage, bf16 activations)
                                 # | "mxfp4" (MX E2M1 + E8M0 per 32, bf16 activations)
+                                # | "mxfp4x8" (the mxfp4 storage, MXFP8 activations)
     mode: str = "softmax"       # "softmax" | "sigmoid"
     renormalize: bool = True
     routed_scale: float = 1.0
@@ -103,6 +104,10 @@ CONFIGS = {
     # workload 4's prefill batch on MXFP4 expert weights (bf16 activations)
     8: MoeConfig("mxfp4-prefill", T=8192, H=7168, E=256, I=2048, top_k=8, wfmt="mxfp4",
                  mode="sigmoid", routed_scale=2.5, sel_bias_std=0.1, seed=8),
+    # the same batch and weights (seed 8) with MXFP8 activations: both
+    # products on the block-scaled fp8 x fp4 matrix instruction
+    9: MoeConfig("mxfp4x8-prefill", T=8192, H=7168, E=256, I=2048, top_k=8, wfmt="mxfp4x8",
+                 mode="sigmoid", routed_scale=2.5, sel_bias_std=0.1, seed=8),
 }
 
 
@@ -116,7 +121,7 @@ def tiny_config(n: int, **overrides) -> MoeConfig:
     kernels still see several tiles and a ragged tail."""
     base = CONFIGS[n]
     small = dict(T=77, H=384, E=8, I=256, top_k=min(base.top_k, 3))
-    if base.wfmt in ("fp8", "fp8a16", "mxfp4"):
+    if base.wfmt in ("fp8", "fp8a16", "mxfp4", "mxfp4x8"):
         small.update(E=16, top_k=4)
     if base.wfmt == "int4":
         small.update(E=12, top_k=4)
@@ -251,7 +256,7 @@ def _weight_arrays(cfg: MoeConfig, N: int, K: int, n_exp: int):
         return np.empty((n_exp, N, K), np.uint8), np.empty((n_exp, N // 128, K // 128), np.float32)
     if cfg.wfmt == "int4":
         return np.empty((n_exp, N, K // 8), np.int32), np.empty((n_exp, N, K // 128), np.uint16)
-    if cfg.wfmt == "mxfp4":
+    if cfg.wfmt in ("mxfp4", "mxfp4x8"):
         return np.empty((n_exp, N, K // 2), np.uint8), np.empty((n_exp, N, K // 32), np.uint8)
     raise ValueError(f"unknown weight format {cfg.wfmt!r}")
 
@@ -272,7 +277,7 @@ def make_expert_weights(cfg: MoeConfig, experts=None, threads=None, identical_ex
             dst[slot] = _bf16_bits(w)
         elif cfg.wfmt in ("fp8", "fp8a16"):
             dst[slot], dst_s[slot] = _fp8_block_quant(w)
-        elif cfg.wfmt == "mxfp4":
+        elif cfg.wfmt in ("mxfp4", "mxfp4x8"):
             dst[slot], dst_s[slot] = _mxfp4_quant(w)
         else:
             dst[slot], dst_s[slot] = _int4_group_quant(w)

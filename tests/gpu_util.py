@@ -6,7 +6,12 @@ import torch
 import paper_2607_12875_amd as moe
 import synth
 
-TOL = {"bf16": 2e-2, "fp8": 6e-2, "int4": 8e-2, "fp8a16": 2e-2, "mxfp4": 2e-2}   # max|err| <= TOL * rms(oracle out)
+# MXFP4 x MXFP8: the fp8 budget times 448/256.  Its error is the fp8
+# route's (requantisation ties the hardware's accumulation tips over, plus
+# bf16 y), but a power-of-two block scale can leave the block maximum as low
+# as 256 X, where one e4m3 step is 32/256 of it, against 32/448 when the
+# maximum maps to 448.
+TOL = {"bf16": 2e-2, "fp8": 6e-2, "int4": 8e-2, "fp8a16": 2e-2, "mxfp4": 2e-2, "mxfp4x8": 1.05e-1}   # max|err| <= TOL * rms(oracle out)
 
 
 def require_gpu():
@@ -59,6 +64,12 @@ def check_forward(cfg, inp=None, out_dtype="f32"):
         s = ws_view(ws, L, "act_s", torch.float32, cfg.T * cfg.H // 128).reshape(cfg.T, cfg.H // 128)
         rq, rsc = O.act_quant_fp8(O.bf16_to_f64(inp["hidden"]).astype(np.float32))
         assert np.array_equal(s, rsc)
+        assert np.array_equal(q, rq)
+    if cfg.wfmt == "mxfp4x8":   # the layer's own MXFP8 quantisation of the hidden rows, every row
+        q = ws_view(ws, L, "act_q", torch.uint8, cfg.T * cfg.H).reshape(cfg.T, cfg.H)
+        s = ws_view(ws, L, "act_s", torch.uint8, cfg.T * cfg.H // 32).reshape(cfg.T, cfg.H // 32)
+        rq, rsx = O.act_quant_mxfp8(O.bf16_to_f64(inp["hidden"]).astype(np.float32))
+        assert np.array_equal(s, rsx)
         assert np.array_equal(q, rq)
     err = rel_err(out, ref["out"])
     print(f"  max|err|/rms = {err:.3e} over {out.size} outputs (block_m={L['block_m']})", flush=True)

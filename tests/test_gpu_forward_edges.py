@@ -20,10 +20,10 @@ def dev():
 # fp8 comparison needs I of the workload's order (its intermediate codes are
 # pinned there at small I).
 def _I(wcfg):
-    return 1024 if wcfg == 4 else 256
+    return 1024 if wcfg in (4, 9) else 256
 
 
-@pytest.mark.parametrize("wcfg", [1, 4, 5, 7])
+@pytest.mark.parametrize("wcfg", [1, 4, 5, 7, 9])
 @pytest.mark.parametrize("T", [3, 700])
 def test_single_expert_top1(dev, wcfg, T):
     # E = 1, k = 1: every token through the one expert with weight 1 (x2.5 in
@@ -31,7 +31,7 @@ def test_single_expert_top1(dev, wcfg, T):
     check_forward(synth.tiny_config(wcfg, T=T, E=1, top_k=1, I=_I(wcfg), logit_bias="none", sel_bias_std=0.0))
 
 
-@pytest.mark.parametrize("wcfg", [1, 4, 5, 7])
+@pytest.mark.parametrize("wcfg", [1, 4, 5, 7, 9])
 def test_skew_onto_one_expert(dev, wcfg):
     # a steep Zipf bias sends most rows to one expert: one segment spans more
     # row tiles than the scheduler groups together

@@ -160,7 +160,7 @@ def _scale_blocks(inp, wfmt, seed=1):
         d = rng.integers(-3, 4, size=inp[k].shape)
         if wfmt == "int4":      # bf16 bits
             out[k] = O.f32_to_bf16_rne((O.bf16_to_f64(inp[k]) * 2.0 ** d).astype(np.float32))
-        elif wfmt == "mxfp4":   # E8M0 exponent bytes
+        elif wfmt in ("mxfp4", "mxfp4x8"):   # E8M0 exponent bytes
             out[k] = (inp[k].astype(np.int64) + d).astype(np.uint8)
         else:                   # fp32
             out[k] = (inp[k] * 2.0 ** d).astype(np.float32)
@@ -288,3 +288,93 @@ def test_mxfp4_tiled_ragged_and_minimum_k(dev):
 
 def test_mxfp4_prefill_workload_full_size(dev):
     _check(synth.config(8))
+
+
+# ---- MXFP4 weights x MXFP8 activations (OCP MX on both operands): the
+# block-scaled fp8 x fp4 matrix instruction, tiled kernels at every batch
+def _mx8_layer(cfg, inp):
+    out, ws, L, _ = run_forward(cfg, inp)
+    return ws, L
+
+
+def test_mxfp8_act_quant_bit_exact_crafted(dev):
+    # the worked blocks of the oracle's pin (ties, saturation, zero block, an
+    # fp32-subnormal amax), fed as bf16 hidden rows through the layer's own
+    # quantiser: codes and E8M0 bytes bit-exact
+    cfg = synth.tiny_config(9, T=4, H=128, I=128, E=4, top_k=2)
+    inp = synth.make_inputs(cfg)
+    x = np.zeros((4, 128), np.float32)
+    x[0, :5] = [1.0, -0.5, 17 / 256, 2.0 ** -17, 2.0 ** -18]
+    x[0, 32:35] = [1.875, -1.75, 1.8125]
+    x[0, 96], x[0, 97] = 3.0 * 2 ** 20, -(2.0 ** 5)
+    x[1, 0] = 2.0 ** -130
+    x[2] = np.linspace(-3, 3, 128)
+    x[3] = np.random.default_rng(1).standard_normal(128) * 1e-3
+    inp["hidden"] = _bf16(x)
+    assert O.bf16_to_f64(inp["hidden"])[1, 0] == 2.0 ** -130
+    out, ws, L, _ = run_forward(cfg, inp)
+    q = ws_view(ws, L, "act_q", torch.uint8, cfg.T * cfg.H).reshape(cfg.T, cfg.H)
+    sx = ws_view(ws, L, "act_s", torch.uint8, cfg.T * cfg.H // 32).reshape(cfg.T, cfg.H // 32)
+    rq, rsx = O.act_quant_mxfp8(O.bf16_to_f64(inp["hidden"]).astype(np.float32))
+    assert np.array_equal(sx, rsx)
+    assert np.array_equal(q, rq)
+
+
+@pytest.mark.parametrize("T", [1, 33, 200, 700])
+def test_mxfp4x8_small(dev, T):
+    _check(synth.tiny_config(9, T=T, H=512, I=1024, E=16, top_k=4))
+
+
+def test_mxfp4x8_ragged_and_minimum_k(dev):
+    # H = I = 384: three K steps, H % 256 != 0 (128-wide GEMM2 tiles);
+    # H = I = 128: a single K step (I = 128 so the tolerance is looser in
+    # practice: one intermediate code step weighs more)
+    _check(synth.tiny_config(9, T=300, H=384, I=1152, E=8, top_k=3))
+    _check(synth.tiny_config(9, T=400, H=128, I=1024, E=4, top_k=2))
+
+
+def test_mxfp4x8_block_scales_vary(dev):
+    cfg = synth.tiny_config(9, T=100, H=512, I=1024, E=8, top_k=2)
+    _check(cfg, inp=_scale_blocks(synth.make_inputs(cfg), cfg.wfmt, seed=9))
+
+
+def test_mxfp4x8_intermediate_codes(dev):
+    """The MXFP8 intermediate GEMM1 writes (e4m3 codes + E8M0 bytes per (row,
+    32 of I)) against the oracle's quantiser on its own fp32 intermediate.
+    The kernel's intermediate differs from the oracle's by ~1e-5 relative
+    (fp32 accumulation order), so: every E8M0 byte equal, except where the
+    block's amax lies within 2e-4 of a power of two (then one step either
+    way); where the bytes agree, every code the rounding of a value within
+    2e-4 * 448 (in scale units) of the oracle's a / X."""
+    cfg = synth.tiny_config(9, T=700, H=512, I=512, E=16, top_k=4)
+    inp = synth.make_inputs(cfg)
+    out, ws, L, _ = run_forward(cfg, inp)
+    n, I, cap = cfg.T * cfg.top_k, cfg.I, L["cap"]
+    sid = ws_view(ws, L, "sorted_ids", torch.int32, cap)
+    codes = ws_view(ws, L, "inter", torch.uint8, cap * I).reshape(cap, I)
+    sbytes = ws_view(ws, L, "inter_s", torch.uint8, cap * (I // 32)).reshape(cap, I // 32)
+    rows = np.nonzero(sid < n)[0]
+    a32 = _oracle_preq_intermediate(cfg, inp)[sid[rows]]
+    qref, sref = O.act_quant_mxfp8(a32)
+    sg = sbytes[rows]
+    amax = np.abs(a32.astype(np.float64)).reshape(-1, I // 32, 32).max(axis=2)
+    frac = amax / np.exp2(np.floor(np.log2(np.maximum(amax, 1e-300))))   # in [1, 2)
+    near = (frac < 1 + 2e-4) | (frac > 2 - 4e-4)
+    assert np.all((sg == sref) | (near & (np.abs(sg.astype(int) - sref.astype(int)) == 1)))
+    same = np.repeat(sg == sref, 32, axis=1)
+    X = np.repeat(O.e8m0_value(sref), 32, axis=1)
+    x = a32.astype(np.float64) / X
+    slack = 2e-4 * O.E4M3_MAX
+    v_lo = O.e4m3_decode(O.e4m3_encode(x - slack))
+    v_hi = O.e4m3_decode(O.e4m3_encode(x + slack))
+    v_g = O.e4m3_decode(codes[rows])
+    ok = ~same | ((v_g >= v_lo) & (v_g <= v_hi))
+    bad = np.argwhere(~ok)
+    assert bad.size == 0, (bad[:3], x[tuple(bad[0])], v_g[tuple(bad[0])])
+    ties = int((codes[rows] != qref).sum())
+    print(f"  {ties} of {qref.size} codes and {int((sg != sref).sum())} scale bytes differ by a tie", flush=True)
+    assert ties <= 0.01 * qref.size
+
+
+def test_mxfp4x8_prefill_workload_full_size(dev):
+    _check(synth.config(9))

@@ -207,3 +207,76 @@ def test_mxfp4_storage_encoder_roundtrip():
     packed, scale = M._mxfp4_quant(w)
     assert np.array_equal(scale, (ex + 127).astype(np.uint8))
     assert np.array_equal(O.dequant_weight("mxfp4", packed, scale), w.astype(np.float64))
+
+
+# ---------------------------------------------------------------- MXFP8 activations (OCP MX)
+def test_mxfp8_quant_worked_blocks():
+    # OCP MX v1.0 conversion: X = 2^(floor(log2 amax) - emax), emax = 8 for
+    # e4m3 (its largest power of two is 2^8), elements e4m3(x / X), saturated
+    x = np.zeros((2, 128), np.float32)
+    # block (0,0): amax 1 -> X = 2^-8 (byte 119); 17/256 -> 17 is a tie
+    # between 16 and 18 -> even mantissa 16; 2^-17 -> 2^-9 (smallest
+    # subnormal); 2^-18 -> 2^-10, a tie between 0 and 2^-9 -> 0
+    x[0, :5] = [1.0, -0.5, 17 / 256, 2.0 ** -17, 2.0 ** -18]
+    # block (0,1): amax 1.875 -> X = 2^-8; 480 saturates to 448; 464 is a tie
+    # between 448 and 480 -> 448 (even mantissa)
+    x[0, 32:35] = [1.875, -1.75, 1.8125]
+    # block (0,2): all zero -> byte 0, codes 0
+    # block (0,3): amax 3 * 2^20 -> X = 2^13 (byte 140): 384 -> 0x7C; -2^5 -> -2^-8
+    x[0, 96], x[0, 97] = 3.0 * 2 ** 20, -(2.0 ** 5)
+    # block (1,0): amax 2^-130 (an fp32 subnormal): the exponent clamps at
+    # 2^-127 (byte 0) and x / X = 2^-3 is still exact
+    x[1, 0] = 2.0 ** -130
+    q, s = O.act_quant_mxfp8(x)
+    assert s.dtype == np.uint8 and s.shape == (2, 4)
+    assert s[0].tolist() == [119, 119, 0, 140] and s[1, 0] == 0
+    assert q[0, :5].tolist() == [0x78, 0xF0, 0x58, 0x01, 0x00]
+    assert q[0, 32:35].tolist() == [0x7E, 0xFE, 0x7E]
+    assert np.all(q[0, 64:96] == 0)
+    assert q[0, 96] == 0x7C and q[0, 97] == 0x82
+    assert q[1, 0] == 0x20
+    d = O.act_dequant_mxfp8(q, s)
+    assert d[0, 0] == 1.0 and d[0, 32] == 1.75 and d[0, 96] == 3.0 * 2 ** 20 and d[1, 0] == 2.0 ** -130
+
+
+def test_mxfp8_quant_sweep_vs_torch():
+    # rows of mixed magnitudes: the scale byte is the one power of two with
+    # amax / X in [256, 512) (checked from the byte alone), and every element
+    # is torch's float8_e4m3fn cast of x / X clamped to +-448; decode through
+    # torch's E8M0 and e4m3 casts
+    rng = np.random.default_rng(5)
+    x = (rng.standard_normal((64, 1024)) * np.exp2(rng.integers(-30, 30, (64, 1)))).astype(np.float32)
+    x[3, 64:96] = 0.0
+    x[5, :32] *= 1e-30
+    q, s = O.act_quant_mxfp8(x)
+    X = torch.from_numpy(s.copy()).view(torch.float8_e8m0fnu).to(torch.float64).numpy()
+    amax = np.abs(x.astype(np.float64)).reshape(64, 32, 32).max(axis=2)
+    nz = amax > 0
+    assert np.all((amax[nz] / X[nz] >= 256) & (amax[nz] / X[nz] < 512))
+    assert np.all(s[~nz] == 0)
+    y = x.astype(np.float64).reshape(64, 32, 32) / X[:, :, None]
+    want = torch.from_numpy(np.clip(y, -448, 448).reshape(64, 1024)).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    assert np.array_equal(q, want)
+    d = O.act_dequant_mxfp8(q, s)
+    dq = torch.from_numpy(q.copy()).view(torch.float8_e4m3fn).to(torch.float64).numpy() * np.repeat(X, 32, axis=1)
+    assert np.array_equal(d, dq)
+    # within half a step (1/16 relative for normal elements, 2^-10 X below),
+    # except where the rule's scale leaves |x| / X above 448: saturation
+    err = np.abs(d - x.astype(np.float64))
+    Xr = np.repeat(X, 32, axis=1)
+    sat = np.abs(x) - 448 * Xr
+    assert np.all(err <= np.maximum(np.maximum(np.abs(x) / 16, Xr * 2.0 ** -10), sat) + 1e-300)
+    assert np.any(sat > np.abs(x) / 16)    # the sweep does reach the saturated range
+
+
+def test_mxfp8_blocks_are_independent():
+    # one element changed in block j changes only block j's scale and codes
+    rng = np.random.default_rng(9)
+    x = rng.standard_normal((1, 256)).astype(np.float32)
+    q0, s0 = O.act_quant_mxfp8(x)
+    x2 = x.copy()
+    x2[0, 100] = 1000.0                    # block 3
+    q1, s1 = O.act_quant_mxfp8(x2)
+    assert np.array_equal(np.nonzero(s0[0] != s1[0])[0], [3])
+    changed = np.nonzero(q0[0] != q1[0])[0]
+    assert changed.size > 0 and np.all((changed >= 96) & (changed < 128))

@@ -1,6 +1,7 @@
 """Pins of the oracle's whole layer: a hand-worked example, the dense SwiGLU
 special case against torch, identical-expert and token-order invariants, and a
 per-token brute force over every expert on tiny shapes."""
+import dataclasses
 import math
 
 import numpy as np
@@ -114,7 +115,44 @@ def test_mxfp4_weights_single_expert(mirror):
     assert np.max(np.abs(r["out"] - ref)) <= tol * rms
 
 
-@pytest.mark.parametrize("n", [1, 4, 5, 6, 7])
+@pytest.mark.parametrize("mirror", [False, True])
+def test_mxfp4_weights_mxfp8_activations_single_expert(mirror):
+    # MXFP4 weights with MXFP8 activations: E = 1, k = 1 is a dense SwiGLU.
+    # Unmirrored it is exactly the MXFP4 layer with bf16 activations.
+    # Mirrored: the hidden rows and the fp32 intermediate each go through the
+    # (separately pinned) MXFP8 quantiser, their codes decoded here through
+    # torch's e4m3 and E8M0 casts, the weights through the OCP E2M1 table
+    cfg = synth.MoeConfig("dense48", T=33, H=256, E=1, I=128, top_k=1, wfmt="mxfp4x8", seed=14)
+    inp = synth.make_inputs(cfg)
+    r = O.forward(cfg, inp, mirror=mirror)
+    if not mirror:
+        r4 = O.forward(dataclasses.replace(cfg, wfmt="mxfp4"), inp, mirror=False)
+        assert np.array_equal(r["out"], r4["out"])
+        return
+    e2m1 = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0, -0.0, -0.5, -1.0, -1.5, -2.0, -3.0, -4.0, -6.0])
+
+    def deq_w(packed, s):
+        codes = np.stack([packed & 0xF, packed >> 4], axis=-1).reshape(packed.shape[0], -1)
+        sc = torch.from_numpy(np.ascontiguousarray(s)).view(torch.float8_e8m0fnu).to(torch.float64)
+        return torch.from_numpy(e2m1[codes]) * sc.repeat_interleave(32, 1)
+
+    def mx_round(v):
+        q, sb = O.act_quant_mxfp8(np.asarray(v, np.float32))
+        qv = torch.from_numpy(q).view(torch.float8_e4m3fn).to(torch.float64)
+        return qv * torch.from_numpy(sb).view(torch.float8_e8m0fnu).to(torch.float64).repeat_interleave(32, 1)
+
+    x = torch.from_numpy(inp["hidden"].view(np.int16)).view(torch.bfloat16).to(torch.float64)
+    w1, w2 = deq_w(inp["w1"][0], inp["w1_scale"][0]), deq_w(inp["w2"][0], inp["w2_scale"][0])
+    xq = mx_round(x.numpy().astype(np.float32))
+    a = torch.nn.functional.silu(xq @ w1[:cfg.I].T) * (xq @ w1[cfg.I:].T)
+    ref = (mx_round(a.numpy().astype(np.float32)) @ w2.T).numpy()
+    rms = np.sqrt((ref ** 2).mean())
+    # a tie of the intermediate's rounding may go the other way (one e4m3 step)
+    assert np.max(np.abs(r["out"] - ref)) <= 2 ** -4 * rms
+    assert np.mean(np.abs(r["out"] - ref)) <= 1e-10 * rms
+
+
+@pytest.mark.parametrize("n", [1, 4, 5, 6, 7, 9])
 def test_identical_experts_any_routing(n):
     cfg = synth.tiny_config(n)
     inp = synth.make_inputs(cfg, identical_experts=True)
@@ -125,7 +163,7 @@ def test_identical_experts_any_routing(n):
     assert np.max(np.abs(r["out"] - ref)) <= 1e-12 * np.sqrt((ref ** 2).mean())
 
 
-@pytest.mark.parametrize("n", [1, 4, 5, 6, 7])
+@pytest.mark.parametrize("n", [1, 4, 5, 6, 7, 9])
 def test_token_order_invariance(n):
     cfg = synth.tiny_config(n)
     inp = synth.make_inputs(cfg)
@@ -177,7 +215,7 @@ def _brute_layer(cfg, inp, mirror):
     return np.array(outs)
 
 
-@pytest.mark.parametrize("n", [1, 4, 5, 6, 7])
+@pytest.mark.parametrize("n", [1, 4, 5, 6, 7, 9])
 @pytest.mark.parametrize("mirror", [False, True])
 def test_brute_force_tiny(n, mirror):
     cfg = synth.tiny_config(n, T=9, H=256, I=128, E=6, top_k=3)
