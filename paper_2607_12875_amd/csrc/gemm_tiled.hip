@@ -146,8 +146,8 @@ void moe_gemm_tiled(GroupedGemm g) {
   __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES][STAGE];
   __shared__ float lds_amax[FMT == 1 && GEMM1 ? WN : 1][FMT == 1 && GEMM1 ? BM : 1];
   __shared__ int lds_off[MOE_MAX_EXPERTS_DEV + 1];  // expert_offsets, read once per workgroup
-  // GEMM1 copy waves: the next tile's row ids, one slot per copy wave
-  __shared__ int lds_sid[GEMM1 && NP > 0 ? NP : 1][GEMM1 && NP > 0 ? BM : 1];
+  // copy waves: the next tile's row ids, one slot per copy wave
+  __shared__ int lds_sid[NP > 0 ? NP : 1][NP > 0 ? BM : 1];
 
   const int tid = threadIdx.x, lane = lane_id(), wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -193,6 +193,7 @@ void moe_gemm_tiled(GroupedGemm g) {
   constexpr int NSL = SC > 0 ? SC : 1;
   struct Src {
     const uint8_t* a[A_CH];  // A rows
+    int am[A_CH];            // A step-advance mask: -1, or 0 for a pad row (its source is the zero chunk)
     const uint8_t* b[B_CH];  // B rows
     const uint8_t* s[NSL];   // scale words
     int ss[NSL];             // scale advance per step
@@ -207,16 +208,18 @@ void moe_gemm_tiled(GroupedGemm g) {
     // XOR swizzle the fragment reads undo.
     // GEMM1 gathers its A rows by token: every row id this lane needs (A rows,
     // fp8 row scales) is requested before the first is used, so the tile
-    // pays one memory round trip.  Pad rows (id n_routed) read the last
-    // token instead; their products are never read.
+    // pays one memory round trip.  A pad row (id n_routed) of either product
+    // copies the zero chunk at every step: one cache line per instruction
+    // rather than a row's eight, and zeros in LDS; its products are never
+    // read.  Scale sources of pad rows read the last token's.
     int sid[A_CH + NSL];
-    if constexpr (GEMM1) {
 #pragma unroll
-      for (int i = 0; i < A_CH; ++i) {
-        const int r = (i * LW + lw) * RPI + lane / LPR;
-        if constexpr (NP > 0) sid[i] = staged ? lds_sid[lw][r] : g.sorted_ids[m0 + r];
-        else sid[i] = g.sorted_ids[m0 + r];
-      }
+    for (int i = 0; i < A_CH; ++i) {
+      const int r = (i * LW + lw) * RPI + lane / LPR;
+      if constexpr (NP > 0) sid[i] = staged ? lds_sid[lw][r] : g.sorted_ids[m0 + r];
+      else sid[i] = g.sorted_ids[m0 + r];
+    }
+    if constexpr (GEMM1) {
 #pragma unroll
       for (int k = 0; k < NSL; ++k) {
         const int r = (lw + k * LW) * 64 + lane;
@@ -245,7 +248,9 @@ void moe_gemm_tiled(GroupedGemm g) {
       } else {
         row = static_cast<const uint8_t*>(g.inter) + static_cast<size_t>(m0 + r) * g.I * (A8 ? 1 : 2);
       }
-      src.a[i] = row + (((lane % LPR) ^ swz<KB>(r)) << 4);
+      const bool pad = sid[i] >= g.n_routed;
+      src.a[i] = pad ? static_cast<const uint8_t*>(kZeroChunk) : row + (((lane % LPR) ^ swz<KB>(r)) << 4);
+      src.am[i] = pad ? 0 : -1;
     }
     const size_t w_row_bytes = FMT == 0 ? K * 2 : (FMT == 1 ? K : K / 2);
     const uint8_t* wbase = static_cast<const uint8_t*>(GEMM1 ? g.w1 : g.w2) +
@@ -337,22 +342,28 @@ void moe_gemm_tiled(GroupedGemm g) {
   // r the row the instruction's lane covers; the bf16 B rows likewise)
   const bool k_ragged = FMT == 0 && K % KE != 0;
   auto tail_src = [&](const uint8_t* p, int blk, int kt) {
-    if (FMT == 0 && k_ragged && kt == nk - 1) {
-      const int r = blk * RPI + lane / LPR;
-      const int c = (lane % LPR) ^ swz<KB>(r);
-      if (kt * KE + 8 * c >= K) return static_cast<const uint8_t*>(kZeroChunk);
-    }
-    return p;
+    const int r = blk * RPI + lane / LPR;
+    const int c = (lane % LPR) ^ swz<KB>(r);
+    return kt * KE + 8 * c >= K ? static_cast<const uint8_t*>(kZeroChunk) : p;
   };
   auto issue_part = [&](const Src& src, int kt, int buf, int q0, int q1) {
     const uint32_t base = smem0 + buf * STAGE;
+    if (FMT == 0 && k_ragged && kt == nk - 1) {  // uniform: only the last step of a ragged K
 #pragma unroll
-    for (int i = 0; i < A_CH; ++i)
-      if (i >= q0 && i < q1) dma16(tail_src(src.a[i] + kt * KB, i * LW + lw, kt), base + (i * LW + lw) * 1024);
+      for (int i = 0; i < A_CH; ++i)
+        if (i >= q0 && i < q1) dma16(tail_src(src.a[i] + (kt * KB & src.am[i]), i * LW + lw, kt), base + (i * LW + lw) * 1024);
 #pragma unroll
-    for (int i = 0; i < B_CH; ++i)
-      if (A_CH + i >= q0 && A_CH + i < q1)
-        dma16(tail_src(src.b[i] + kt * BB, i * LW + lw, kt), base + A_BYTES + (i * LW + lw) * 1024);
+      for (int i = 0; i < B_CH; ++i)
+        if (A_CH + i >= q0 && A_CH + i < q1)
+          dma16(tail_src(src.b[i] + kt * BB, i * LW + lw, kt), base + A_BYTES + (i * LW + lw) * 1024);
+    } else {
+#pragma unroll
+      for (int i = 0; i < A_CH; ++i)
+        if (i >= q0 && i < q1) dma16(src.a[i] + (kt * KB & src.am[i]), base + (i * LW + lw) * 1024);
+#pragma unroll
+      for (int i = 0; i < B_CH; ++i)
+        if (A_CH + i >= q0 && A_CH + i < q1) dma16(src.b[i] + kt * BB, base + A_BYTES + (i * LW + lw) * 1024);
+    }
     if (q1 < N_DMA) return;
 #pragma unroll
     for (int k = 0; k < SC; ++k) {
@@ -408,7 +419,7 @@ void moe_gemm_tiled(GroupedGemm g) {
         for (int q = 0; q < STAGES - 1; ++q)
           if (q < nk) issue(cur, q, q);
       }
-      // the next tile's sources are computed in step kc; its row ids (GEMM1),
+      // the next tile's sources are computed in step kc; its row ids,
       // copied to this wave's LDS slot ahead of step STAGES-1's loads, have
       // landed by then: in-order completion, and the wait of step kt covers
       // every load issued before step kt+1 (all of them in the last step)
@@ -420,10 +431,8 @@ void moe_gemm_tiled(GroupedGemm g) {
         int en = 0, m0n = 0, n0n = 0;
         if (next) {
           coords(tn, en, m0n, n0n);
-          if constexpr (GEMM1) {
 #pragma unroll
-            for (int q = 0; q < BM / 64; ++q) dma4(g.sorted_ids + m0n + q * 64 + lane, lds_addr(&lds_sid[lw][q * 64]));
-          }
+          for (int q = 0; q < BM / 64; ++q) dma4(g.sorted_ids + m0n + q * 64 + lane, lds_addr(&lds_sid[lw][q * 64]));
         }
         for (int kt = 0; kt < nk; ++kt) {
           wait_ahead(min(STAGES - 2, nk - 1 - kt));
@@ -990,16 +999,20 @@ void moe_gemm_tiled(GroupedGemm g) {
         }
       } else {
         uint16_t* o = static_cast<uint16_t*>(g.inter);
+        auto store = [&](bool masked) {
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+          for (int i = 0; i < TM; ++i)
 #pragma unroll
-          for (int j = 0; j < TH; ++j)
+            for (int j = 0; j < TH; ++j)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-              const int row = m0 + wm * WTM + i * 32 + 8 * (v >> 2) + 4 * kg + (v & 3);
-              const int col = n0 + wn * (WTN / 2) + j * 32 + l32;
-              if (col < g.I) o[static_cast<size_t>(row) * g.I + col] = f32_to_bf16(av[i][j][v]);
-            }
+              for (int v = 0; v < 16; ++v) {
+                const int row = m0 + wm * WTM + i * 32 + 8 * (v >> 2) + 4 * kg + (v & 3);
+                const int col = n0 + wn * (WTN / 2) + j * 32 + l32;
+                if (!masked || col < g.I) o[static_cast<size_t>(row) * g.I + col] = f32_to_bf16(av[i][j][v]);
+              }
+        };
+        if (n0 + NC <= g.I) store(false);  // uniform: only a ragged last column tile masks
+        else store(true);
       }
     } else if constexpr (A8) {
       // transposed layout: four consecutive output columns per 8-byte store
@@ -1021,6 +1034,7 @@ void moe_gemm_tiled(GroupedGemm g) {
     } else {
       // transposed layout, fp32 y: four consecutive output columns per 16-byte store
       static_assert(TRB && y_is_f32(FMT), "bf16 and int4 routes keep y in fp32");
+      const bool masked = n0 + NC > g.H;  // uniform: only a ragged last column tile masks
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int row = m0 + wm * WTM + i * 32 + l32;
@@ -1032,7 +1046,7 @@ void moe_gemm_tiled(GroupedGemm g) {
           for (int v4 = 0; v4 < 4; ++v4) {
             const int col = n0 + wn * WTN + j * 32 + 8 * v4 + 4 * kg;
             const f32x16& c = acc[i][j];
-            if (col < g.H)  // four columns, all in or all out (H % 4 == 0)
+            if (!masked || col < g.H)  // four columns, all in or all out (H % 4 == 0)
               *reinterpret_cast<f32x4*>(yr + col) = f32x4{c[4 * v4], c[4 * v4 + 1], c[4 * v4 + 2], c[4 * v4 + 3]};
           }
       }
