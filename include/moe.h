@@ -141,23 +141,33 @@ moe_status moe_gate_topk(const float* logits, const float* sel_bias, int T, int 
                          float* topk_w, hipStream_t stream);
 
 /*
- * Router GEMM fused with the gate (the step in front of the MoE Gate node,
+ * Router GEMM in front of the gate (the step before the MoE Gate node,
  * Fig. 1): logits[t,e] = sum_h hidden[t,h] * w_router[e,h], bf16 products
  * accumulated in fp32, then exactly the selection and weights of
- * moe_gate_topk on those fp32 logits, in one kernel.
+ * moe_gate_topk on those fp32 logits.  Two launches: the logits GEMM in K
+ * slices over many workgroups (partial logits in ws), then one wavefront
+ * per token that sums the slices in slice order and selects (up to 64
+ * tokens); above 64 tokens one kernel per 16-token tile, and no scratch.
  *   hidden    device bf16 bits [T,H], 16-byte aligned; H % 128 == 0, H <= 65536
  *   w_router  device bf16 bits [E,H], 16-byte aligned
  *   logits    device fp32 [T,E] or NULL: receives the logits the selection used
+ *   ws        device scratch of >= moe_router_workspace_bytes(T, H, E) bytes,
+ *             16-byte aligned (contents on entry do not matter); may be NULL
+ *             when that size is 0
  *   other arguments and the outputs as moe_gate_topk.
- * The fp32 accumulation order is the kernel's own: logits agree with the
- * exact sums to within a few fp32 roundings of sum_h |hidden * w_router|.
+ * The fp32 accumulation order is the kernel's own and the same on every run:
+ * logits agree with the exact sums to within a few fp32 roundings of
+ * sum_h |hidden * w_router|.
  * Errors: MOE_ERR_NULL, MOE_ERR_SHAPE, MOE_ERR_UNSUPPORTED, MOE_ERR_ALIGN,
- * MOE_ERR_HIP.  T == 0 is a no-op.
+ * MOE_ERR_WORKSPACE, MOE_ERR_HIP.  T == 0 is a no-op.
  */
 moe_status moe_router_gate_topk(const uint16_t* hidden, const uint16_t* w_router, int T, int H, int E,
                                 int top_k, int mode, int renormalize, float routed_scale,
                                 const float* sel_bias, float* logits, int32_t* topk_ids, float* topk_w,
-                                hipStream_t stream);
+                                void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Scratch moe_router_gate_topk needs (bytes); 0 for invalid sizes.  Host-only, pure. */
+size_t moe_router_workspace_bytes(int T, int H, int E);
 
 /* Rows needed by moe_permute's sorted_ids: T*top_k + E*(block_m-1).  Host-only. */
 size_t moe_permute_capacity(int T, int top_k, int E, int block_m);
@@ -238,6 +248,7 @@ typedef struct moe_ws_layout {
                                         MOE_W_FP8E4M3_B128 and MOE_W_MXFP4_MXFP8,
                                         fp32 otherwise; pad rows unspecified */
   int64_t permute_ws;                /* moe_permute scratch                      */
+  int64_t router_ws;                 /* router partial logits (w_router set), else -1 */
   int32_t block_m, cap;              /* padding granule and sorted_ids length   */
   int64_t total;                     /* == moe_workspace_bytes                  */
 } moe_ws_layout;
@@ -257,8 +268,8 @@ moe_status moe_workspace_layout(const moe_args* a, moe_ws_layout* layout);
  * are unspecified.  T == 0 is a no-op.
  * MOE_W_FP8E4M3_B128_A16 additionally needs
  * T * top_k <= 32 * E.  With
- * w_router set the router GEMM and the gate run as one kernel (as
- * moe_router_gate_topk) and `logits` may be NULL.
+ * w_router set the router GEMM and the gate run as moe_router_gate_topk
+ * (its scratch inside the workspace) and `logits` may be NULL.
  * Errors: MOE_ERR_NULL, MOE_ERR_SHAPE, MOE_ERR_UNSUPPORTED, MOE_ERR_ALIGN,
  * MOE_ERR_WORKSPACE, MOE_ERR_HIP.
  */

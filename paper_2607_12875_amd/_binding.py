@@ -23,7 +23,7 @@ WFMT = {"bf16": 0, "fp8": 1, "int4": 2, "fp8a16": 3, "mxfp4": 4, "mxfp4x8": 5}
 OFMT = {"f32": 0, "bf16": 1}
 
 EXPORTED = ("moe_status_str", "moe_permute_capacity", "moe_permute_workspace_bytes",
-            "moe_gate_topk", "moe_router_gate_topk", "moe_permute", "moe_act_quant_fp8", "moe_workspace_bytes",
+            "moe_gate_topk", "moe_router_gate_topk", "moe_router_workspace_bytes", "moe_permute", "moe_act_quant_fp8", "moe_workspace_bytes",
             "moe_workspace_layout", "moe_forward", "moe_forward_profiled", "moe_forward_static_ws")
 STATIC_WS_BYTES = 256 << 20  # MOE_STATIC_WS_BYTES: the library's own per-GPU workspace
 NUM_STAGES = 6
@@ -53,7 +53,7 @@ class MoeArgs(ctypes.Structure):
 class MoeWsLayout(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int64) for n in (
         "topk_ids", "topk_w", "expert_offsets", "sorted_ids", "inv_pos", "act_q", "act_s",
-        "inter", "inter_s", "y", "permute_ws")] + [
+        "inter", "inter_s", "y", "permute_ws", "router_ws")] + [
         ("block_m", ctypes.c_int32), ("cap", ctypes.c_int32), ("total", ctypes.c_int64)]
 
 
@@ -78,7 +78,9 @@ def lib() -> ctypes.CDLL:
         L.moe_gate_topk.restype = i32
         L.moe_gate_topk.argtypes = [vp, vp, i32, i32, i32, i32, i32, f32, vp, vp, vp]
         L.moe_router_gate_topk.restype = i32
-        L.moe_router_gate_topk.argtypes = [vp, vp, i32, i32, i32, i32, i32, i32, f32, vp, vp, vp, vp, vp]
+        L.moe_router_gate_topk.argtypes = [vp, vp, i32, i32, i32, i32, i32, i32, f32, vp, vp, vp, vp, vp, sz, vp]
+        L.moe_router_workspace_bytes.restype = sz
+        L.moe_router_workspace_bytes.argtypes = [i32, i32, i32]
         L.moe_permute.restype = i32
         L.moe_permute.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, i32, vp, sz, vp]
         L.moe_act_quant_fp8.restype = i32
@@ -144,7 +146,7 @@ def moe_gate_topk(logits, top_k, mode="softmax", renormalize=True, routed_scale=
 
 def moe_router_gate_topk(hidden, w_router, top_k, mode="softmax", renormalize=True, routed_scale=1.0,
                          sel_bias=None, logits=None, topk_ids=None, topk_w=None, stream=None):
-    """Router GEMM (bf16 hidden [T,H] x w_router [E,H]^T, fp32) fused with the
+    """Router GEMM (bf16 hidden [T,H] x w_router [E,H]^T, fp32) then the
     gate: returns (topk_ids int32 [T,k], topk_w fp32 [T,k]); logits, if given
     (fp32 [T,E]), receives the logits the selection used."""
     _dev(hidden, w_router, sel_bias, logits)
@@ -154,9 +156,12 @@ def moe_router_gate_topk(hidden, w_router, top_k, mode="softmax", renormalize=Tr
         topk_ids = torch.empty((T, top_k), dtype=torch.int32, device=hidden.device)
     if topk_w is None:
         topk_w = torch.empty((T, top_k), dtype=torch.float32, device=hidden.device)
+    nws = lib().moe_router_workspace_bytes(T, H, E)
+    ws = torch.empty(max(nws, 16), dtype=torch.uint8, device=hidden.device)
     _check(lib().moe_router_gate_topk(_ptr(hidden), _ptr(w_router), T, H, E, top_k, SCORE[mode],
                                       int(renormalize), float(routed_scale), _ptr(sel_bias),
-                                      _ptr(logits), _ptr(topk_ids), _ptr(topk_w), _stream(stream)),
+                                      _ptr(logits), _ptr(topk_ids), _ptr(topk_w), _ptr(ws), ws.numel(),
+                                      _stream(stream)),
            "moe_router_gate_topk")
     return topk_ids, topk_w
 

@@ -11,11 +11,13 @@ hipError_t launch_gate_topk(const float* logits, const float* bias, int T, int E
                             int renorm, float scale, int32_t* ids, float* w, int32_t* ids2,
                             float* w2, hipStream_t s);
 
-// Router GEMM (bf16 hidden [T,H] x w_router [E,H]^T, fp32) fused with the gate
-// selection; logits_out (fp32 [T,E]) optional.  H % 128 == 0.
+// Router GEMM (bf16 hidden [T,H] x w_router [E,H]^T, fp32) then the gate
+// selection; logits_out (fp32 [T,E]) optional.  H % 128 == 0.  ws holds the
+// K-slice partial logits: router_workspace_bytes(T, H, E) bytes.
+size_t router_workspace_bytes(int T, int H, int E);
 hipError_t launch_router_gate(const uint16_t* hidden, const uint16_t* wr, int T, int H, int E, int k, int mode,
                               int renorm, float scale, const float* bias, float* logits_out, int32_t* ids,
-                              float* w, int32_t* ids2, float* w2, hipStream_t s);
+                              float* w, int32_t* ids2, float* w2, void* ws, hipStream_t s);
 
 int permute_chunk(int E);
 size_t permute_workspace_bytes(int T, int k, int E);

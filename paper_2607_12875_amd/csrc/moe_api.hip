@@ -53,7 +53,7 @@ moe_status check_args(const moe_args* a) {
   if (a->wfmt == MOE_W_FP8E4M3_B128_A16 && static_cast<long>(a->T) * a->top_k > 32L * a->E)
     return MOE_ERR_UNSUPPORTED;
   if (a->ofmt != MOE_OUT_F32 && a->ofmt != MOE_OUT_BF16) return MOE_ERR_UNSUPPORTED;
-  // the fused router GEMM steps through H 128 elements at a time
+  // the router GEMM steps through H in K slices of 128-element multiples
   if (a->w_router && a->H % 128) return MOE_ERR_UNSUPPORTED;
   if (a->T == 0) return MOE_OK;
   if (!a->hidden || (!a->logits && !a->w_router) || !a->w1 || !a->w2 || !a->out) return MOE_ERR_NULL;
@@ -106,6 +106,7 @@ moe_ws_layout make_layout(const moe_args* a) {
   }
   L.y = take(static_cast<size_t>(cap) * a->H * (moe::y_is_f32(a->wfmt) ? 4 : 2));
   L.permute_ws = take(moe::permute_workspace_bytes(a->T, a->top_k, a->E));
+  L.router_ws = a->w_router ? take(moe::router_workspace_bytes(a->T, a->H, a->E)) : -1;
   L.total = static_cast<int64_t>(off);
   return L;
 }
@@ -159,10 +160,15 @@ moe_status moe_gate_topk(const float* logits, const float* sel_bias, int T, int 
   return MOE_OK;
 }
 
+size_t moe_router_workspace_bytes(int T, int H, int E) {
+  if (T < 0 || E < 1 || E > MOE_MAX_EXPERTS || H < 128 || H % 128 || H > (1 << 16)) return 0;
+  return moe::router_workspace_bytes(T, H, E);
+}
+
 moe_status moe_router_gate_topk(const uint16_t* hidden, const uint16_t* w_router, int T, int H, int E,
                                 int top_k, int mode, int renormalize, float routed_scale,
                                 const float* sel_bias, float* logits, int32_t* topk_ids, float* topk_w,
-                                hipStream_t stream) {
+                                void* ws, size_t ws_bytes, hipStream_t stream) {
   moe_status st = check_topk_shape(T, E, top_k);
   if (st != MOE_OK) return st;
   if (H < 128 || H % 128 || H > (1 << 16)) return MOE_ERR_SHAPE;
@@ -170,11 +176,13 @@ moe_status moe_router_gate_topk(const uint16_t* hidden, const uint16_t* w_router
   if (renormalize != 0 && renormalize != 1) return MOE_ERR_UNSUPPORTED;
   if (T == 0) return MOE_OK;
   if (!hidden || !w_router || !topk_ids || !topk_w) return MOE_ERR_NULL;
-  if (!aligned16(hidden) || !aligned16(w_router)) return MOE_ERR_ALIGN;
+  const size_t need = moe::router_workspace_bytes(T, H, E);
+  if (need > 0 && (!ws || ws_bytes < need)) return MOE_ERR_WORKSPACE;
+  if (!aligned16(hidden) || !aligned16(w_router) || !aligned16(ws)) return MOE_ERR_ALIGN;
   if (!aligned4(logits) || !aligned4(sel_bias) || !aligned4(topk_ids) || !aligned4(topk_w))
     return MOE_ERR_ALIGN;
   if (moe::launch_router_gate(hidden, w_router, T, H, E, top_k, mode, renormalize, routed_scale, sel_bias,
-                              logits, topk_ids, topk_w, nullptr, nullptr, stream) != hipSuccess)
+                              logits, topk_ids, topk_w, nullptr, nullptr, ws, stream) != hipSuccess)
     return MOE_ERR_HIP;
   return MOE_OK;
 }
@@ -255,7 +263,7 @@ moe_status run_layer(const moe_args* a, void* ws, size_t ws_bytes, hipEvent_t* e
       a->w_router
           ? moe::launch_router_gate(a->hidden, a->w_router, a->T, a->H, a->E, a->top_k, a->score_mode,
                                     a->renormalize, a->routed_scale, a->sel_bias, a->logits_out, ids, wts,
-                                    a->topk_ids_out, a->topk_w_out, stream)
+                                    a->topk_ids_out, a->topk_w_out, at<void>(ws, L.router_ws), stream)
           : moe::launch_gate_topk(a->logits, a->sel_bias, a->T, a->E, a->top_k, a->score_mode, a->renormalize,
                                   a->routed_scale, ids, wts, a->topk_ids_out, a->topk_w_out, stream);
   if (gate_err != hipSuccess) return MOE_ERR_HIP;

@@ -1,17 +1,24 @@
-// Router GEMM fused with the MoE Gate (the step in front of the Gate node of
-// the paper's MoE skeleton, Fig. 1):
+// Router GEMM in front of the MoE Gate (the step before the Gate node of the
+// paper's MoE skeleton, Fig. 1):
 //   logits[t, e] = sum_h hidden[t, h] * w_router[e, h]     (bf16 in, fp32 accumulate)
-// followed, in the same kernel, by the gate's top-k selection and routing
-// weights on those fp32 logits (gate_select.hpp), so the [T, E] logits never
-// make a round trip through HBM and decode saves a launch.
+// followed by the gate's top-k selection and routing weights on those fp32
+// logits (gate_select.hpp).  Two forms, by batch size:
+//  * up to 64 tokens (decode), two launches: the logits GEMM spread over many
+//    workgroups in K slices (a workgroup that owned whole logits rows would
+//    read the whole router matrix and be bound by one CU's read rate: 40 us on
+//    a 16-token decode step), then one wave per token that sums the slices in
+//    slice order -- a fixed order, so the logits are the same on every run --
+//    and selects;
+//  * above, one kernel, one workgroup per 16-token tile (router_gate_kernel):
+//    there are enough tiles to occupy the CUs, and the [T, E] logits stay in
+//    LDS.
 //
-// One workgroup per 16-token tile, 4 * KS waves.  Wave w computes the
+// router_gate_kernel: 4 * KS waves.  Wave w computes the
 // 16-expert column tiles (w % 4) + 4 j (EPL of them: 64 * EPL >= E) over K
 // slice w / 4 with v_mfma_f32_16x16x32_bf16, the K loop software-pipelined U
 // steps ahead (splitting K over more waves shortens each wave's chain of
-// dependent loads, which bounds this kernel at small T); the slices' partial
-// logits are summed in slice order in LDS, then wave w selects for tokens
-// w, w + 4 KS, ...
+// dependent loads); the slices' partial logits are summed in slice order in
+// LDS, then wave w selects for tokens w, w + 4 KS, ...
 #include "gate_select.hpp"
 #include "launch.hpp"
 
@@ -136,27 +143,158 @@ __global__ __launch_bounds__(256 * KS) void router_gate_kernel(
   }
 }
 
+// router_partial_kernel: workgroup (token tile, 64-expert group, K slice);
+// wave w computes the 16 TT tokens x 16 experts tile of experts
+// 64 g + 16 w over K slice ks with v_mfma_f32_16x16x32_bf16 (fragments
+// loaded straight from HBM/L2 into registers; the four waves of a workgroup
+// share the token rows through L1) and stores the fp32 partial logits
+// P[ks][t][e].  Every K slice is a whole number of 32-element MFMA steps.
+template <int TT, int U>
+__global__ __launch_bounds__(256) void router_partial_kernel(const uint16_t* __restrict__ hidden,
+                                                             const uint16_t* __restrict__ wr, int T, int H, int E,
+                                                             int hs, float* __restrict__ part) {
+  const int lane = lane_id(), wv = threadIdx.x >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int t0 = blockIdx.x * 16 * TT, ks = blockIdx.z, h0 = ks * hs;
+  const int e = blockIdx.y * 64 + wv * 16 + r16;  // this lane's expert (B row)
+  const bool ev = e < E;
+  if (blockIdx.y * 64 + wv * 16 >= E) return;  // a wave with no expert of its own (uniform)
+  const uint16_t* arow[TT];
+#pragma unroll
+  for (int i = 0; i < TT; ++i) arow[i] = hidden + static_cast<size_t>(min(t0 + 16 * i + r16, T - 1)) * H + h0 + 8 * kg;
+  const uint16_t* brow = wr + static_cast<size_t>(ev ? e : 0) * H + h0 + 8 * kg;
+  f32x4 acc[TT];
+#pragma unroll
+  for (int i = 0; i < TT; ++i) acc[i] = f32x4{};
+  // U K steps per iteration, the next U steps' fragments loaded ahead
+  const int n = hs / 32;
+  u32x4 a[2][U][TT], b[2][U];
+  auto load = [&](int buf, int st) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int h = (st + u) * 32;
+      const bool in = st + u < n;
+#pragma unroll
+      for (int i = 0; i < TT; ++i) a[buf][u][i] = in ? ld16(arow[i] + h) : u32x4{};
+      b[buf][u] = in && ev ? ld16(brow + h) : u32x4{};
+    }
+  };
+  load(0, 0);
+  for (int st = 0, buf = 0; st < n; st += U, buf ^= 1) {
+    if (st + U < n) load(buf ^ 1, st + U);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int i = 0; i < TT; ++i) acc[i] = mfma16x16x32(as_bf16x8(a[buf][u][i]), as_bf16x8(b[buf][u]), acc[i]);
+  }
+  // D element v of a 16x16 tile: token 4*(lane/16) + v, expert lane%16 of the tile
+  if (!ev) return;
+#pragma unroll
+  for (int i = 0; i < TT; ++i)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int t = t0 + 16 * i + 4 * kg + v;
+      if (t < T) part[(static_cast<size_t>(ks) * T + t) * E + e] = acc[i][v];
+    }
+}
+
+// One wave per token: logits = the KS partials summed in slice order (fp32),
+// written out if asked, then the gate's selection and weights on them.
+template <int EPL>
+__global__ __launch_bounds__(256) void router_select_kernel(const float* __restrict__ part, int KS, int T, int E,
+                                                            int k, int mode, int renorm, float scale,
+                                                            const float* __restrict__ bias,
+                                                            float* __restrict__ logits_out, int32_t* __restrict__ ids,
+                                                            float* __restrict__ w, int32_t* __restrict__ ids2,
+                                                            float* __restrict__ w2) {
+  constexpr bool RANK = EPL <= MOE_GATE_RANK_MAX_EPL;
+  __shared__ float lg[4][EPL * 64];
+  __shared__ double skey[RANK ? 4 : 1][RANK ? EPL * 64 : 1];
+  __shared__ double sval[RANK ? 4 : 1][RANK ? EPL * 64 : 1];
+  __shared__ double ssel[RANK ? 4 : 1][RANK ? MOE_GATE_MAX_K : 1];
+  const int wv = threadIdx.x >> 6, lane = lane_id();
+  const int t = blockIdx.x * 4 + wv;
+  if (t >= T) return;  // uniform per wave
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const int e = lane + 64 * i;
+    if (e >= E) continue;
+    // the slices' partials are requested eight at a time, then added in slice order
+    float v = 0.f;
+    for (int q0 = 0; q0 < KS; q0 += 8) {
+      float x[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[j] = q0 + j < KS ? part[(static_cast<size_t>(q0 + j) * T + t) * E + e] : 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (q0 + j < KS) v += x[j];
+    }
+    lg[wv][e] = v;  // read back below by this same lane only
+    if (logits_out) logits_out[static_cast<size_t>(t) * E + e] = v;
+  }
+  const size_t o = static_cast<size_t>(t) * k;
+  if constexpr (RANK)
+    gate_rank_row<EPL>(lg[wv], bias, E, k, mode, renorm, scale, ids + o, w + o, ids2 ? ids2 + o : nullptr,
+                       w2 ? w2 + o : nullptr, skey[wv], sval[wv], ssel[wv]);
+  else
+    gate_argmax_row<EPL>(lg[wv], bias, E, k, mode, renorm, scale, ids + o, w + o, ids2 ? ids2 + o : nullptr,
+                         w2 ? w2 + o : nullptr);
+}
+
+namespace {
+constexpr int kRouterSplitMaxT = 64;  // the two-launch form up to this many tokens
+// K slices of the split router: enough workgroups to spread the router matrix
+// over the CUs, slices of at least 128 elements, at most 32 of them.
+int router_ks(int T, int H, int E) {
+  const long tiles = static_cast<long>((T + 15) / 16) * ((E + 63) / 64);
+  int ks = 1;
+  while (ks < 32 && tiles * ks < 256 && H % (64 * ks) == 0 && H / (2 * ks) >= 128) ks *= 2;
+  return ks;
+}
+}  // namespace
+
+size_t router_workspace_bytes(int T, int H, int E) {
+  if (T > kRouterSplitMaxT) return 0;
+  return static_cast<size_t>(router_ks(T, H, E)) * T * E * sizeof(float);
+}
+
 hipError_t launch_router_gate(const uint16_t* hidden, const uint16_t* wr, int T, int H, int E, int k, int mode,
                               int renorm, float scale, const float* bias, float* logits_out, int32_t* ids,
-                              float* w, int32_t* ids2, float* w2, hipStream_t s) {
+                              float* w, int32_t* ids2, float* w2, void* ws, hipStream_t s) {
   const int epl = (E + 63) / 64;
-  // KS slices of K per column-tile group (more waves in flight, shorter load
-  // chains), U K-steps of 32 loaded ahead per stage; the partial logits of
-  // all slices fit in LDS.  H % 128 == 0, so every slice is whole K-steps.
-  // One 16-token tile per workgroup: a workgroup that owns whole logits rows
-  // reads the whole router matrix, so its time is bounded by one CU's read
-  // rate whatever its token count, and 16-token tiles keep the most CUs busy
-  // (64-token tiles measured 2.5x slower at 4096 tokens).
+  if (T > kRouterSplitMaxT) {
+    // KS slices of K per column-tile group, U K-steps of 32 loaded ahead per
+    // stage; the partial logits of all slices fit in LDS.  H % 128 == 0, so
+    // every slice is whole K-steps.  16-token tiles keep the most CUs busy
+    // (64-token tiles measured 2.5x slower at 4096 tokens).
 #define MOE_ROUTER_CASE(N, TT_, KS_, U_)                                                              \
   hipLaunchKernelGGL((router_gate_kernel<N, TT_, KS_, U_>), dim3((T + 16 * TT_ - 1) / (16 * TT_)), \
                      dim3(256 * KS_), 0, s, hidden, wr, T, H, E, k, mode, renorm, scale, bias, logits_out, ids, w, \
                      ids2, w2)
-  if (epl <= 1) MOE_ROUTER_CASE(1, 1, 4, 4);
-  else if (epl <= 2) MOE_ROUTER_CASE(2, 1, 4, 2);
-  else if (epl <= 4) MOE_ROUTER_CASE(4, 1, 2, 2);
-  else if (epl <= 8) MOE_ROUTER_CASE(8, 1, 2, 2);
-  else MOE_ROUTER_CASE(16, 1, 1, 1);
+    if (epl <= 1) MOE_ROUTER_CASE(1, 1, 4, 4);
+    else if (epl <= 2) MOE_ROUTER_CASE(2, 1, 4, 2);
+    else if (epl <= 4) MOE_ROUTER_CASE(4, 1, 2, 2);
+    else if (epl <= 8) MOE_ROUTER_CASE(8, 1, 2, 2);
+    else MOE_ROUTER_CASE(16, 1, 1, 1);
 #undef MOE_ROUTER_CASE
+    return hipGetLastError();
+  }
+  const int KS = router_ks(T, H, E), hs = H / KS;
+  float* part = static_cast<float*>(ws);
+  const dim3 g1((T + 15) / 16, (E + 63) / 64, KS);
+  // all of a short slice's K steps in flight at once
+  if (hs <= 128) hipLaunchKernelGGL((router_partial_kernel<1, 4>), g1, dim3(256), 0, s, hidden, wr, T, H, E, hs, part);
+  else hipLaunchKernelGGL((router_partial_kernel<1, 8>), g1, dim3(256), 0, s, hidden, wr, T, H, E, hs, part);
+  const dim3 g2((T + 3) / 4);
+#define MOE_ROUTER_SEL(N)                                                                                  \
+  hipLaunchKernelGGL(router_select_kernel<N>, g2, dim3(256), 0, s, part, KS, T, E, k, mode, renorm, scale, \
+                     bias, logits_out, ids, w, ids2, w2)
+  if (epl <= 1) MOE_ROUTER_SEL(1);
+  else if (epl <= 2) MOE_ROUTER_SEL(2);
+  else if (epl <= 4) MOE_ROUTER_SEL(4);
+  else if (epl <= 8) MOE_ROUTER_SEL(8);
+  else MOE_ROUTER_SEL(16);
+#undef MOE_ROUTER_SEL
   return hipGetLastError();
 }
 

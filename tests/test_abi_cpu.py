@@ -102,13 +102,19 @@ def test_gate_and_permute_validation():
     assert L.moe_gate_topk(FAKE + 2, None, 4, 8, 2, 0, 1, 1.0, FAKE, FAKE, None) == 4
     assert L.moe_gate_topk(None, None, 0, 8, 2, 0, 1, 1.0, None, None, None) == 0
     R = L.moe_router_gate_topk
-    assert R(FAKE, FAKE, 4, 256, 8, 9, 0, 1, 1.0, None, None, FAKE, FAKE, None) == 2   # top_k > E
-    assert R(FAKE, FAKE, 4, 200, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, None) == 2   # H % 128
-    assert R(FAKE, None, 4, 256, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, None) == 1
-    assert R(FAKE, FAKE, 4, 256, 8, 2, 3, 1, 1.0, None, None, FAKE, FAKE, None) == 3
-    assert R(FAKE + 8, FAKE, 4, 256, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, None) == 4
-    assert R(FAKE, FAKE, 4, 256, 8, 2, 0, 1, 1.0, None, FAKE + 1, FAKE, FAKE, None) == 4
-    assert R(None, None, 0, 256, 8, 2, 0, 1, 1.0, None, None, None, None, None) == 0
+    BIG = 1 << 40
+    assert R(FAKE, FAKE, 4, 256, 8, 9, 0, 1, 1.0, None, None, FAKE, FAKE, FAKE, BIG, None) == 2   # top_k > E
+    assert R(FAKE, FAKE, 4, 200, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, FAKE, BIG, None) == 2   # H % 128
+    assert R(FAKE, None, 4, 256, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, FAKE, BIG, None) == 1
+    assert R(FAKE, FAKE, 4, 256, 8, 2, 3, 1, 1.0, None, None, FAKE, FAKE, FAKE, BIG, None) == 3
+    assert R(FAKE + 8, FAKE, 4, 256, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, FAKE, BIG, None) == 4
+    assert R(FAKE, FAKE, 4, 256, 8, 2, 0, 1, 1.0, None, FAKE + 1, FAKE, FAKE, FAKE, BIG, None) == 4
+    assert R(FAKE, FAKE, 4, 256, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, FAKE + 4, BIG, None) == 4
+    need = L.moe_router_workspace_bytes(4, 256, 8)
+    assert need > 0 and L.moe_router_workspace_bytes(4, 200, 8) == 0
+    assert R(FAKE, FAKE, 4, 256, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, FAKE, need - 1, None) == 5
+    assert R(FAKE, FAKE, 4, 256, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, None, BIG, None) == 5
+    assert R(None, None, 0, 256, 8, 2, 0, 1, 1.0, None, None, None, None, None, 0, None) == 0
     cap = moe.moe_permute_capacity(10, 2, 8, 16)
     assert cap == 10 * 2 + 8 * 15
     assert L.moe_permute(FAKE, 10, 2, 8, 16, FAKE, FAKE, FAKE, cap - 1, None, 0, None) == 2
