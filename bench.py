@@ -187,6 +187,35 @@ def traffic_summary(fetch_csv, write_csv, calib_fetch_csv, calib_write_csv, cali
             "hbm_bytes_per_launch": fetch + write, "kernel_source_hash": kernel_source_hash()}
 
 
+def counter_summary(csv_paths, simd_per_cu=4):
+    """Per-kernel averages per dispatch of every counter in rocprofv3
+    counter-collection CSVs, plus MFMA busy as a fraction of the SIMD cycles
+    (SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE * SIMDs)) when both were
+    collected in the same pass."""
+    import csv
+    from collections import defaultdict
+    vals = defaultdict(lambda: defaultdict(list))   # kernel -> counter -> per-dispatch values
+    for path in csv_paths:
+        rows = defaultdict(dict)                    # (kernel, dispatch) -> counter -> value
+        for r in csv.DictReader(open(path)):
+            key = (r["Kernel_Name"], r.get("Dispatch_Id") or r.get("Correlation_Id"))
+            name = r["Counter_Name"]
+            rows[key][name] = rows[key].get(name, 0.0) + float(r["Counter_Value"])
+        for (kern, _), cs in rows.items():
+            for name, v in cs.items():
+                vals[kern][name].append(v)
+    out = {}
+    for kern, cs in vals.items():
+        rec = {name: sum(v) / len(v) for name, v in cs.items()}
+        rec["dispatches"] = max(len(v) for v in cs.values())
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in rec and "GRBM_GUI_ACTIVE" in rec:
+            import torch
+            cus = torch.cuda.get_device_properties(0).multi_processor_count if torch.cuda.is_available() else 256
+            rec["mfma_busy_frac"] = rec["SQ_VALU_MFMA_BUSY_CYCLES"] / (rec["GRBM_GUI_ACTIVE"] * cus * simd_per_cu)
+        out[kern] = rec
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -204,7 +233,13 @@ def main():
     ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="host only: print the GEMM1 HBM-traffic record from rocprofv3 counter CSVs "
                          "(the copy ones from --copy-calibration 1024) and exit")
+    ap.add_argument("--counter-summary", nargs="+", metavar="CSV",
+                    help="host only: print per-kernel counter averages (and MFMA busy fraction) from "
+                         "rocprofv3 counter-collection CSVs and exit")
     args = ap.parse_args()
+    if args.counter_summary:
+        print(json.dumps(counter_summary(args.counter_summary), indent=1))
+        return
     if args.traffic_summary:
         print(json.dumps(traffic_summary(*args.traffic_summary, 1024), indent=1))
         return

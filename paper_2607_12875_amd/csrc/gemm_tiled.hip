@@ -85,8 +85,9 @@ __device__ __forceinline__ bf16x8 int4x8_biased_bf16(uint32_t w, uint32_t keep) 
 template <int KB>
 __device__ __forceinline__ int swz(int r) { return KB == 256 ? r & 15 : KB == 128 ? (r >> 1) & 7 : (r >> 2) & 3; }
 // int4 B rows (32 or 64 bytes: 2 or 4 chunks)
+// (128-byte 4-bit rows, 256-element MXFP8 steps: as swz<128>)
 template <int BB>
-__device__ __forceinline__ int swz_b(int r) { return BB == 32 ? (r >> 2) & 1 : (r >> 2) & 3; }
+__device__ __forceinline__ int swz_b(int r) { return BB == 32 ? (r >> 2) & 1 : BB == 64 ? (r >> 2) & 3 : (r >> 1) & 7; }
 
 // NP > 0: NP extra waves only issue the global->LDS copies and the NW math
 // waves never touch global memory in the main loop, so a stalled load queue
@@ -105,8 +106,8 @@ void moe_gemm_tiled(GroupedGemm g) {
   constexpr bool MX8 = FMT == 5;              // MXFP4 weights, MXFP8 activations
   constexpr bool A8 = FMT == 1 || MX8;        // one-byte (e4m3) activations
   constexpr bool B4 = F4B || MX8;             // 4-bit weight rows
-  static_assert(KBT == 128 || (KBT == 64 && FMT == 0) || (KBT == 256 && F4B),
-                "64-byte steps are bf16 only, 256-byte steps 4-bit weights with bf16 activations only");
+  static_assert(KBT == 128 || (KBT == 64 && FMT == 0) || (KBT == 256 && (F4B || FMT == 5)),
+                "64-byte steps are bf16 only, 256-byte steps 4-bit weights only");
   constexpr int KB = KBT;                                       // A bytes per row per step
   constexpr int KE = A8 ? KB : KB / 2;                                 // K elements per step
   constexpr int BB = B4 ? KE / 2 : KB;                                 // B bytes per row per step
@@ -123,17 +124,19 @@ void moe_gemm_tiled(GroupedGemm g) {
   static_assert(A_CH >= 1 && B_CH >= 1 && A_CH * LW * 1024 == BM * KB && B_CH * LW * 1024 == BNW * BB, "");
   static_assert(!GEMM1 || TN % 2 == 0, "gate/up pairs");
   static_assert(FMT != 1 || !GEMM1 || NC == 128, "fp8 requant needs one 128-column group per tile");
-  static_assert(!MX8 || (NP > 0 && WM * WN == 4 && KB == 128), "MXFP8: four math waves beside copy waves");
+  static_assert(!MX8 || (NP > 0 && WM * WN == 4), "MXFP8: four math waves beside copy waves");
   // per-stage scale block: NW slots of 256 bytes, one 4-byte DMA instruction
   // each (64 floats); fp8: slots [0, BM/64) the row scales of A, slot BM/64
   // the block scales of B; int4: slots [0, BNW/64) the bf16 pair holding each
   // B row's group scale, int4 GEMM1 also slots [BNW/64, BNW/64 + BM/64) the
   // rows' biased group sums (x_gsum).  Copy wave lw fills slots lw, lw + LW, ...
-  // MXFP8: slots [0, BM/64) the E8M0 dwords of the A rows (four 32-element
-  // blocks per step), then BNW/64 slots of the B rows' E8M0 dwords; slots
-  // past those load a harmless dummy.
+  // MXFP8: MXD E8M0 dwords per row per step (four 32-element blocks each);
+  // slots [0, MXD BM/64) the A rows' dwords (slot d BM/64 + g: dword d of
+  // row group g), then MXD BNW/64 slots of the B rows' likewise; slots past
+  // those load a harmless dummy.
   constexpr bool GSUM = FMT == 2 && GEMM1;
-  constexpr int NSLOT = FMT == 0 ? 0 : (MX8 ? (BM + BNW) / 64 : (GSUM ? 2 : 1) * NW);
+  constexpr int MXD = MX8 ? KE / 128 : 1;
+  constexpr int NSLOT = FMT == 0 ? 0 : (MX8 ? MXD * (BM + BNW) / 64 : (GSUM ? 2 : 1) * NW);
   constexpr int SC = (NSLOT + LW - 1) / LW;  // scale loads per copy wave per stage
   static_assert(FMT != 1 || BM / 64 < NW, "fp8 scale DMA layout");
   static_assert(!F4B || (NW == 4 && BNW / 64 <= NW), "4-bit scale DMA layout");
@@ -224,9 +227,10 @@ void moe_gemm_tiled(GroupedGemm g) {
       for (int k = 0; k < NSL; ++k) {
         const int r = (lw + k * LW) * 64 + lane;
         int v = 0;
-        if (A8 && lw + k * LW < BM / 64) {
-          if constexpr (NP > 0) v = staged ? lds_sid[lw][r] : g.sorted_ids[m0 + r];
-          else v = g.sorted_ids[m0 + r];
+        if (A8 && lw + k * LW < MXD * (BM / 64)) {
+          const int ra = ((lw + k * LW) % (BM / 64)) * 64 + lane;  // A row of the slot
+          if constexpr (NP > 0) v = staged ? lds_sid[lw][ra] : g.sorted_ids[m0 + ra];
+          else v = g.sorted_ids[m0 + ra];
         }
         const int rg = (lw + k * LW - BNW / 64) * 64 + lane;  // group-sum slot row
         if (GSUM && lw + k * LW >= BNW / 64 && lw + k * LW < BNW / 64 + BM / 64) {
@@ -308,18 +312,19 @@ void moe_gemm_tiled(GroupedGemm g) {
           src.ss[k] = 4;
         }
       } else if constexpr (MX8) {
-        if (sl < BM / 64) {
-          // A row (sl*64 + lane): its E8M0 bytes [K/32], the four of step kt one dword
-          const int r = sl * 64 + lane;
-          if (GEMM1) src.s[k] = g.x_mx + token(sid[A_CH + k]) * (g.H / 32);
-          else src.s[k] = g.inter_mx + static_cast<size_t>(m0 + r) * (g.I / 32);
-          src.ss[k] = 4;
-        } else if (sl < BM / 64 + BNW / 64) {
-          const int r = (sl - BM / 64) * 64 + lane;
+        if (sl < MXD * (BM / 64)) {
+          // A row (sl % (BM/64))*64 + lane: its E8M0 bytes [K/32]; dword sl / (BM/64) of step kt
+          const int r = (sl % (BM / 64)) * 64 + lane, d = sl / (BM / 64);
+          if (GEMM1) src.s[k] = g.x_mx + token(sid[A_CH + k]) * (g.H / 32) + 4 * d;
+          else src.s[k] = g.inter_mx + static_cast<size_t>(m0 + r) * (g.I / 32) + 4 * d;
+          src.ss[k] = 4 * MXD;
+        } else if (sl < MXD * (BM / 64 + BNW / 64)) {
+          const int sb2 = sl - MXD * (BM / 64);
+          const int r = (sb2 % (BNW / 64)) * 64 + lane, d = sb2 / (BNW / 64);
           const int n = GEMM1 ? (r < NC ? n0 + r : g.I + n0 + (r - NC)) : n0 + r;
           src.s[k] = static_cast<const uint8_t*>(GEMM1 ? g.w1_scale : g.w2_scale) +
-                     (static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) + n) * (K / 32);
-          src.ss[k] = 4;
+                     (static_cast<size_t>(e) * (GEMM1 ? 2 * g.I : g.H) + n) * (K / 32) + 4 * d;
+          src.ss[k] = 4 * MXD;
         }
       } else if constexpr (FMT == 4) {
         if (sl < BNW / 64) {
@@ -824,46 +829,52 @@ void moe_gemm_tiled(GroupedGemm g) {
         // weight fragment is the first operand).  MFMA kk of the step covers
         // K [64 kk, 64 kk + 64) in two 32-element scale blocks, and lane
         // group kg supplies block kg's E8M0 byte for both operands (byte
-        // 2 kk + kg of each row's step dword; the instruction applies the
-        // scales itself, so the products accumulate in place: no rescale on
-        // the VALU).  Weights: lane group kg holds block kg, 16 bytes (chunk
-        // 2 kk + kg of the 64-byte row).  Activations: the e4m3 operand
-        // interleaves the blocks in 16-element halves -- lane group kg holds
-        // elements [16 kg, +16) of block 0, then of block 1, i.e. chunks
-        // 4 kk + kg and 4 kk + 2 + kg of the 128-byte row.
-        i32x8 af[2][TM], bq[2][TN];
+        // 2 (kk % 2) + kg of the row's dword kk / 2 for the step; the
+        // instruction applies the scales itself, so the products accumulate
+        // in place: no rescale on the VALU).  Weights: lane group kg holds
+        // block kg, 16 bytes (chunk 2 kk + kg of the row's KE/2 bytes).
+        // Activations: the e4m3 operand interleaves the blocks in 16-element
+        // halves -- lane group kg holds elements [16 kg, +16) of block 0,
+        // then of block 1, i.e. chunks 4 kk + kg and 4 kk + 2 + kg of the
+        // row's KE bytes.
+        const uint32_t* sA = reinterpret_cast<const uint32_t*>(Ss);                          // [MXD][BM]
+        const uint32_t* sB = reinterpret_cast<const uint32_t*>(Ss + MXD * (BM / 64) * 256);  // [MXD][BNW]
+        // per 128 K elements (one E8M0 dword per row): MFMAs 2 d and 2 d + 1
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
+        for (int d = 0; d < MXD; ++d) {
+          i32x8 af[2][TM], bq[2][TN];
 #pragma unroll
-          for (int i = 0; i < TM; ++i) {
-            const int r = wm * WTM + i * 32 + l32;
-            const i32x4 lo = __builtin_bit_cast(i32x4, ld16(As + r * KB + (((4 * kk + kg) ^ swz<KB>(r)) << 4)));
-            const i32x4 hi = __builtin_bit_cast(i32x4, ld16(As + r * KB + (((4 * kk + 2 + kg) ^ swz<KB>(r)) << 4)));
-            af[kk][i] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          for (int h = 0; h < 2; ++h) {
+            const int kk = 2 * d + h;
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+              const int r = wm * WTM + i * 32 + l32;
+              const i32x4 lo = __builtin_bit_cast(i32x4, ld16(As + r * KB + (((4 * kk + kg) ^ swz<KB>(r)) << 4)));
+              const i32x4 hi = __builtin_bit_cast(i32x4, ld16(As + r * KB + (((4 * kk + 2 + kg) ^ swz<KB>(r)) << 4)));
+              af[h][i] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+              const int r = brow(j) + l32;
+              const i32x4 q = __builtin_bit_cast(i32x4, ld16(Bs + r * BB + (((2 * kk + kg) ^ swz_b<BB>(r)) << 4)));
+              bq[h][j] = __builtin_shufflevector(q, q, 0, 1, 2, 3, 0, 1, 2, 3);  // upper half unused
+            }
           }
+          int da[TM], db[TN];  // the row's dword d moved down by kg bytes: byte 2 h is block 2 h + kg
 #pragma unroll
-          for (int j = 0; j < TN; ++j) {
-            const int r = brow(j) + l32;
-            const i32x4 q = __builtin_bit_cast(i32x4, ld16(Bs + r * BB + (((2 * kk + kg) ^ swz_b<BB>(r)) << 4)));
-            bq[kk][j] = __builtin_shufflevector(q, q, 0, 1, 2, 3, 0, 1, 2, 3);  // upper half unused
-          }
+          for (int i = 0; i < TM; ++i) da[i] = static_cast<int>(sA[d * BM + wm * WTM + i * 32 + l32] >> (8 * kg));
+#pragma unroll
+          for (int j = 0; j < TN; ++j) db[j] = static_cast<int>(sB[d * BNW + brow(j) + l32] >> (8 * kg));
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x64_f4f8<0>(bq[0][j], af[0][i], db[j], da[i], acc[i][j]);
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x64_f4f8<2>(bq[1][j], af[1][i], db[j], da[i], acc[i][j]);
         }
-        const uint32_t* sA = reinterpret_cast<const uint32_t*>(Ss);                    // [BM]
-        const uint32_t* sB = reinterpret_cast<const uint32_t*>(Ss + (BM / 64) * 256);  // [BNW]
-        int da[TM], db[TN];  // the row's step dword moved down by kg bytes: byte 2 kk is block 2 kk + kg
-#pragma unroll
-        for (int i = 0; i < TM; ++i) da[i] = static_cast<int>(sA[wm * WTM + i * 32 + l32] >> (8 * kg));
-#pragma unroll
-        for (int j = 0; j < TN; ++j) db[j] = static_cast<int>(sB[brow(j) + l32] >> (8 * kg));
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x64_f4f8<0>(bq[0][j], af[0][i], db[j], da[i], acc[i][j]);
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x64_f4f8<2>(bq[1][j], af[1][i], db[j], da[i], acc[i][j]);
       } else {  // MXFP4
         // lane group kg covers elements [64 kg, 64 kg + 64) of the step, the
         // 32-element blocks 2 kg and 2 kg + 1: their E8M0 bytes are bytes
@@ -1086,6 +1097,10 @@ template <int FMT, bool GEMM1, int BM, int BNW, int WM, int WN, int GM, int KBT 
 hipError_t launch_tiled(const GroupedGemm& g, hipStream_t s) {
   constexpr int NC = GEMM1 ? BNW / 2 : BNW;
   constexpr int NT = (WM * WN + NP) * 64;
+  // only bf16 handles a ragged last K step; every other format's steps must
+  // tile K exactly (a step past K would read beyond its rows)
+  constexpr int KE = (FMT == 1 || FMT == 5) ? KBT : KBT / 2;
+  if (FMT != 0 && (GEMM1 ? g.H : g.I) % KE != 0) return hipErrorInvalidValue;
   const long mt = g.max_rows / BM, nt = ((GEMM1 ? g.I : g.H) + NC - 1) / NC;
   auto kern = moe_gemm_tiled<FMT, GEMM1, BM, BNW, WM, WN, GM, KBT, STAGES, NP>;
   // workgroups per CU depend on the kernel's registers and LDS only: queried
@@ -1211,18 +1226,21 @@ hipError_t launch_gemm2_mxfp4_tiled(const GroupedGemm& g, hipStream_t s) {
   }
 }
 // MXFP4 weights x MXFP8 activations: the fp8 tile (128 x 256, four math
-// waves beside four copy waves), 128-element K steps (128 bytes of each
-// activation row, 64 of each weight row, and one E8M0 dword per row of
-// either), four stages
-#ifndef MOE_TM8_STAGES
-#define MOE_TM8_STAGES 4
-#endif
-hipError_t launch_gemm1_mx8(const GroupedGemm& g, hipStream_t s) {
-  return launch_tiled<5, true, 128, 256, 2, 2, MOE_TGM, 128, MOE_TM8_STAGES, 4>(g, s);
+// waves beside four copy waves).  When K is a multiple of 256, 256-element K
+// steps, so each weight row gives a whole 128-byte line per step (256 bytes
+// of each activation row, two E8M0 dwords per row of either), two stages;
+// otherwise (K a multiple of 128) 128-element steps (half a line of each
+// weight row) with four stages.  A step never reaches past K.
+template <bool GEMM1, int BNW>
+hipError_t launch_mx8(const GroupedGemm& g, hipStream_t s) {
+  const int K = GEMM1 ? g.H : g.I;
+  if (K % 256 == 0) return launch_tiled<5, GEMM1, 128, BNW, 2, 2, MOE_TGM, 256, 2, 4>(g, s);
+  return launch_tiled<5, GEMM1, 128, BNW, 2, 2, MOE_TGM, 128, 4, 4>(g, s);
 }
+hipError_t launch_gemm1_mx8(const GroupedGemm& g, hipStream_t s) { return launch_mx8<true, 256>(g, s); }
 hipError_t launch_gemm2_mx8(const GroupedGemm& g, hipStream_t s) {
-  if (g.H % 256) return launch_tiled<5, false, 128, 128, 2, 2, MOE_TGM, 128, MOE_TM8_STAGES, 4>(g, s);
-  return launch_tiled<5, false, 128, 256, 2, 2, MOE_TGM, 128, MOE_TM8_STAGES, 4>(g, s);
+  if (g.H % 256) return launch_mx8<false, 128>(g, s);
+  return launch_mx8<false, 256>(g, s);
 }
 hipError_t launch_gemm2_int4(const GroupedGemm& g, hipStream_t s) {
   if (g.H % 256) return launch_tiled<2, false, MOE_TI4_BM, 128, 1, 4, MOE_TGM_INT4, MOE_TI4_KB, MOE_TI4_STAGES, MOE_TI4_NP2>(g, s);
