@@ -84,7 +84,12 @@ typedef enum {
      of codes exactly and applies the group's scale in fp32; the second
      rounds q * scale to bf16 before its products.  A scale may be zero;
      the nonzero scales must be normal numbers within a factor 2^64 of each
-     other along a weight row (other scales are unspecified). */
+     other along a weight row (other scales are unspecified): the first
+     product carries its running sums divided by the current group's scale,
+     so a ratio r between groups multiplies them by r, and 2^64 keeps them
+     inside the fp32 range with about 2^30 to spare for the sums themselves.
+     Scales from a per-group amax quantiser of real weight rows differ by a
+     few powers of two. */
   MOE_W_INT4_G128 = 2,
   /* Weight-only fp8 (a decode route): the MOE_W_FP8E4M3_B128 storage and
      scales, but the hidden rows enter unquantised (bf16) and the SwiGLU
@@ -176,7 +181,10 @@ size_t moe_permute_capacity(int T, int top_k, int E, int block_m);
 size_t moe_permute_workspace_bytes(int T, int top_k, int E);
 
 /*
- * Permute / align: groups the T*top_k routed rows by expert.
+ * Permute / align: groups the T*top_k routed rows by expert -- the hand-over
+ * from the MoE Gate node to the Fused MoE node of Fig. 1 (and Fig. 3): the
+ * fused expert products consume each expert's routed rows as one contiguous
+ * segment (the paper names the nodes, not this step's algorithm).
  *   topk_ids        device int32 [T,top_k], each in [0,E)
  *   block_m         1..1024: every expert segment is padded to a multiple
  *   expert_offsets  device int32 [E+1]: off[0]=0,
