@@ -117,6 +117,14 @@ def test_fp8_h_not_multiple_of_256(dev):
     _check(synth.tiny_config(4, T=150, H=384, I=384, E=8, top_k=3))
 
 
+# A single K step in GEMM2 (I = 128) with a full-width GEMM2 tile (H = 256),
+# and several row tiles per expert on a wider layer.
+@pytest.mark.parametrize("shape", [dict(T=400, H=256, I=128, E=4, top_k=2),
+                                   dict(T=2000, H=768, I=1024, E=24, top_k=3)])
+def test_fp8_more_shapes(dev, shape):
+    _check(synth.tiny_config(4, **shape))
+
+
 @pytest.mark.parametrize("T", [1, 45, 300, 1000])
 def test_int4_small(dev, T):
     _check(synth.tiny_config(5, T=T, H=512, I=256, E=12, top_k=4))
