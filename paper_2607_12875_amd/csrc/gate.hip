@@ -29,7 +29,7 @@ __global__ __launch_bounds__(256) void gate_rank_kernel(
     const float* __restrict__ logits, const float* __restrict__ bias, int T, int E, int k,
     int mode, int renorm, float scale, int32_t* __restrict__ ids, float* __restrict__ w,
     int32_t* __restrict__ ids2, float* __restrict__ w2) {
-  __shared__ double skey[4][EPL * 64];
+  __shared__ __attribute__((aligned(16))) double skey[4][EPL * 64];
   __shared__ double sval[4][EPL * 64];  // logit (softmax) or sigmoid score, for the weights
   __shared__ double sel[4][MOE_GATE_MAX_K];
   const int wv = threadIdx.x >> 6;

@@ -161,13 +161,17 @@ __device__ __forceinline__ void gate_rank_row(const float* lg, const float* bias
   int rank[EPL];
 #pragma unroll
   for (int i = 0; i < EPL; ++i) rank[i] = 0;
-#pragma unroll 4
-  for (int e2 = 0; e2 < E; ++e2) {
-    const double k2 = skey[e2];  // same address in every lane: a broadcast read
+  // every one of the wave's EPL*64 key slots, two per 16-byte read: slots
+  // past E hold -inf at indices above every real expert, so they never beat
+  // a real key and the ranks are those over the E experts
+#pragma unroll 8
+  for (int e2 = 0; e2 < EPL * 64; e2 += 2) {
+    const double2 k2 = *reinterpret_cast<const double2*>(skey + e2);  // same address in every lane: a broadcast read
 #pragma unroll
     for (int i = 0; i < EPL; ++i) {
       const int e = lane + 64 * i;
-      rank[i] += (k2 > key[i]) || (k2 == key[i] && e2 < e);
+      rank[i] += (k2.x > key[i]) || (k2.x == key[i] && e2 < e);
+      rank[i] += (k2.y > key[i]) || (k2.y == key[i] && e2 + 1 < e);
     }
   }
   __builtin_amdgcn_wave_barrier();  // every lane is done reading the keys
@@ -183,31 +187,32 @@ __device__ __forceinline__ void gate_rank_row(const float* lg, const float* bias
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  if (lane >= k) return;
 
-  const double my_v = sel[lane];
+  // lane j < k holds selected slot j; the sums and maxima are wave
+  // reductions (one exp per lane), every lane taking part
+  const bool on = lane < k;
+  const double my_v = on ? sel[lane] : 0.0;
   double wt;
   if (mode == 0) {
     if (renorm) {
-      double m = -INFINITY;
-      for (int j = 0; j < k; ++j) m = fmax(m, sel[j]);
-      double z = 0.0;
-      for (int j = 0; j < k; ++j) z += exp(sel[j] - m);
-      wt = exp(my_v - m) / z;
+      const double m = wave_max(on ? my_v : -INFINITY);
+      const double z = on ? exp(my_v - m) : 0.0;
+      wt = z / wave_sum(z);
     } else {
       double m = -INFINITY;
-      for (int e2 = 0; e2 < E; ++e2) m = fmax(m, sval[e2]);
-      double z = 0.0;
-      for (int e2 = 0; e2 < E; ++e2) z += exp(sval[e2] - m);
-      wt = exp(my_v - m) / z;
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) m = fmax(m, lv[i]);
+      m = wave_max(m);
+      double zs = 0.0;
+#pragma unroll
+      for (int i = 0; i < EPL; ++i)
+        if (lane + 64 * i < E) zs += exp(lv[i] - m);
+      wt = exp(my_v - m) / wave_sum(zs);
     }
-  } else if (renorm) {
-    double z = 0.0;
-    for (int j = 0; j < k; ++j) z += sel[j];
-    wt = my_v / z;
   } else {
-    wt = my_v;
+    wt = renorm ? my_v / wave_sum(my_v) : my_v;
   }
+  if (!on) return;
   wt *= static_cast<double>(scale);
   const int my_id = slot_id[lane];
   ids[lane] = my_id;

@@ -38,7 +38,7 @@ __global__ __launch_bounds__(256 * KS) void router_gate_kernel(
   constexpr int TM = 16 * TT;        // tokens per workgroup
   constexpr int LDE = 64 * EPL + 4;  // LDS row stride of the logits (floats)
   __shared__ float part[KS][TM][LDE];  // per-slice partial logits; slice 0 then holds the sums
-  __shared__ double skey[RANK ? NW : 1][RANK ? EPL * 64 : 1];
+  __shared__ __attribute__((aligned(16))) double skey[RANK ? NW : 1][RANK ? EPL * 64 : 1];
   __shared__ double sval[RANK ? NW : 1][RANK ? EPL * 64 : 1];
   __shared__ double ssel[RANK ? NW : 1][RANK ? MOE_GATE_MAX_K : 1];
 
@@ -209,7 +209,7 @@ __global__ __launch_bounds__(256) void router_select_kernel(const float* __restr
                                                             float* __restrict__ w2) {
   constexpr bool RANK = EPL <= MOE_GATE_RANK_MAX_EPL;
   __shared__ float lg[4][EPL * 64];
-  __shared__ double skey[RANK ? 4 : 1][RANK ? EPL * 64 : 1];
+  __shared__ __attribute__((aligned(16))) double skey[RANK ? 4 : 1][RANK ? EPL * 64 : 1];
   __shared__ double sval[RANK ? 4 : 1][RANK ? EPL * 64 : 1];
   __shared__ double ssel[RANK ? 4 : 1][RANK ? MOE_GATE_MAX_K : 1];
   const int wv = threadIdx.x >> 6, lane = lane_id();
