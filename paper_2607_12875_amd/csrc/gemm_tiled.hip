@@ -472,6 +472,14 @@ void moe_gemm_tiled(GroupedGemm g) {
         if (q < nk) issue(cur, q, (sb + q) % STAGES);
     }
 
+    // GEMM2: the ids of this lane's output rows, for the epilogue's pad-row
+    // check, requested before the K loop (the math waves issue no other
+    // global loads, so this one has landed long before it is used)
+    int sid_ep[GEMM1 ? 1 : TM];
+    if constexpr (!GEMM1) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) sid_ep[i] = g.sorted_ids[m0 + wm * WTM + i * 32 + l32];
+    }
     f32x16 acc[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -1030,7 +1038,7 @@ void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int row = m0 + wm * WTM + i * 32 + l32;
-        if (g.sorted_ids[row] >= g.n_routed) continue;  // pad rows are never read
+        if (sid_ep[i] >= g.n_routed) continue;  // pad rows are never read
         uint16_t* yr = static_cast<uint16_t*>(g.y) + static_cast<size_t>(row) * g.H;
 #pragma unroll
         for (int j = 0; j < TN; ++j)
@@ -1049,7 +1057,7 @@ void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int row = m0 + wm * WTM + i * 32 + l32;
-        if (g.sorted_ids[row] >= g.n_routed) continue;  // pad rows are never read
+        if (sid_ep[i] >= g.n_routed) continue;  // pad rows are never read
         float* yr = static_cast<float*>(g.y) + static_cast<size_t>(row) * g.H;
 #pragma unroll
         for (int j = 0; j < TN; ++j)
