@@ -97,12 +97,13 @@ __device__ __forceinline__ void gate_argmax_row(const float* lg, const float* bi
 #pragma unroll
     for (int i = 0; i < EPL; ++i)
       if (lane + 64 * i == be) taken |= 1u << i;
-    // the owner lane broadcasts the selected expert's logit / score
+    // the owner lane (be % 64: be is the same in every lane) broadcasts the
+    // selected expert's logit / score
     double v = 0.0;
 #pragma unroll
     for (int i = 0; i < EPL; ++i)
       if (lane + 64 * i == be) v = lv[i];
-    v = wave_sum(v);  // exactly one lane contributed
+    v = __shfl(v, be & 63);
     if (lane == j) { my_id = be; my_v = v; }
   }
 

@@ -66,7 +66,7 @@ __global__ __launch_bounds__(kPermThreads) void permute_scatter_kernel(
     const int32_t* __restrict__ ids, int n, int E, int C, int block_m, int nchunks,
     const int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
     int32_t* __restrict__ sorted_ids, int32_t* __restrict__ inv_pos, int cap) {
-  __shared__ uint32_t bitmap[kBitmapWords];
+  __shared__ __attribute__((aligned(16))) uint32_t bitmap[kBitmapWords];
   __shared__ int base[1024];
   __shared__ int wave_tot[16];
   __shared__ int total_padded;
@@ -91,14 +91,15 @@ __global__ __launch_bounds__(kPermThreads) void permute_scatter_kernel(
     if (counts == nullptr) {
       for (int w = 0; w < W; ++w) tot += __popc(bitmap[tid * W + w]);
     } else {
-      // every chunk's count of expert tid, sixteen loads in flight at a time
-      // (indices clamped so the loads issue unconditionally)
-      for (int c0 = 0; c0 < nchunks; c0 += 16) {
-        int v[16];
+      // every chunk's count of expert tid, up to 64 loads in flight at a time
+      // (one round of memory latency up to 64 chunks, i.e. 65536 routed rows;
+      // indices clamped so the loads issue unconditionally)
+      for (int c0 = 0; c0 < nchunks; c0 += 64) {
+        int v[64];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) v[u] = counts[min(c0 + u, nchunks - 1) * E + tid];
+        for (int u = 0; u < 64; ++u) v[u] = counts[min(c0 + u, nchunks - 1) * E + tid];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) {
+        for (int u = 0; u < 64; ++u) {
           const int cc = c0 + u;
           if (cc < nchunks) tot += v[u];
           if (cc < c) pre += v[u];
@@ -121,10 +122,14 @@ __global__ __launch_bounds__(kPermThreads) void permute_scatter_kernel(
     for (int p = total_padded + tid; p < cap; p += kPermThreads) sorted_ids[p] = n;
 
   if (my_e >= 0) {
-    const uint32_t* row = bitmap + my_e * W;
+    const uint32_t* row = bitmap + my_e * W;  // 16-byte aligned: W is a multiple of 4
     const int wi = tid >> 5;
     int rank = __popc(row[wi] & ((1u << (tid & 31)) - 1u));
-    for (int w = 0; w < wi; ++w) rank += __popc(row[w]);
+    for (int w = 0; w + 4 <= wi; w += 4) {  // the whole words below, four per read
+      const u32x4 q = *reinterpret_cast<const u32x4*>(row + w);
+      rank += __popc(q.x) + __popc(q.y) + __popc(q.z) + __popc(q.w);
+    }
+    for (int w = wi & ~3; w < wi; ++w) rank += __popc(row[w]);
     const int pos = base[my_e] + rank;
     sorted_ids[pos] = f;
     inv_pos[f] = pos;
