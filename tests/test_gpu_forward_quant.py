@@ -40,7 +40,31 @@ def test_act_quant_bit_exact_crafted(dev):
     x[1, 5], x[1, 6] = 1.0, -0.5                        # amax 1: top code, non-exact scale
     x[2, 128], x[2, 129], x[2, 130] = 896.0, 2.125, 2.375   # s = 2: ties 1.0625 / 1.1875
     x[3] = np.linspace(-3, 3, 256)
+    x[3, 100] = -0.0                                    # keeps its sign: code 0x80
     _act_quant_check(_bf16(x))
+
+
+def test_act_quant_bit_exact_structured(dev):
+    # Groups whose scale is set by one amax (255 bf16 patterns across the
+    # normal range, plus zero and denormal ones) holding every bf16 magnitude
+    # up to it, signs alternating: the quantiser's per-element quotient is
+    # checked code for code against the oracle's IEEE division.
+    amaxes = list(range(0x0080, 0x7F80, 128)) + [0x0000, 0x0001, 0x007F]
+    groups = []
+    for a in amaxes:
+        xs = np.arange(0, a + 1, dtype=np.uint16)
+        sign = (np.arange(xs.size) & 1).astype(np.uint16) << 15
+        xs = np.concatenate([xs | sign, np.array([0x8000], np.uint16)])  # and -0
+        for g0 in range(0, xs.size, 127):
+            grp = np.zeros(128, np.uint16)
+            grp[0] = a
+            piece = xs[g0:g0 + 127]
+            grp[1:1 + piece.size] = piece
+            groups.append(grp)
+    while len(groups) % 8:
+        groups.append(np.zeros(128, np.uint16))
+    bits = np.stack(groups).reshape(-1, 8 * 128)
+    _act_quant_check(bits)
 
 
 def test_act_quant_bit_exact_fp8_workload_rows(dev):
