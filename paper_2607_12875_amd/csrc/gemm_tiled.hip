@@ -1034,7 +1034,11 @@ void moe_gemm_tiled(GroupedGemm g) {
         else store(true);
       }
     } else if constexpr (A8) {
-      // transposed layout: four consecutive output columns per 8-byte store
+      // transposed layout: a lane holds four consecutive output columns per
+      // group and the lane 32 away the next four of the same row, so one
+      // exchange makes eight consecutive columns per 16-byte store (half the
+      // store instructions of 8-byte stores: GEMM2 of the fp8 workload
+      // 1608 -> 1502 us)
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int row = m0 + wm * WTM + i * 32 + l32;
@@ -1043,11 +1047,19 @@ void moe_gemm_tiled(GroupedGemm g) {
 #pragma unroll
         for (int j = 0; j < TN; ++j)
 #pragma unroll
-          for (int v4 = 0; v4 < 4; ++v4) {
-            const int col = n0 + wn * WTN + j * 32 + 8 * v4 + 4 * kg;
+          for (int p = 0; p < 2; ++p) {
+            // groups 2p and 2p+1 (columns 16p + [0,16) of the block): lane kg
+            // keeps its own four columns of group 2p+kg and takes the other
+            // lane's four of that group, then stores eight columns at once
             const f32x16& c = acc[i][j];
-            const uint2 pk = {pack_bf16x2(c[4 * v4], c[4 * v4 + 1]), pack_bf16x2(c[4 * v4 + 2], c[4 * v4 + 3])};
-            *reinterpret_cast<uint2*>(yr + col) = pk;
+            const int ga = 2 * p, gb = 2 * p + 1;
+            const uint32_t a0 = pack_bf16x2(c[4 * ga], c[4 * ga + 1]), a1 = pack_bf16x2(c[4 * ga + 2], c[4 * ga + 3]);
+            const uint32_t b0 = pack_bf16x2(c[4 * gb], c[4 * gb + 1]), b1 = pack_bf16x2(c[4 * gb + 2], c[4 * gb + 3]);
+            const uint32_t s0 = kg ? a0 : b0, s1 = kg ? a1 : b1;
+            const uint32_t r0 = __shfl_xor(s0, 32), r1 = __shfl_xor(s1, 32);
+            const u32x4 o = kg ? u32x4{r0, r1, b0, b1} : u32x4{a0, a1, r0, r1};
+            const int col = n0 + wn * WTN + j * 32 + 16 * p + 8 * kg;
+            *reinterpret_cast<u32x4*>(yr + col) = o;
           }
       }
     } else {
