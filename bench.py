@@ -126,6 +126,43 @@ class HipEvents:
             self.rt.hipEventDestroy(e)
 
 
+def measure_peaks(moe, torch) -> dict:
+    """Achievable peaks of this machine, from the library's probes (see
+    include/moe_peaks.h), each timed with HIP events over three launches on
+    torch's current stream: MFMA-only loops in bf16 and fp8 (TFLOP/s), a
+    2 GiB streaming read and a 2 GiB streaming copy (read + write bytes),
+    GB/s."""
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    ev = HipEvents(2)
+    ev.rt.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    out = {}
+
+    def timed(fn, reps=3):
+        fn()  # warm
+        ev.rt.hipEventRecord(ev.ev[0], stream)
+        for _ in range(reps):
+            fn()
+        ev.rt.hipEventRecord(ev.ev[1], stream)
+        return ev.elapsed_ms(0, 1) / reps
+
+    sink = torch.empty(moe.moe_peak_sink_elems(), dtype=torch.float32, device="cuda")
+    iters = 4096
+    for name, fp8 in (("mfma_bf16_tflops", False), ("mfma_fp8_tflops", True)):
+        ms = timed(lambda: moe.moe_peak_mfma(fp8, iters, sink))
+        out[name] = moe.moe_peak_mfma_flops_per_launch(fp8, iters) / (ms * 1e-3) / 1e12
+    nbytes = 2 << 30
+    src = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    words = torch.zeros(moe.moe_peak_sink_elems(), dtype=torch.int32, device="cuda")
+    ms = timed(lambda: moe.moe_peak_read(src, words))
+    out["hbm_read_gbs"] = nbytes / (ms * 1e-3) / 1e9
+    ms = timed(lambda: moe.moe_peak_copy(src, dst))
+    out["hbm_copy_gbs"] = 2 * nbytes / (ms * 1e-3) / 1e9
+    ev.close()
+    del src, dst, sink, words
+    return out
+
+
 def cpu_baseline(cfg, inputs, budget_s: float):
     """Time the fp64 oracle on the host: the whole layer when it fits the
     budget, else a token sample; returns the baseline record."""
@@ -233,6 +270,8 @@ def main():
     ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="host only: print the GEMM1 HBM-traffic record from rocprofv3 counter CSVs "
                          "(the copy ones from --copy-calibration 1024) and exit")
+    ap.add_argument("--peaks", action="store_true",
+                    help="only measure the box's achievable MFMA and copy peaks, print them, and exit")
     ap.add_argument("--counter-summary", nargs="+", metavar="CSV",
                     help="host only: print per-kernel counter averages (and MFMA busy fraction) from "
                          "rocprofv3 counter-collection CSVs and exit")
@@ -265,6 +304,9 @@ def main():
         print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 5}))
         return
     moe.lib()
+    if args.peaks:
+        print(json.dumps(measure_peaks(moe, torch)))
+        return
     cfg = synth.config(args.config)
     t0 = time.perf_counter()
     inputs = synth.make_inputs(cfg)
@@ -388,6 +430,13 @@ def main():
         roof = {"bound": "mfma", "achieved": achieved, "peak": mfma_peak,
                 "unit": "TFLOP/s", "frac": achieved / mfma_peak, **common}
 
+    # the box's achievable peaks beside the published ones the fraction uses
+    peaks = measure_peaks(moe, torch)
+    # (the GEMM's HBM traffic is almost all reads: the read ceiling)
+    roof["peak_measured"] = peaks["hbm_read_gbs"] if bound == "hbm" else \
+        peaks["mfma_fp8_tflops" if cfg.wfmt in ("fp8", "mxfp4x8") else "mfma_bf16_tflops"]
+    roof["frac_of_measured_peak"] = roof["achieved"] / roof["peak_measured"]
+
     base = None
     if args.cpu_seconds > 0:
         base = cpu_baseline(cfg, inputs, args.cpu_seconds)
@@ -418,6 +467,7 @@ def main():
         "graph_us_per_layer": graph_us,
         "stage_us": stage_us,
         "roofline": roof,
+        "peaks_measured": peaks,
         "cpu_baseline": base,
         "kernel_source_hash": src_hash,
         "input_generation_s": gen_s,

@@ -24,7 +24,9 @@ OFMT = {"f32": 0, "bf16": 1}
 
 EXPORTED = ("moe_status_str", "moe_permute_capacity", "moe_permute_workspace_bytes",
             "moe_gate_topk", "moe_router_gate_topk", "moe_router_workspace_bytes", "moe_permute", "moe_act_quant_fp8", "moe_workspace_bytes",
-            "moe_workspace_layout", "moe_forward", "moe_forward_profiled", "moe_forward_static_ws")
+            "moe_workspace_layout", "moe_forward", "moe_forward_profiled", "moe_forward_static_ws",
+            # include/moe_peaks.h: achievable-peak probes
+            "moe_peak_mfma_flops_per_launch", "moe_peak_sink_elems", "moe_peak_mfma", "moe_peak_read", "moe_peak_copy")
 STATIC_WS_BYTES = 256 << 20  # MOE_STATIC_WS_BYTES: the library's own per-GPU workspace
 NUM_STAGES = 6
 STAGES = ("gate", "permute", "act_quant", "gemm1", "gemm2", "combine")
@@ -93,6 +95,16 @@ def lib() -> ctypes.CDLL:
         L.moe_forward.argtypes = [ctypes.POINTER(MoeArgs), vp, sz, vp]
         L.moe_forward_static_ws.restype = i32
         L.moe_forward_static_ws.argtypes = [ctypes.POINTER(MoeArgs), vp]
+        L.moe_peak_mfma_flops_per_launch.restype = ctypes.c_longlong
+        L.moe_peak_mfma_flops_per_launch.argtypes = [i32, i32]
+        L.moe_peak_sink_elems.restype = i32
+        L.moe_peak_sink_elems.argtypes = []
+        L.moe_peak_read.restype = i32
+        L.moe_peak_read.argtypes = [vp, sz, vp, vp]
+        L.moe_peak_mfma.restype = i32
+        L.moe_peak_mfma.argtypes = [i32, i32, vp, vp]
+        L.moe_peak_copy.restype = i32
+        L.moe_peak_copy.argtypes = [vp, vp, sz, vp]
         L.moe_forward_profiled.restype = i32
         L.moe_forward_profiled.argtypes = [ctypes.POINTER(MoeArgs), vp, sz,
                                            ctypes.POINTER(ctypes.c_void_p), vp]
@@ -267,3 +279,40 @@ def moe_forward(hidden, logits, w1, w2, top_k, *, mode="softmax", renormalize=Tr
         workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=hidden.device)
     moe_forward_args(args, workspace, stream)
     return out, workspace
+
+
+# ------------------------------------------------------------ peak probes
+def moe_peak_mfma_flops_per_launch(fp8: bool, iters: int) -> int:
+    return lib().moe_peak_mfma_flops_per_launch(int(bool(fp8)), iters)
+
+
+def moe_peak_sink_elems() -> int:
+    return lib().moe_peak_sink_elems()
+
+
+def moe_peak_mfma(fp8: bool, iters: int, sink, stream=None):
+    """One launch of the MFMA-only probe; sink: float32 device tensor of at
+    least moe_peak_sink_elems() elements."""
+    _dev(sink)
+    if sink.dtype != torch.float32 or sink.numel() < moe_peak_sink_elems():
+        raise ValueError("sink: float32, moe_peak_sink_elems() elements")
+    _check(lib().moe_peak_mfma(int(bool(fp8)), iters, _ptr(sink), _stream(stream)), "moe_peak_mfma")
+
+
+def moe_peak_read(src, sink, stream=None):
+    """Read src once with the streaming probe; sink: int32 device tensor of at
+    least moe_peak_sink_elems() zeroed elements, XORed with per-workgroup folds."""
+    _dev(src, sink)
+    if sink.dtype != torch.int32 or sink.numel() < moe_peak_sink_elems():
+        raise ValueError("sink: int32, moe_peak_sink_elems() elements")
+    n = src.numel() * src.element_size()
+    _check(lib().moe_peak_read(_ptr(src), n, _ptr(sink), _stream(stream)), "moe_peak_read")
+
+
+def moe_peak_copy(src, dst, stream=None):
+    """dst[:] = src[:] (same byte size, 16-byte multiple) with the streaming copy probe."""
+    _dev(src, dst)
+    n = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != n:
+        raise ValueError("src and dst must have the same size in bytes")
+    _check(lib().moe_peak_copy(_ptr(src), _ptr(dst), n, _stream(stream)), "moe_peak_copy")

@@ -15,9 +15,12 @@ FAKE = 0x10000  # a 16-byte aligned non-null address; never dereferenced on thes
 
 
 def _declared():
-    src = open(os.path.join(ROOT, "include", "moe.h")).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return set(re.findall(r"\b(moe_[a-z0-9_]+)\s*\(", src))
+    names = set()
+    for h in ("moe.h", "moe_peaks.h"):
+        src = open(os.path.join(ROOT, "include", h)).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        names |= set(re.findall(r"\b(moe_[a-z0-9_]+)\s*\(", src))
+    return names
 
 
 def test_every_declared_symbol_is_exported():
@@ -26,6 +29,28 @@ def test_every_declared_symbol_is_exported():
     assert declared == set(B.EXPORTED)
     for name in declared:
         assert hasattr(L, name), name
+
+
+def test_peak_probes_validate_on_host():
+    L = moe.lib()
+    assert L.moe_peak_mfma_flops_per_launch(1, 0) == 0
+    n_cu = L.moe_peak_sink_elems() // 8
+    assert n_cu >= 1 and L.moe_peak_sink_elems() == 8 * n_cu
+    # fp8 32x32x64 and bf16 32x32x16 per instruction, 4 chains, 8 waves per CU
+    assert L.moe_peak_mfma_flops_per_launch(1, 10) == n_cu * 8 * 10 * 4 * 2 * 32 * 32 * 64
+    assert L.moe_peak_mfma_flops_per_launch(0, 10) == n_cu * 8 * 10 * 4 * 2 * 32 * 32 * 16
+    assert L.moe_peak_mfma(1, 10, None, None) == B.MOE_ERR_NULL
+    assert L.moe_peak_mfma(1, 0, FAKE, None) == B.MOE_ERR_SHAPE
+    assert L.moe_peak_mfma(2, 10, FAKE, None) == B.MOE_ERR_SHAPE
+    assert L.moe_peak_copy(None, FAKE, 16, None) == B.MOE_ERR_NULL
+    assert L.moe_peak_copy(FAKE, FAKE, 24, None) == B.MOE_ERR_SHAPE
+    assert L.moe_peak_copy(FAKE + 8, FAKE, 16, None) == B.MOE_ERR_ALIGN
+    assert L.moe_peak_copy(FAKE, FAKE, 0, None) == B.MOE_OK
+    assert L.moe_peak_read(None, 16, FAKE, None) == B.MOE_ERR_NULL
+    assert L.moe_peak_read(FAKE, 16, None, None) == B.MOE_ERR_NULL
+    assert L.moe_peak_read(FAKE, 20, FAKE, None) == B.MOE_ERR_SHAPE
+    assert L.moe_peak_read(FAKE + 4, 16, FAKE, None) == B.MOE_ERR_ALIGN
+    assert L.moe_peak_read(FAKE, 0, FAKE, None) == B.MOE_OK
 
 
 def test_status_strings():
