@@ -131,7 +131,9 @@ def measure_peaks(moe, torch) -> dict:
     include/moe_peaks.h), each timed with HIP events over three launches on
     torch's current stream: MFMA-only loops in bf16 and fp8 (TFLOP/s), a
     2 GiB streaming read and a 2 GiB streaming copy (read + write bytes),
-    GB/s."""
+    GB/s; and the per-CU staging paths of the tiled GEMMs (global -> LDS
+    copies from L2 and from HBM, LDS fragment reads), bytes per clock per
+    CU."""
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     ev = HipEvents(2)
     ev.rt.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
@@ -158,6 +160,24 @@ def measure_peaks(moe, torch) -> dict:
     out["hbm_read_gbs"] = nbytes / (ms * 1e-3) / 1e9
     ms = timed(lambda: moe.moe_peak_copy(src, dst))
     out["hbm_copy_gbs"] = 2 * nbytes / (ms * 1e-3) / 1e9
+    # per-CU staging paths of the tiled GEMMs, in bytes per clock per CU at
+    # the 2.4 GHz peak engine clock: global -> LDS copies by 4 or 8 issuing
+    # waves (8 copies in flight each) from a 1 MiB region per XCD (L2) or a
+    # 256 MiB one (HBM), and LDS fragment reads by 4 or 16 waves
+    ncu = torch.cuda.get_device_properties(0).multi_processor_count
+
+    def per_cu_clk(nb, ms_):
+        return nb / (ms_ * 1e-3) / 2.4e9 / ncu
+
+    steps = 200
+    for tag, region in (("l2", 1 << 20), ("hbm", 256 << 20)):
+        for waves in (4, 8):
+            ms = timed(lambda: moe.moe_peak_lds_copy(src, region, waves, 8, steps))
+            out[f"{tag}_to_lds_w{waves}_bytes_per_clk_cu"] = per_cu_clk(
+                moe.moe_peak_lds_copy_bytes_per_launch(waves, 8, steps), ms)
+    for waves in (4, 16):
+        ms = timed(lambda: moe.moe_peak_lds_read(waves, 2000, words))
+        out[f"lds_read_w{waves}_bytes_per_clk_cu"] = per_cu_clk(moe.moe_peak_lds_read_bytes_per_launch(waves, 2000), ms)
     ev.close()
     del src, dst, sink, words
     return out

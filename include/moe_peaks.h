@@ -17,6 +17,16 @@
  *   moe_peak_copy   a streaming device copy; it moves 2 * bytes through HBM
  *                   (read and write), a lower ceiling than reads alone.
  *
+ * and two per-CU probes of the paths the tiled expert GEMMs stage their
+ * operands through (one workgroup of 16 waves per CU):
+ *
+ *   moe_peak_lds_copy  global -> LDS copies (global_load_lds_dwordx4, 1 KB per
+ *                   instruction) issued by the first `waves` waves, one step
+ *                   of copies kept in flight across the workgroup barrier;
+ *                   from a region small enough to stay in L2, or from HBM;
+ *   moe_peak_lds_read  ds_read_b128 in the GEMMs' swizzled fragment pattern,
+ *                   sixteen reads in flight per wave.
+ *
  * Same conventions as moe.h: device pointers owned by the caller, work
  * enqueued on `stream` and never synchronised, arguments checked on the
  * host before anything is enqueued.  They are measurement tools, not part
@@ -59,6 +69,30 @@ moe_status moe_peak_read(const void* src, size_t bytes, uint32_t* sink, hipStrea
  * overlapping; bytes a multiple of 16 (0 is a no-op).  Errors: MOE_ERR_NULL,
  * MOE_ERR_SHAPE (bytes % 16), MOE_ERR_ALIGN, MOE_ERR_HIP. */
 moe_status moe_peak_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
+
+/* Bytes one moe_peak_lds_copy launch moves on this device: CUs * waves *
+ * copies * steps * 1024; 0 for arguments moe_peak_lds_copy rejects. */
+long long moe_peak_lds_copy_bytes_per_launch(int waves, int copies, int steps);
+
+/* Workgroup b (one per CU) copies from region b % 8 of src: src must hold
+ * 8 * region_bytes readable bytes, 16-byte aligned; region_bytes a power of
+ * two in [64 KiB, 256 MiB].  With round-robin dispatch the workgroups of one
+ * XCD share a region, so 1 MiB stays in that XCD's L2 and 256 MiB streams
+ * from HBM.  waves in [1, 16] issue copies, copies (4, 8 or 16) per wave per
+ * step, steps >= 1.  Nothing is written outside the workgroup's LDS.
+ * Errors: MOE_ERR_NULL, MOE_ERR_SHAPE, MOE_ERR_ALIGN, MOE_ERR_HIP. */
+moe_status moe_peak_lds_copy(const void* src, size_t region_bytes, int waves, int copies, int steps,
+                             hipStream_t stream);
+
+/* Bytes one moe_peak_lds_read launch reads from LDS on this device: CUs *
+ * waves * 64 lanes * 16 bytes * 16 reads * iters; 0 for rejected arguments. */
+long long moe_peak_lds_read_bytes_per_launch(int waves, int iters);
+
+/* waves in [1, 16] per CU, iters >= 1 rounds of sixteen reads per wave.
+ * sink: device, at least moe_peak_sink_elems() words; word b is written by
+ * workgroup b (a fold of the values read; meaningless).
+ * Errors: MOE_ERR_NULL, MOE_ERR_SHAPE, MOE_ERR_HIP. */
+moe_status moe_peak_lds_read(int waves, int iters, uint32_t* sink, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -12,4 +12,5 @@ from ._binding import (  # noqa: F401
     moe_router_gate_topk,
     moe_permute_workspace_bytes, moe_workspace_bytes, moe_workspace_layout,
     moe_peak_copy, moe_peak_mfma, moe_peak_mfma_flops_per_launch, moe_peak_read, moe_peak_sink_elems,
+    moe_peak_lds_copy, moe_peak_lds_copy_bytes_per_launch, moe_peak_lds_read, moe_peak_lds_read_bytes_per_launch,
 )

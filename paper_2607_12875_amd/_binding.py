@@ -26,7 +26,9 @@ EXPORTED = ("moe_status_str", "moe_permute_capacity", "moe_permute_workspace_byt
             "moe_gate_topk", "moe_router_gate_topk", "moe_router_workspace_bytes", "moe_permute", "moe_act_quant_fp8", "moe_workspace_bytes",
             "moe_workspace_layout", "moe_forward", "moe_forward_profiled", "moe_forward_static_ws",
             # include/moe_peaks.h: achievable-peak probes
-            "moe_peak_mfma_flops_per_launch", "moe_peak_sink_elems", "moe_peak_mfma", "moe_peak_read", "moe_peak_copy")
+            "moe_peak_mfma_flops_per_launch", "moe_peak_sink_elems", "moe_peak_mfma", "moe_peak_read", "moe_peak_copy",
+            "moe_peak_lds_copy_bytes_per_launch", "moe_peak_lds_copy", "moe_peak_lds_read_bytes_per_launch",
+            "moe_peak_lds_read")
 STATIC_WS_BYTES = 256 << 20  # MOE_STATIC_WS_BYTES: the library's own per-GPU workspace
 NUM_STAGES = 6
 STAGES = ("gate", "permute", "act_quant", "gemm1", "gemm2", "combine")
@@ -105,6 +107,14 @@ def lib() -> ctypes.CDLL:
         L.moe_peak_mfma.argtypes = [i32, i32, vp, vp]
         L.moe_peak_copy.restype = i32
         L.moe_peak_copy.argtypes = [vp, vp, sz, vp]
+        L.moe_peak_lds_copy_bytes_per_launch.restype = ctypes.c_longlong
+        L.moe_peak_lds_copy_bytes_per_launch.argtypes = [i32, i32, i32]
+        L.moe_peak_lds_copy.restype = i32
+        L.moe_peak_lds_copy.argtypes = [vp, sz, i32, i32, i32, vp]
+        L.moe_peak_lds_read_bytes_per_launch.restype = ctypes.c_longlong
+        L.moe_peak_lds_read_bytes_per_launch.argtypes = [i32, i32]
+        L.moe_peak_lds_read.restype = i32
+        L.moe_peak_lds_read.argtypes = [i32, i32, vp, vp]
         L.moe_forward_profiled.restype = i32
         L.moe_forward_profiled.argtypes = [ctypes.POINTER(MoeArgs), vp, sz,
                                            ctypes.POINTER(ctypes.c_void_p), vp]
@@ -316,3 +326,30 @@ def moe_peak_copy(src, dst, stream=None):
     if dst.numel() * dst.element_size() != n:
         raise ValueError("src and dst must have the same size in bytes")
     _check(lib().moe_peak_copy(_ptr(src), _ptr(dst), n, _stream(stream)), "moe_peak_copy")
+
+
+def moe_peak_lds_copy_bytes_per_launch(waves: int, copies: int, steps: int) -> int:
+    return lib().moe_peak_lds_copy_bytes_per_launch(waves, copies, steps)
+
+
+def moe_peak_lds_copy(src, region_bytes: int, waves: int, copies: int, steps: int, stream=None):
+    """One launch of the global -> LDS copy probe over region b % 8 of src per
+    workgroup b; src must hold 8 * region_bytes bytes."""
+    _dev(src)
+    if src.numel() * src.element_size() < 8 * region_bytes:
+        raise ValueError("src must hold 8 * region_bytes bytes")
+    _check(lib().moe_peak_lds_copy(_ptr(src), region_bytes, waves, copies, steps, _stream(stream)),
+           "moe_peak_lds_copy")
+
+
+def moe_peak_lds_read_bytes_per_launch(waves: int, iters: int) -> int:
+    return lib().moe_peak_lds_read_bytes_per_launch(waves, iters)
+
+
+def moe_peak_lds_read(waves: int, iters: int, sink, stream=None):
+    """One launch of the LDS fragment-read probe; sink: int32 device tensor of
+    at least moe_peak_sink_elems() elements."""
+    _dev(sink)
+    if sink.dtype != torch.int32 or sink.numel() < moe_peak_sink_elems():
+        raise ValueError("sink: int32, moe_peak_sink_elems() elements")
+    _check(lib().moe_peak_lds_read(waves, iters, _ptr(sink), _stream(stream)), "moe_peak_lds_read")

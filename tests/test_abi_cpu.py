@@ -51,6 +51,25 @@ def test_peak_probes_validate_on_host():
     assert L.moe_peak_read(FAKE, 20, FAKE, None) == B.MOE_ERR_SHAPE
     assert L.moe_peak_read(FAKE + 4, 16, FAKE, None) == B.MOE_ERR_ALIGN
     assert L.moe_peak_read(FAKE, 0, FAKE, None) == B.MOE_OK
+    # global -> LDS copy and LDS read probes: 1 KB per copy, 16 x 16 B per lane per read round
+    assert L.moe_peak_lds_copy_bytes_per_launch(4, 8, 10) == n_cu * 4 * 8 * 10 * 1024
+    assert L.moe_peak_lds_copy_bytes_per_launch(17, 8, 10) == 0
+    assert L.moe_peak_lds_copy_bytes_per_launch(4, 6, 10) == 0
+    assert L.moe_peak_lds_read_bytes_per_launch(4, 10) == n_cu * 4 * 64 * 16 * 16 * 10
+    assert L.moe_peak_lds_read_bytes_per_launch(0, 10) == 0
+    mib = 1 << 20
+    assert L.moe_peak_lds_copy(None, mib, 4, 8, 1, None) == B.MOE_ERR_NULL
+    assert L.moe_peak_lds_copy(FAKE, mib, 0, 8, 1, None) == B.MOE_ERR_SHAPE
+    assert L.moe_peak_lds_copy(FAKE, mib, 17, 8, 1, None) == B.MOE_ERR_SHAPE
+    assert L.moe_peak_lds_copy(FAKE, mib, 4, 5, 1, None) == B.MOE_ERR_SHAPE
+    assert L.moe_peak_lds_copy(FAKE, mib, 4, 8, 0, None) == B.MOE_ERR_SHAPE
+    assert L.moe_peak_lds_copy(FAKE, 3 * mib, 4, 8, 1, None) == B.MOE_ERR_SHAPE  # not a power of two
+    assert L.moe_peak_lds_copy(FAKE, 32 << 10, 4, 8, 1, None) == B.MOE_ERR_SHAPE  # below 64 KiB
+    assert L.moe_peak_lds_copy(FAKE, 512 * mib, 4, 8, 1, None) == B.MOE_ERR_SHAPE  # above 256 MiB
+    assert L.moe_peak_lds_copy(FAKE + 8, mib, 4, 8, 1, None) == B.MOE_ERR_ALIGN
+    assert L.moe_peak_lds_read(4, 10, None, None) == B.MOE_ERR_NULL
+    assert L.moe_peak_lds_read(0, 10, FAKE, None) == B.MOE_ERR_SHAPE
+    assert L.moe_peak_lds_read(4, 0, FAKE, None) == B.MOE_ERR_SHAPE
 
 
 def test_status_strings():

@@ -1,8 +1,9 @@
 """The achievable-peak probes (include/moe_peaks.h) on the GPU: the copy
-reproduces its source byte for byte, the read touches every word, and the
-MFMA-only loops, the read and the copy
-reach plausible fractions of MI355X's published peaks (they are the
-denominators bench.py reports beside those peaks)."""
+reproduces its source byte for byte, the read touches every word, the
+MFMA-only loops, the read and the copy reach plausible fractions of
+MI355X's published peaks (they are the denominators bench.py reports beside
+those peaks), and the per-CU staging probes (global -> LDS copies, LDS
+fragment reads) report rates in a plausible range."""
 import pytest
 import torch
 
@@ -47,3 +48,13 @@ def test_measured_peaks_are_plausible():
     assert 0.3 * 5000 < p["mfma_fp8_tflops"] < 1.05 * 5000
     assert 0.3 * 8000 < p["hbm_read_gbs"] < 1.05 * 8000
     assert 0.3 * 8000 < p["hbm_copy_gbs"] < 1.05 * 8000
+    # per-CU staging paths, bytes per clock per CU at 2.4 GHz (measured on
+    # MI355X: about 35 / 55 from L2 with 4 / 8 copy waves, 10-12 from HBM
+    # with either, LDS reads about 160 / 240 with 4 / 16 waves); the bounds
+    # only catch a probe that stopped measuring what it names
+    for w in (4, 8):
+        assert 8 < p[f"l2_to_lds_w{w}_bytes_per_clk_cu"] < 128
+        assert 3 < p[f"hbm_to_lds_w{w}_bytes_per_clk_cu"] < 20
+    assert p["l2_to_lds_w8_bytes_per_clk_cu"] > p["hbm_to_lds_w8_bytes_per_clk_cu"]
+    for w in (4, 16):
+        assert 60 < p[f"lds_read_w{w}_bytes_per_clk_cu"] < 520
