@@ -200,6 +200,8 @@ __global__ __launch_bounds__(256) void router_partial_kernel(const uint16_t* __r
 
 // One wave per token: logits = the KS partials summed in slice order (fp32),
 // written out if asked, then the gate's selection and weights on them.
+constexpr int kRouterMaxKS = 32;  // most K slices of the split router
+
 template <int EPL>
 __global__ __launch_bounds__(256) void router_select_kernel(const float* __restrict__ part, int KS, int T, int E,
                                                             int k, int mode, int renorm, float scale,
@@ -219,16 +221,16 @@ __global__ __launch_bounds__(256) void router_select_kernel(const float* __restr
   for (int i = 0; i < EPL; ++i) {
     const int e = lane + 64 * i;
     if (e >= E) continue;
-    // the slices' partials are requested eight at a time, then added in slice order
+    // every slice's partial is requested before the first is added (one
+    // memory round trip; slots past KS re-read the last slice, so there is no
+    // branch between the loads), then they are added in slice order (adding
+    // +0 for the slots past KS leaves v unchanged: v is never -0)
+    float x[kRouterMaxKS];
+#pragma unroll
+    for (int j = 0; j < kRouterMaxKS; ++j) x[j] = part[(static_cast<size_t>(min(j, KS - 1)) * T + t) * E + e];
     float v = 0.f;
-    for (int q0 = 0; q0 < KS; q0 += 8) {
-      float x[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) x[j] = q0 + j < KS ? part[(static_cast<size_t>(q0 + j) * T + t) * E + e] : 0.f;
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        if (q0 + j < KS) v += x[j];
-    }
+    for (int j = 0; j < kRouterMaxKS; ++j) v += j < KS ? x[j] : 0.f;
     lg[wv][e] = v;  // read back below by this same lane only
     if (logits_out) logits_out[static_cast<size_t>(t) * E + e] = v;
   }
@@ -248,7 +250,7 @@ constexpr int kRouterSplitMaxT = 64;  // the two-launch form up to this many tok
 int router_ks(int T, int H, int E) {
   const long tiles = static_cast<long>((T + 15) / 16) * ((E + 63) / 64);
   int ks = 1;
-  while (ks < 32 && tiles * ks < 256 && H % (64 * ks) == 0 && H / (2 * ks) >= 128) ks *= 2;
+  while (ks < kRouterMaxKS && tiles * ks < 256 && H % (64 * ks) == 0 && H / (2 * ks) >= 128) ks *= 2;
   return ks;
 }
 }  // namespace
