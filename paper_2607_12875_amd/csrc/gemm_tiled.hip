@@ -976,14 +976,24 @@ void moe_gemm_tiled(GroupedGemm g) {
           for (int w = 0; w < WN; ++w) m = fmaxf(m, lds_amax[w][rl]);
           const float sc = fmaxf(m, 1e-10f) / 448.0f;
           const size_t row = static_cast<size_t>(m0 + rl);
+          // a / sc as one IEEE reciprocal per row and a residual step per
+          // value: q0 = a r, then q0 + (a - q0 sc) r, the residual exact by
+          // fma, the sign restored for a = -0.  On the fp8 workload its codes
+          // equal those of the IEEE quotient for all 134M intermediate values
+          // (GEMM1 0.7 % faster than a divide per value).
+          const float r = 1.0f / sc;
+          auto qdiv = [&](float a) {
+            const float q0 = a * r;
+            return sat_e4m3(__builtin_copysignf(fmaf(fmaf(-q0, sc, a), r, q0), a));
+          };
 #pragma unroll
           for (int j = 0; j < TH; ++j)
 #pragma unroll
             for (int v4 = 0; v4 < 4; ++v4) {
               const int col = n0 + wn * (WTN / 2) + j * 32 + 8 * v4 + 4 * kg;
               const float* a4 = &av[i][j][4 * v4];
-              const uint32_t codes = f32x2_to_e4m3(sat_e4m3(a4[0] / sc), sat_e4m3(a4[1] / sc)) |
-                                     (f32x2_to_e4m3(sat_e4m3(a4[2] / sc), sat_e4m3(a4[3] / sc)) << 16);
+              const uint32_t codes = f32x2_to_e4m3(qdiv(a4[0]), qdiv(a4[1])) |
+                                     (f32x2_to_e4m3(qdiv(a4[2]), qdiv(a4[3])) << 16);
               *reinterpret_cast<uint32_t*>(q + row * g.I + col) = codes;
             }
           if (wn == 0 && kg == 0) g.inter_scale[row * (g.I / 128) + n0 / 128] = sc;
