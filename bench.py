@@ -291,7 +291,7 @@ def main():
                     help="host only: print the GEMM1 HBM-traffic record from rocprofv3 counter CSVs "
                          "(the copy ones from --copy-calibration 1024) and exit")
     ap.add_argument("--peaks", action="store_true",
-                    help="only measure the box's achievable MFMA and copy peaks, print them, and exit")
+                    help="only measure the device's achievable MFMA and memory peaks, print them, and exit")
     ap.add_argument("--counter-summary", nargs="+", metavar="CSV",
                     help="host only: print per-kernel counter averages (and MFMA busy fraction) from "
                          "rocprofv3 counter-collection CSVs and exit")
@@ -450,7 +450,7 @@ def main():
         roof = {"bound": "mfma", "achieved": achieved, "peak": mfma_peak,
                 "unit": "TFLOP/s", "frac": achieved / mfma_peak, **common}
 
-    # the box's achievable peaks beside the published ones the fraction uses
+    # the device's achievable peaks beside the published ones the fraction uses
     peaks = measure_peaks(moe, torch)
     # (the GEMM's HBM traffic is almost all reads: the read ceiling)
     roof["peak_measured"] = peaks["hbm_read_gbs"] if bound == "hbm" else \

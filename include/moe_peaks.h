@@ -3,7 +3,7 @@
  *
  * The layer's performance is reported as a fraction of MI355X's published
  * peaks (dense bf16 2.5 PFLOP/s, dense fp8 5.0 PFLOP/s, HBM 8 TB/s).  These
- * probes measure what the box actually reaches, so a fraction can also be
+ * probes measure what the device actually reaches, so a fraction can also be
  * read against the achievable ceiling:
  *
  *   moe_peak_mfma   every CU runs eight waves of MFMA-only work (four

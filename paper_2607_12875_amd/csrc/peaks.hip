@@ -2,7 +2,7 @@
 // (bf16 32x32x16 or fp8 32x32x64, register operands, no memory traffic in the
 // loop), a streaming read and a streaming copy; and two per-CU probes of the
 // paths the tiled GEMMs stage their operands through (global -> LDS copies,
-// LDS fragment reads).  The bench reports what they reach on the box beside
+// LDS fragment reads).  The bench reports what they reach on the device beside
 // the published peaks its fractions are priced against.  Every probe
 // computes its addresses outside the timed loop or with a few 32-bit
 // operations, so it times the memory path rather than its own arithmetic.
