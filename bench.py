@@ -63,6 +63,8 @@ DESCR = {
        "scales per 32, bf16 activations, sigmoid+bias top-8 x2.5",
     9: "MXFP4 x MXFP8 prefill MoE layer: T=8192 H=7168 E=256 I=2048 top_k=8, OCP MX E2M1 weights and "
        "in-layer MXFP8 (e4m3, E8M0 per 32) activations, sigmoid+bias top-8 x2.5",
+    10: "int4 decode MoE layer: T=16 H=4096 E=128 I=1536 top_k=8, int4 g128 weights, "
+        "Zipf(1.1)-skewed softmax top-8",
 }
 
 

@@ -82,7 +82,9 @@ typedef enum {
      value = q * scale.  Hidden rows enter as bf16 and the SwiGLU
      intermediate is rounded to bf16.  The first product sums each 128-group
      of codes exactly and applies the group's scale in fp32; the second
-     rounds q * scale to bf16 before its products.  A scale may be zero;
+     rounds q * scale to bf16 before its products, except at decode sizes
+     (T * top_k <= 8 * E, H and I in {512, 1024, 1536, 2048, 3072, 4096}),
+     where both products take the first one's exact form.  A scale may be zero;
      the nonzero scales must be normal numbers within a factor 2^64 of each
      other along a weight row (other scales are unspecified): the first
      product carries its running sums divided by the current group's scale,
@@ -249,7 +251,8 @@ typedef struct moe_ws_layout {
   int64_t act_q, act_s;              /* fp8: uint8 [T,H], fp32 [T,H/128]; MXFP8:
                                         uint8 [T,H] e4m3, uint8 [T,H/32] E8M0;
                                         int4: act_s = fp32 [T,H/128] group sums
-                                        of the hidden rows (times -136)       */
+                                        of the hidden rows (times -136), not
+                                        written at the decode sizes above     */
   int64_t inter, inter_s;            /* bf16 [cap,I] (fp8: uint8 [cap,I], fp32 [cap,I/128];
                                         MXFP8: uint8 [cap,I], uint8 [cap,I/32] E8M0) */
   int64_t y;                         /* [cap,H] rows in sorted order: bf16 for

@@ -149,6 +149,22 @@ __device__ __forceinline__ bf16x8 e4m3x8_to_bf16(uint32_t lo, uint32_t hi) {
   return r;
 }
 
+// 8 signed nibbles (element k of the word in bits [4k, 4k+4)) -> 8 bf16
+// values 136 + q, exact: bits 0x4300 | (q + 8), i.e. 128 + (q + 8) with the
+// nibble in the low mantissa bits of 128, and q + 8 = n ^ 8 for the two's-
+// complement nibble n.  In the order two operations per dword give: dword d
+// takes nibbles d and d + 4 (bf16 slots 2d, 2d + 1), so slot s holds element
+// {0,4,1,5,2,6,3,7}[s] of the word.  Each half is (n & 0xF) ^ 0x4308: v_bitop3
+// with the truth table of (S0 & S1) ^ S2 over (0xF0, 0xCC, 0xAA), 0x6A.
+__device__ __forceinline__ bf16x8 int4x8_biased_bf16_strided(uint32_t w) {
+  u32x4 r;
+  r.x = __builtin_amdgcn_bitop3_b32(w, 0x000F000Fu, 0x43084308u, 0x6A);
+  r.y = __builtin_amdgcn_bitop3_b32(w >> 4, 0x000F000Fu, 0x43084308u, 0x6A);
+  r.z = __builtin_amdgcn_bitop3_b32(w >> 8, 0x000F000Fu, 0x43084308u, 0x6A);
+  r.w = __builtin_amdgcn_bitop3_b32(w >> 12, 0x000F000Fu, 0x43084308u, 0x6A);
+  return as_bf16x8(r);
+}
+
 // ------------------------------------------------------ streamed (decode)
 #ifndef MOE_STREAM_NS
 #define MOE_STREAM_NS 4
@@ -184,19 +200,28 @@ __device__ __forceinline__ bf16x8 e4m3x8_to_bf16(uint32_t lo, uint32_t hi) {
 // the weights; inside a 128-wide block lane group kg takes bytes
 // [32 kg, 32 kg + 32), the four MFMAs of the block decode them exactly to
 // bf16 (the activation fragments use the same K order), and the block's
-// partial is scaled into the accumulator.
+// partial is scaled into the accumulator.  FMT 2: int4 weights (eight
+// signed nibbles per word along K) with a bf16 scale per row and 128-wide K
+// group: the stage also copies each of its 16 rows' group scales for the
+// piece (whole dwords), the codes enter the MFMA exactly as bf16 136 + q (the
+// activation fragments permuted once per run to the decode's element
+// order), each group's partial starts from the row's -136 * (sum of its
+// activations over the group), formed once per run by the MFMA itself, and
+// the lane's weight row scale multiplies it into the accumulator.
 // NG: 16-row weight groups per block (GEMM1: NG/2 gate + NG/2 up); NP
 // pieces of JP MFMAs (32 K elements each) per row and wave: K = 4 * 32 * NP * JP.
 
 template <int FMT, int NWV, int NG, int NP, int JP, bool GEMM1>
 __global__ __launch_bounds__(64 * NWV) void gemm_bf16_stream(GroupedGemm g) {
-  constexpr bool F8 = FMT == 3, F4 = FMT == 4;
-  constexpr int B32 = F8 ? 32 : (F4 ? 16 : 64);     // weight bytes per 32 elements
+  constexpr bool F8 = FMT == 3, F4 = FMT == 4, I4 = FMT == 2;
+  constexpr bool BLK = F8 || F4 || I4;              // K taken in 128-wide blocks
+  constexpr int B32 = F8 ? 32 : ((F4 || I4) ? 16 : 64);  // weight bytes per 32 elements
   constexpr int PC = B32 * JP, ROWB = PC + 16;      // piece bytes, LDS row stride
-  constexpr int NSI = F4 ? (JP + 15) / 16 : (F8 ? 1 : 0);  // scale copy instructions per stage
-  constexpr int STAGE = 16 * ROWB + (F8 ? 64 : 0) + (F4 ? ((16 * JP + 15) / 16) * 16 : 0);
+  constexpr int NSI = F4 ? (JP + 15) / 16 : ((F8 || I4) ? 1 : 0);  // scale copy instructions per stage
+  constexpr int STAGE = 16 * ROWB + (F8 ? 64 : 0) + (F4 ? ((16 * JP + 15) / 16) * 16 : 0) + (I4 ? 8 * JP : 0);
   constexpr int CPS = 16 + NSI;                     // copy instructions per stage
-  static_assert(!(F8 || F4) || JP % 4 == 0, "pieces are whole 128-wide blocks");
+  static_assert(!BLK || JP % 4 == 0, "pieces are whole 128-wide blocks");
+  static_assert(!I4 || (JP % 8 == 0 && JP <= 32), "int4: a row's group scales of a piece are whole dwords, one copy");
   // stage buffers per wave: as many as LDS holds beside the reduction, up to MOE_STREAM_NS
   constexpr int RED = (NWV - 1) * NG * 1024;  // bytes of the reduction buffer
   constexpr int NSO = (160 * 1024 / MOE_STREAM_OCC - RED) / (NWV * STAGE);
@@ -248,11 +273,30 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_stream(GroupedGemm g) {
     u32x4 a[NJ];
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
-      a[j] = ld16(arow + ((F8 || F4) ? 128 * (j / 4) + 32 * kg + 8 * (j % 4) : 32 * j + 8 * kg));
+      a[j] = ld16(arow + (BLK ? 128 * (j / 4) + 32 * kg + 8 * (j % 4) : 32 * j + 8 * kg));
     bool live[4];  // GEMM2: rows m0 + 4 kg + i that are routed rows (pads are never read)
 #pragma unroll
     for (int i = 0; i < 4; ++i) live[i] = GEMM1 || g.sorted_ids[m0 + 4 * kg + i] < g.n_routed;
     vm_wait<0>();
+    // int4: each fragment's elements put in the order the weight decode
+    // gives (int4x8_biased_bf16_strided), and nbias[b] = -136 * (each row's
+    // sum over the quarter's 128-group b), the start of that group's partial
+    f32x4 nbias[I4 ? NJ / 4 : 1];
+    if constexpr (I4) {
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const u32x4 v = a[j];
+        a[j] = u32x4{__builtin_amdgcn_perm(v.z, v.x, 0x05040100u), __builtin_amdgcn_perm(v.z, v.x, 0x07060302u),
+                     __builtin_amdgcn_perm(v.w, v.y, 0x05040100u), __builtin_amdgcn_perm(v.w, v.y, 0x07060302u)};
+      }
+      const u32x4 c = {0xC308C308u, 0xC308C308u, 0xC308C308u, 0xC308C308u};  // bf16 -136
+#pragma unroll
+      for (int b = 0; b < NJ / 4; ++b) {
+        nbias[b] = f32x4{};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) nbias[b] = mfma16x16x32(as_bf16x8(a[4 * b + u]), as_bf16x8(c), nbias[b]);
+      }
+    }
 
     const int NR = GEMM1 ? 2 * g.I : g.H;  // weight rows per expert
     const uint8_t* wq = static_cast<const uint8_t*>(GEMM1 ? g.w1 : g.w2) + static_cast<size_t>(e) * NR * rowbytes +
@@ -265,6 +309,10 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_stream(GroupedGemm g) {
     const uint8_t* wsc4 = F4 ? static_cast<const uint8_t*>(GEMM1 ? g.w1_scale : g.w2_scale) +
                                    static_cast<size_t>(e) * NR * (K / 32) + k0 / 32
                              : nullptr;
+    // int4: the expert's bf16 group scales [NR][K/128], at this wave's first group
+    const uint16_t* wsc2 = I4 ? static_cast<const uint16_t*>(GEMM1 ? g.w1_scale : g.w2_scale) +
+                                    static_cast<size_t>(e) * NR * (K / 128) + k0 / 128
+                              : nullptr;
     const int nsg = (cb1 - cb0) * NST;  // stages of this run
     // stage q of the run: block cb0 + q / NST, group gi, piece p
     auto issue = [&](int q) {
@@ -287,6 +335,12 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_stream(GroupedGemm g) {
           if (row < 16)
             dma4(wsc4 + static_cast<size_t>(wr + row) * (K / 32) + p * JP + 4 * dw, dst + 16 * ROWB + 256 * c);
         }
+      }
+      if constexpr (I4) {  // the piece's JP / 4 group scales of each of the 16 rows, [row][JP / 4] in LDS
+        constexpr int DW = JP / 8;  // dwords per row
+        if (lane < 16 * DW)
+          dma4(wsc2 + static_cast<size_t>(wr + lane / DW) * (K / 128) + p * (JP / 4) + 2 * (lane % DW),
+               dst + 16 * ROWB);
       }
     };
 #pragma unroll
@@ -320,6 +374,21 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_stream(GroupedGemm g) {
               const uint32_t w = u == 0 ? wv.x : (u == 1 ? wv.y : (u == 2 ? wv.z : wv.w));
               acc[gi] = mfma16x16x32(as_bf16x8(a[p * JP + 4 * b + u]), as_bf16x8(mxfp4x8_to_bf16(w, scf)), acc[gi]);
             }
+          }
+        } else if constexpr (I4) {
+          const uint8_t* B = St + r16 * ROWB + 16 * kg;
+          const uint16_t* sc = reinterpret_cast<const uint16_t*>(St + 16 * ROWB) + r16 * (JP / 4);
+#pragma unroll
+          for (int b = 0; b < JP / 4; ++b) {
+            const u32x4 wv = ld16(B + 64 * b);
+            f32x4 part = nbias[(p * JP) / 4 + b];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const uint32_t w = u == 0 ? wv.x : (u == 1 ? wv.y : (u == 2 ? wv.z : wv.w));
+              part = mfma16x16x32(as_bf16x8(a[p * JP + 4 * b + u]), int4x8_biased_bf16_strided(w), part);
+            }
+            const float sw = __uint_as_float(static_cast<uint32_t>(sc[b]) << 16);  // this lane's weight row
+            acc[gi] += part * sw;
           }
         } else if constexpr (F8) {
           const uint8_t* B = St + r16 * ROWB + 32 * kg;
@@ -799,6 +868,47 @@ hipError_t launch_stream_f4(const GroupedGemm& g, hipStream_t s) {
 }
 bool stream_fits_f4(int K, int N, int nc) {
   return MOE_STREAM && K % 512 == 0 && K <= 7168 && (K <= 4096 || K % 1024 == 0) && N % nc == 0;
+}
+
+// int4 weights (half a byte per element, a bf16 scale per 128-wide group):
+// one piece per wave and row, whose group scales must be whole dwords (JP a
+// multiple of 8): two waves (K in halves, two workgroups per CU) up to
+// K = 2048, four waves for K = 3072 and 4096.
+template <int NG, bool GEMM1>
+hipError_t launch_stream_i4(const GroupedGemm& g, hipStream_t s) {
+  constexpr int NC = GEMM1 ? NG / 2 * 16 : NG * 16;
+  const int K = GEMM1 ? g.H : g.I;
+  const long units = static_cast<long>(g.max_rows / 16) * ((GEMM1 ? g.I : g.H) / NC);
+#define MOE_STREAM_CASE(NWV, JP, GRID) \
+  hipLaunchKernelGGL((gemm_bf16_stream<2, NWV, NG, 1, JP, GEMM1>), GRID, dim3(64 * NWV), 0, s, g)
+  if (K <= 2048) {
+    const dim3 grid2(static_cast<unsigned>(std::max(1L, std::min<long>(2L * stream_grid(), units))));
+    switch (K / 512) {
+      case 1: MOE_STREAM_CASE(2, 8, grid2); break;
+      case 2: MOE_STREAM_CASE(2, 16, grid2); break;
+      case 3: MOE_STREAM_CASE(2, 24, grid2); break;
+      default: MOE_STREAM_CASE(2, 32, grid2); break;
+    }
+  } else {
+    const dim3 grid(static_cast<unsigned>(std::max(1L, std::min<long>(stream_grid(), units))));
+    if (K == 3072) MOE_STREAM_CASE(4, 24, grid);
+    else MOE_STREAM_CASE(4, 32, grid);
+  }
+#undef MOE_STREAM_CASE
+  return hipGetLastError();
+}
+bool stream_fits_i4(int K, int N, int nc) {
+  return MOE_STREAM && K % 512 == 0 && (K <= 2048 || K == 3072 || K == 4096) && N % nc == 0;
+}
+// Both int4 products fit the streamed kernel (the 16-row decode route)
+bool int4_stream_fits(int H, int I) {
+  return stream_fits_i4(H, I, MOE_STREAM_NG1 / 2 * 16) && stream_fits_i4(I, H, MOE_STREAM_NG2 * 16);
+}
+hipError_t launch_gemm1_int4_stream(const GroupedGemm& g, hipStream_t s) {
+  return launch_stream_i4<MOE_STREAM_NG1, true>(g, s);
+}
+hipError_t launch_gemm2_int4_stream(const GroupedGemm& g, hipStream_t s) {
+  return launch_stream_i4<MOE_STREAM_NG2, false>(g, s);
 }
 
 // Streamed when each wave's quarter of a row is whole 512-byte pieces (K a

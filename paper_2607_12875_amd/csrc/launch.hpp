@@ -65,6 +65,8 @@ __host__ __device__ constexpr bool y_is_f32(int wfmt) { return wfmt != 1 && wfmt
 
 // Row tile (padding granule) the kernels for this format/shape use.
 int gemm_block_m(int wfmt, int T, int top_k, int E, int H, int I);
+// int4 weights on the 16-row streamed kernels, which need no group sums of x
+bool int4_decode(int T, int top_k, int E, int H, int I);
 int bf16_tiled_block_m();
 hipError_t launch_gemm1_bf16_tiled(const GroupedGemm& g, hipStream_t s);
 hipError_t launch_gemm2_bf16_tiled(const GroupedGemm& g, hipStream_t s);

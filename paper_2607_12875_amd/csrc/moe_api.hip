@@ -278,7 +278,7 @@ moe_status run_layer(const moe_args* a, void* ws, size_t ws_bytes, hipEvent_t* e
   g.x_mx = nullptr;
   g.x_gsum = nullptr;
   if (!mark(2)) return MOE_ERR_HIP;
-  if (a->wfmt == MOE_W_INT4_G128) {
+  if (a->wfmt == MOE_W_INT4_G128 && !moe::int4_decode(a->T, a->top_k, a->E, a->H, a->I)) {
     float* gs = at<float>(ws, L.act_s);
     if (moe::launch_group_sum(a->hidden, a->T, a->H, gs, stream) != hipSuccess) return MOE_ERR_HIP;
     g.x_gsum = gs;

@@ -12,7 +12,7 @@ The layer is the MoE Gate -> Fused MoE -> Weight Sum skeleton of the paper
 semantics explicitly (e4m3 format, scale granularity, zero points, layout),
 as Sec. 6.2 and the "FP8 representation" row of Table 3 require.
 
-Value recipe (the five workloads, plus a decode step on fp8 weights):
+Value recipe (the five workloads and their decode / format variants):
   * hidden  ~ N(0, 1) drawn in fp32, stored as bf16 (round-to-nearest-even).
   * logits  ~ N(0, 1) fp32, plus an optional per-expert bias:
       - "normal:<std>"  b_e ~ N(0, std^2), added to the logits (uneven loads);
@@ -108,6 +108,9 @@ CONFIGS = {
     # products on the block-scaled fp8 x fp4 matrix instruction
     9: MoeConfig("mxfp4x8-prefill", T=8192, H=7168, E=256, I=2048, top_k=8, wfmt="mxfp4x8",
                  mode="sigmoid", routed_scale=2.5, sel_bias_std=0.1, seed=8),
+    # one decode step of workload 5's layer (int4 weights, Zipf-skewed routing)
+    10: MoeConfig("int4-decode", T=16, H=4096, E=128, I=1536, top_k=8, wfmt="int4",
+                  logit_bias="zipf:1.1", seed=10),
 }
 
 

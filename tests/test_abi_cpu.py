@@ -188,6 +188,22 @@ def test_workspace_layout_is_consistent():
             assert L["block_m"] == (16 if T * k <= 32 * E else 128)
 
 
+def test_int4_route_choice():
+    # int4 takes the 16-row streamed kernels up to 8 routed rows per expert on
+    # average when H and I are both K sizes they take (512..2048 in steps of
+    # 512, 3072, 4096), the 64-row tiled kernels otherwise
+    cases = [((16, 4096, 128, 1536, 8), 16), ((128, 4096, 128, 1536, 8), 16),
+             ((129, 4096, 128, 1536, 8), 64), ((512, 4096, 128, 1536, 8), 64),
+             ((4, 512, 8, 3072, 2), 16), ((4, 2048, 8, 512, 2), 16),
+             ((4, 2560, 8, 512, 2), 64), ((4, 7168, 8, 2048, 2), 64),
+             ((4, 1024, 8, 384, 2), 64), ((4, 384, 8, 1024, 2), 64)]
+    for (T, H, E, I, k), bm in cases:
+        a = B.make_args(T, H, E, I, k, wfmt="int4")
+        L = moe.moe_workspace_layout(a)
+        assert L["block_m"] == bm, (T, H, E, I, k, L["block_m"])
+        assert L["act_s"] >= 0 and L["cap"] == T * k + E * (bm - 1)
+
+
 def test_static_workspace_entry_point_validation():
     L = moe.lib()
     st = lambda a: L.moe_forward_static_ws(ctypes.byref(a), None)  # noqa: E731

@@ -239,6 +239,62 @@ def test_int4_zero_and_wide_scales(dev):
     _check(cfg, inp=out)
 
 
+# ---- int4 decode route: the 16-row streamed kernels up to 8 routed rows per
+# expert on average; both products sum each 128-group of codes exactly and
+# apply the row's group scale to the group's partial in fp32
+def _int4_decode_layout(cfg):
+    a = moe.make_args(cfg.T, cfg.H, cfg.E, cfg.I, cfg.top_k, wfmt=cfg.wfmt)
+    return moe.moe_workspace_layout(a)["block_m"]
+
+
+@pytest.mark.parametrize("T", [1, 5, 16, 32])
+def test_int4_decode_small(dev, T):
+    # T = 32: T * top_k = 128 = 8 * E, the largest batch of the decode route
+    cfg = synth.tiny_config(5, T=T, H=1024, I=512, E=16, top_k=4)
+    assert _int4_decode_layout(cfg) == 16
+    _check(cfg)
+
+
+def test_int4_decode_route_boundary(dev):
+    # one token more than the decode route takes: the 64-row tiled kernels
+    cfg = synth.tiny_config(5, T=33, H=1024, I=512, E=16, top_k=4)
+    assert _int4_decode_layout(cfg) == 64
+    _check(cfg)
+
+
+@pytest.mark.parametrize("H,I", [(512, 2048), (1536, 1024), (2048, 3072), (3072, 512), (4096, 1536)])
+def test_int4_decode_streamed(dev, H, I):
+    # K up to 2048 splits over two waves, 3072 and 4096 over four; every piece
+    # carries its 16 rows' group scales (randomised here by up to 2^+-3)
+    cfg = synth.tiny_config(5, T=12, H=H, I=I, E=9, top_k=3)
+    assert _int4_decode_layout(cfg) == 16
+    _check(cfg, inp=_scale_blocks(synth.make_inputs(cfg), cfg.wfmt, seed=H + I))
+
+
+def test_int4_decode_zero_and_wide_scales(dev):
+    # zero group scales (scattered, leading runs, whole rows) and scales
+    # spread over 2^-8 .. 2^8 along a row, on the decode route
+    cfg = synth.tiny_config(5, T=12, H=2048, I=1024, E=6, top_k=2)
+    assert _int4_decode_layout(cfg) == 16
+    inp = synth.make_inputs(cfg)
+    rng = np.random.default_rng(11)
+    out = dict(inp)
+    for k in ("w1_scale", "w2_scale"):
+        f = O.bf16_to_f64(inp[k]) * 2.0 ** rng.integers(-8, 9, size=inp[k].shape)
+        f[rng.random(f.shape) < 0.2] = 0.0
+        f[:, ::7, :2] = 0.0
+        f[:, 3::11, :] = 0.0
+        out[k] = O.f32_to_bf16_rne(f.astype(np.float32))
+    _check(cfg, inp=out)
+
+
+def test_int4_decode_workload_full_size(dev):
+    # workload 5's layer at 16 tokens: every output against the oracle
+    cfg = synth.config(10)
+    assert _int4_decode_layout(cfg) == 16
+    _check(cfg)
+
+
 # ---- weight-only fp8: e4m3 weights with their block scales, bf16 activations
 @pytest.mark.parametrize("T", [1, 5, 16, 33, 128])
 def test_w8a16_small(dev, T):
