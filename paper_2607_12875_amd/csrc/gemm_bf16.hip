@@ -149,20 +149,29 @@ __device__ __forceinline__ bf16x8 e4m3x8_to_bf16(uint32_t lo, uint32_t hi) {
   return r;
 }
 
-// 8 signed nibbles (element k of the word in bits [4k, 4k+4)) -> 8 bf16
-// values 136 + q, exact: bits 0x4300 | (q + 8), i.e. 128 + (q + 8) with the
-// nibble in the low mantissa bits of 128, and q + 8 = n ^ 8 for the two's-
-// complement nibble n.  In the order two operations per dword give: dword d
-// takes nibbles d and d + 4 (bf16 slots 2d, 2d + 1), so slot s holds element
-// {0,4,1,5,2,6,3,7}[s] of the word.  Each half is (n & 0xF) ^ 0x4308: v_bitop3
-// with the truth table of (S0 & S1) ^ S2 over (0xF0, 0xCC, 0xAA), 0x6A.
-__device__ __forceinline__ bf16x8 int4x8_biased_bf16_strided(uint32_t w) {
-  u32x4 r;
-  r.x = __builtin_amdgcn_bitop3_b32(w, 0x000F000Fu, 0x43084308u, 0x6A);
-  r.y = __builtin_amdgcn_bitop3_b32(w >> 4, 0x000F000Fu, 0x43084308u, 0x6A);
-  r.z = __builtin_amdgcn_bitop3_b32(w >> 8, 0x000F000Fu, 0x43084308u, 0x6A);
-  r.w = __builtin_amdgcn_bitop3_b32(w >> 12, 0x000F000Fu, 0x43084308u, 0x6A);
-  return as_bf16x8(r);
+// Two words of 8 signed nibbles each (element k of a word in bits
+// [4k, 4k+4)) -> 2 x 8 bf16 values 136 + q, exact: bits 0x4300 | (q + 8),
+// i.e. 128 + (q + 8) with the nibble in the low mantissa bits of 128, and
+// q + 8 = n ^ 8 for the two's-complement nibble n.  In the order two
+// operations per dword give: dword d takes nibbles d and d + 4 (bf16 slots
+// 2d, 2d + 1), so slot s holds element {0,4,1,5,2,6,3,7}[s] of the word.
+// Each half is (n & 0xF) ^ 0x4308, one v_bitop3 (truth table of
+// (S0 & S1) ^ S2 over (0xF0, 0xCC, 0xAA): 0x6A) on the word shifted right by
+// 4 d.  The shifted copies of both words come from 64-bit shifts of the pair
+// (one v_lshrrev_b64 in place of two 32-bit shifts; the bits of w1 that move
+// into the top of w0's copy are never selected), written as asm because the
+// compiler splits a 64-bit shift into v_alignbit_b32 + v_lshrrev_b32.
+__device__ __forceinline__ void int4x16_biased_bf16_strided(uint32_t w0, uint32_t w1, bf16x8& d0, bf16x8& d1) {
+  const uint64_t pr = static_cast<uint64_t>(w1) << 32 | w0;
+  uint64_t s4, s8, s12;
+  asm("v_lshrrev_b64 %0, 4, %1" : "=v"(s4) : "v"(pr));
+  asm("v_lshrrev_b64 %0, 8, %1" : "=v"(s8) : "v"(pr));
+  asm("v_lshrrev_b64 %0, 12, %1" : "=v"(s12) : "v"(pr));
+  auto dw = [](uint32_t v) { return static_cast<uint32_t>(__builtin_amdgcn_bitop3_b32(v, 0x000F000Fu, 0x43084308u, 0x6A)); };
+  auto lo = [](uint64_t v) { return static_cast<uint32_t>(v); };
+  auto hi = [](uint64_t v) { return static_cast<uint32_t>(v >> 32); };
+  d0 = as_bf16x8(u32x4{dw(w0), dw(lo(s4)), dw(lo(s8)), dw(lo(s12))});
+  d1 = as_bf16x8(u32x4{dw(w1), dw(hi(s4)), dw(hi(s8)), dw(hi(s12))});
 }
 
 // ------------------------------------------------------ streamed (decode)
@@ -279,7 +288,7 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_stream(GroupedGemm g) {
     for (int i = 0; i < 4; ++i) live[i] = GEMM1 || g.sorted_ids[m0 + 4 * kg + i] < g.n_routed;
     vm_wait<0>();
     // int4: each fragment's elements put in the order the weight decode
-    // gives (int4x8_biased_bf16_strided), and nbias[b] = -136 * (each row's
+    // gives (int4x16_biased_bf16_strided), and nbias[b] = -136 * (each row's
     // sum over the quarter's 128-group b), the start of that group's partial
     f32x4 nbias[I4 ? NJ / 4 : 1];
     if constexpr (I4) {
@@ -382,11 +391,11 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_stream(GroupedGemm g) {
           for (int b = 0; b < JP / 4; ++b) {
             const u32x4 wv = ld16(B + 64 * b);
             f32x4 part = nbias[(p * JP) / 4 + b];
+            bf16x8 dq[4];
+            int4x16_biased_bf16_strided(wv.x, wv.y, dq[0], dq[1]);
+            int4x16_biased_bf16_strided(wv.z, wv.w, dq[2], dq[3]);
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-              const uint32_t w = u == 0 ? wv.x : (u == 1 ? wv.y : (u == 2 ? wv.z : wv.w));
-              part = mfma16x16x32(as_bf16x8(a[p * JP + 4 * b + u]), int4x8_biased_bf16_strided(w), part);
-            }
+            for (int u = 0; u < 4; ++u) part = mfma16x16x32(as_bf16x8(a[p * JP + 4 * b + u]), dq[u], part);
             const float sw = __uint_as_float(static_cast<uint32_t>(sc[b]) << 16);  // this lane's weight row
             acc[gi] += part * sw;
           }
