@@ -218,7 +218,7 @@ __device__ __forceinline__ void int4x16_biased_bf16_strided(uint32_t w0, uint32_
 // activations over the group), formed once per run by the MFMA itself, and
 // the lane's weight row scale multiplies it into the accumulator.
 // NG: 16-row weight groups per block (GEMM1: NG/2 gate + NG/2 up); NP
-// pieces of JP MFMAs (32 K elements each) per row and wave: K = 4 * 32 * NP * JP.
+// pieces of JP MFMAs (32 K elements each) per row and wave: K = NWV * 32 * NP * JP.
 
 template <int FMT, int NWV, int NG, int NP, int JP, bool GEMM1>
 __global__ __launch_bounds__(64 * NWV) void gemm_bf16_stream(GroupedGemm g) {
