@@ -31,9 +31,10 @@ def _args(cfg, d, out):
     synth.tiny_config(2, T=16, H=1024, I=1408, E=24, top_k=6),   # streamed decode kernels
     synth.tiny_config(1, T=600, H=512, I=384, E=8, top_k=2),     # tiled bf16 kernels
     synth.tiny_config(5, T=300, H=512, I=256, E=12, top_k=4),    # int4 route
+    synth.tiny_config(5, T=12, H=1024, I=512, E=12, top_k=4),    # int4, streamed decode kernels
     synth.tiny_config(7, T=300, H=512, I=256, E=12, top_k=4),    # MXFP4, tiled
     synth.tiny_config(9, T=300, H=512, I=512, E=12, top_k=4),    # MXFP4 x MXFP8
-], ids=["decode", "tiled", "int4", "mxfp4", "mxfp4x8"])
+], ids=["decode", "tiled", "int4", "int4-decode", "mxfp4", "mxfp4x8"])
 def test_graph_replays_match_eager(dev, cfg):
     print(f"graph replay {cfg}", flush=True)
     d = synth.to_device(synth.make_inputs(cfg))

@@ -27,8 +27,9 @@ def _args(cfg, d, out):
     (dict(n=1, T=300, H=512, I=256, E=8, top_k=2), dict(n=1, T=12, H=512, I=256, E=8, top_k=2)),
     # fp8: 700 tokens, then 40 on a smaller layer
     (dict(n=4, T=700, H=512, I=1024, E=16, top_k=4), dict(n=4, T=40, H=256, I=1024, E=8, top_k=2)),
-    # int4, the full-size skewed workload (226 MiB of workspace), then a small one
-    (dict(n=5), dict(n=5, T=37, H=512, I=256, E=12, top_k=4)),
+    # int4, the full-size skewed workload (226 MiB of workspace, tiled
+    # kernels), then a small batch on the streamed decode kernels
+    (dict(n=5), dict(n=5, T=12, H=1024, I=512, E=12, top_k=4)),
 ])
 def test_static_workspace_matches_caller_workspace(pair):
     require_gpu()
