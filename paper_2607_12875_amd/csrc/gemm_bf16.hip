@@ -1,15 +1,20 @@
-// Grouped expert GEMMs for bf16 weights (the "Fused MoE" node, Fig. 1 /
-// Fig. 3): per expert e, over the rows of its permuted segment,
+// Grouped expert GEMMs with bf16 activations at decode sizes (the "Fused
+// MoE" node, Fig. 1 / Fig. 3): per expert e, over the rows of its permuted
+// segment,
 //   GEMM1  a = SiLU(x W1[e,:I]^T) * (x W1[e,I:]^T)   (SiLU*up fused in the epilogue)
 //   GEMM2  y = a W2[e]^T
 // Weights are [N,K] with K contiguous, so both products read B rows along K.
 //
-// Two kernel families: the LDS-tiled persistent kernel shared with the other
-// formats (gemm_tiled.hip) when experts hold many rows, and here
-//  * skinny (decode: a few rows per expert): 16-row tile, the K range split
-//    over the four waves on 128-byte line boundaries, weight fragments streamed from HBM straight into
-//    registers (no reuse to stage for), v_mfma_f32_16x16x32_bf16, partial sums
-//    reduced through LDS.
+// When experts hold many rows the LDS-tiled persistent kernel of
+// gemm_tiled.hip runs; here are the 16-row kernels for a few rows per expert
+// (no reuse to stage for), all on v_mfma_f32_16x16x32_bf16 with the weights
+// decoded to bf16 in registers and partial sums reduced through LDS:
+//  * streamed (gemm_bf16_stream): the weight slab copied straight into LDS
+//    row by row in long pieces, for bf16, int4, weight-only fp8 and MXFP4
+//    weights;
+//  * skinny (gemm_bf16_skinny, gemm_w8a16_skinny, gemm_w4a16_skinny): the K
+//    range split over the four waves, weight fragments loaded straight into
+//    registers, for the K sizes the streamed kernel does not take.
 // Segments are padded to the row tile, so every tile belongs to one expert;
 // tiles past the last segment exit at once.
 #include <algorithm>
