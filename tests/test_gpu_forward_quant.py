@@ -288,6 +288,19 @@ def test_int4_decode_zero_and_wide_scales(dev):
     _check(cfg, inp=out)
 
 
+def test_int4_decode_concentrated_routing(dev):
+    # every token routed to the same four experts: 32 rows each, so each of
+    # them spans two 16-row tiles and the other experts hold none
+    cfg = synth.tiny_config(5, T=32, H=2048, I=1536, E=16, top_k=4)
+    assert _int4_decode_layout(cfg) == 16
+    inp = synth.make_inputs(cfg)
+    inp = dict(inp)
+    lg = inp["logits"].copy()
+    lg[:, [3, 7, 8, 13]] += 20.0
+    inp["logits"] = lg
+    _check(cfg, inp=inp)
+
+
 def test_int4_decode_workload_full_size(dev):
     # workload 5's layer at 16 tokens: every output against the oracle
     cfg = synth.config(10)
