@@ -86,10 +86,12 @@ typedef enum {
      (T * top_k <= 8 * E, H and I in {512, 1024, 1536, 2048, 3072, 4096}),
      where both products take the first one's exact form.  A scale may be zero;
      the nonzero scales must be normal numbers within a factor 2^64 of each
-     other along a weight row (other scales are unspecified): the first
-     product carries its running sums divided by the current group's scale,
-     so a ratio r between groups multiplies them by r, and 2^64 keeps them
-     inside the fp32 range with about 2^30 to spare for the sums themselves.
+     other along a weight row (other scales are unspecified): above the
+     decode sizes the first product carries its running sums divided by the
+     current group's scale, so a ratio r between groups multiplies them by r,
+     and 2^64 keeps them inside the fp32 range with about 2^30 to spare for
+     the sums themselves (the decode sizes scale each group's own partial
+     and have no such limit).
      Scales from a per-group amax quantiser of real weight rows differ by a
      few powers of two. */
   MOE_W_INT4_G128 = 2,

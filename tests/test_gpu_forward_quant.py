@@ -288,6 +288,21 @@ def test_int4_decode_zero_and_wide_scales(dev):
     _check(cfg, inp=out)
 
 
+def test_int4_decode_scales_beyond_tiled_range(dev):
+    # group scales alternating by 2^+-36 along every weight row: ratios of
+    # 2^72 between neighbouring groups, past the 64-row kernels' 2^64 limit;
+    # the decode kernels scale each group's own partial, so none applies
+    cfg = synth.tiny_config(5, T=12, H=2048, I=1024, E=6, top_k=2)
+    assert _int4_decode_layout(cfg) == 16
+    inp = synth.make_inputs(cfg)
+    out = dict(inp)
+    for k in ("w1_scale", "w2_scale"):
+        f = O.bf16_to_f64(inp[k])
+        f = f * 2.0 ** np.where(np.arange(f.shape[-1]) % 2 == 0, 36, -36)
+        out[k] = O.f32_to_bf16_rne(f.astype(np.float32))
+    _check(cfg, inp=out)
+
+
 def test_int4_decode_concentrated_routing(dev):
     # every token routed to the same four experts: 32 rows each, so each of
     # them spans two 16-row tiles and the other experts hold none
