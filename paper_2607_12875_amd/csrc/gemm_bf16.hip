@@ -270,7 +270,9 @@ __global__ __launch_bounds__(64 * NWV) void gemm_bf16_stream(GroupedGemm g) {
     const int e = find_segment(g.offsets, g.E, m0);
 
     // A fragments: MFMA j covers K [k0 + 32 j, +32), lane group kg its
-    // elements [8 kg, 8 kg + 8); the B fragments use the same K order.
+    // elements [8 kg, 8 kg + 8) (the 128-wide block formats: MFMA 4 b + u
+    // covers block b, lane group kg its elements [32 kg + 8 u, +8)); the B
+    // fragments use the same K order.
     // They (and the pad flags of the rows this lane stores) have landed
     // before the run's first weight copy is issued, and the previous run
     // ended with every copy landed, so the compiler's own wait counts never
