@@ -14,25 +14,64 @@ namespace moe {
 
 constexpr int MOE_GATE_MAX_K = 32;  // the ABI's top_k limit
 
+// Wave reductions without LDS round trips: four DPP steps (VALU lane
+// permutes) inside each row of 16 lanes -- quad_perm [1,0,3,2] (0xB1) and
+// [2,3,0,1] (0x4E) pair lanes at distance 1 and 2, row_half_mirror (0x141)
+// the two quads of a half row, row_mirror (0x140) the two half rows -- after
+// which every lane of a row holds the row's result; the four row results
+// are then read as wave-uniform values and combined in row order.  Every
+// lane of the wave must take part.
+template <int CTRL>
+__device__ __forceinline__ int dpp_i32(int v) {
+  return __builtin_amdgcn_update_dpp(v, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const unsigned long long b = static_cast<unsigned long long>(__double_as_longlong(v));
+  const uint32_t lo = static_cast<uint32_t>(dpp_i32<CTRL>(static_cast<int>(b)));
+  const uint32_t hi = static_cast<uint32_t>(dpp_i32<CTRL>(static_cast<int>(b >> 32)));
+  return __longlong_as_double(static_cast<long long>(static_cast<unsigned long long>(hi) << 32 | lo));
+}
+__device__ __forceinline__ double readlane_f64(double v, int l) {
+  const unsigned long long b = static_cast<unsigned long long>(__double_as_longlong(v));
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(b), l));
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(b >> 32), l));
+  return __longlong_as_double(static_cast<long long>(static_cast<unsigned long long>(hi) << 32 | lo));
+}
+
+// (v, e) <- the better of (v, e) and (ov, oe): larger value, equal values ->
+// lower index.  A total order, so the reduction's pairing does not matter.
+__device__ __forceinline__ void argmax_take(double& v, int& e, double ov, int oe) {
+  if (ov > v || (ov == v && oe < e)) { v = ov; e = oe; }
+}
+
 __device__ __forceinline__ void wave_argmax(double& v, int& e) {
+  argmax_take(v, e, dpp_f64<0xB1>(v), dpp_i32<0xB1>(e));
+  argmax_take(v, e, dpp_f64<0x4E>(v), dpp_i32<0x4E>(e));
+  argmax_take(v, e, dpp_f64<0x141>(v), dpp_i32<0x141>(e));
+  argmax_take(v, e, dpp_f64<0x140>(v), dpp_i32<0x140>(e));
+  double bv = readlane_f64(v, 0);
+  int be = __builtin_amdgcn_readlane(e, 0);
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    double ov = __shfl_xor(v, off);
-    int oe = __shfl_xor(e, off);
-    if (ov > v || (ov == v && oe < e)) { v = ov; e = oe; }
-  }
+  for (int r = 1; r < 4; ++r) argmax_take(bv, be, readlane_f64(v, 16 * r), __builtin_amdgcn_readlane(e, 16 * r));
+  v = bv;
+  e = be;
 }
 
 __device__ __forceinline__ double wave_sum(double v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-  return v;
+  v += dpp_f64<0xB1>(v);
+  v += dpp_f64<0x4E>(v);
+  v += dpp_f64<0x141>(v);
+  v += dpp_f64<0x140>(v);
+  return ((readlane_f64(v, 0) + readlane_f64(v, 16)) + readlane_f64(v, 32)) + readlane_f64(v, 48);
 }
 
 __device__ __forceinline__ double wave_max(double v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off));
-  return v;
+  v = fmax(v, dpp_f64<0xB1>(v));
+  v = fmax(v, dpp_f64<0x4E>(v));
+  v = fmax(v, dpp_f64<0x141>(v));
+  v = fmax(v, dpp_f64<0x140>(v));
+  return fmax(fmax(readlane_f64(v, 0), readlane_f64(v, 16)), fmax(readlane_f64(v, 32), readlane_f64(v, 48)));
 }
 
 // Keys (and the values the weights use) of this lane's experts.
@@ -103,7 +142,7 @@ __device__ __forceinline__ void gate_argmax_row(const float* lg, const float* bi
 #pragma unroll
     for (int i = 0; i < EPL; ++i)
       if (lane + 64 * i == be) v = lv[i];
-    v = __shfl(v, be & 63);
+    v = readlane_f64(v, be & 63);
     if (lane == j) { my_id = be; my_v = v; }
   }
 
