@@ -100,9 +100,19 @@ hipError_t launch_combine(const void* y, bool y_f32, const float* w, const int32
   return hipGetLastError();
 }
 
+// Value of the lane that the DPP control CTRL pairs with this one (a VALU
+// lane permute, no LDS round trip): quad_perm [1,0,3,2] (0xB1) and [2,3,0,1]
+// (0x4E) pair lanes at distance 1 and 2, row_half_mirror (0x141) the two
+// quads of each half of a 16-lane row, row_mirror (0x140) the two halves.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
 // Per (row, 128-column group): s = max(amax, 1e-10) / 448 with an IEEE fp32
 // divide, q = e4m3(RNE(x / s)) after saturating x / s to +-448.  Sixteen lanes
-// own one group (8 columns each); amax is reduced with lane shuffles.  The
+// (one DPP row) own one group (8 columns each); amax is reduced over the row
+// with four DPP steps.  The
 // quotients come from one divide per lane, r = 1 / s, and a residual step per
 // element: q0 = x r, q = q0 + fma(-q0, s, x) r.  That q can differ from the
 // IEEE quotient in its last fp32 bit, but for bf16 x it always lands on the
@@ -126,8 +136,10 @@ __global__ __launch_bounds__(256) void act_quant_kernel(
   float amax = 0.f;
 #pragma unroll
   for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(f[i]));
-#pragma unroll
-  for (int off = 1; off < 16; off <<= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
+  amax = fmaxf(amax, dpp_f32<0xB1>(amax));
+  amax = fmaxf(amax, dpp_f32<0x4E>(amax));
+  amax = fmaxf(amax, dpp_f32<0x141>(amax));
+  amax = fmaxf(amax, dpp_f32<0x140>(amax));
   const float sc = fmaxf(amax, 1e-10f) / 448.0f;
   if (!live) return;
   const float r = 1.0f / sc;
@@ -177,8 +189,8 @@ __global__ __launch_bounds__(256) void act_quant_mx_kernel(
   float amax = 0.f;
 #pragma unroll
   for (int i = 0; i < 8; ++i) amax = fmaxf(amax, fabsf(f[i]));
-  amax = fmaxf(amax, __shfl_xor(amax, 1));
-  amax = fmaxf(amax, __shfl_xor(amax, 2));
+  amax = fmaxf(amax, dpp_f32<0xB1>(amax));
+  amax = fmaxf(amax, dpp_f32<0x4E>(amax));
   if (!live) return;
   const uint32_t byte = mx_e8m0_of_amax(amax);
   const float mul = __uint_as_float((254u - byte) << 23);  // 2^(127 - byte), a normal fp32
@@ -201,7 +213,7 @@ hipError_t launch_act_quant_mx(const uint16_t* x, int M, int K, uint8_t* q, uint
 
 // Per (row, 128-column group): -136 times the fp32 sum of the group's values,
 // the term the int4 GEMM1 takes off its biased codes (136 + q).  Sixteen
-// lanes own one group, as in the quantiser above.
+// lanes (one DPP row) own one group, as in the quantiser above.
 __global__ __launch_bounds__(256) void group_sum_kernel(const uint16_t* __restrict__ x, int M, int K,
                                                          float* __restrict__ out) {
   const long idx = static_cast<long>(blockIdx.x) * 256 + threadIdx.x;  // one per 8 columns
@@ -213,8 +225,10 @@ __global__ __launch_bounds__(256) void group_sum_kernel(const uint16_t* __restri
   float sum = 0.f;
 #pragma unroll
   for (int i = 0; i < 4; ++i) sum += __uint_as_float(u[i] << 16) + __uint_as_float(u[i] & 0xFFFF0000u);
-#pragma unroll
-  for (int off = 1; off < 16; off <<= 1) sum += __shfl_xor(sum, off);
+  sum += dpp_f32<0xB1>(sum);
+  sum += dpp_f32<0x4E>(sum);
+  sum += dpp_f32<0x141>(sum);
+  sum += dpp_f32<0x140>(sum);
   if (live && (threadIdx.x & 15) == 0) out[idx / 16] = -136.0f * sum;
 }
 
