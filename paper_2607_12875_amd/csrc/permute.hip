@@ -38,23 +38,32 @@ __global__ __launch_bounds__(kPermThreads) void permute_count_kernel(
   for (int e = threadIdx.x; e < E; e += blockDim.x) counts[blockIdx.x * E + e] = hist[e];
 }
 
-// Inclusive scan of one int per thread across the block (blockDim = 1024).
+// Inclusive scan inside each 16-lane row of the wave with DPP shifts
+// (row_shr:n, 0x110 + n; lanes whose source falls before the row read 0):
+// VALU lane moves in place of ds_bpermute round trips.
+__device__ __forceinline__ int row_inclusive_scan(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, true);
+  return v;
+}
+
+// Inclusive scan of one int per thread across the block (blockDim = 1024):
+// rows of 16 lanes, then the rows of each wave joined with row_bcast:15
+// (0x142: lane 15 of rows 0 and 2 added to rows 1 and 3) and row_bcast:31
+// (0x143: lane 31 added to rows 2 and 3), then the waves through LDS.
 __device__ __forceinline__ int block_inclusive_scan(int v, int* wave_tot) {
   const int lane = lane_id(), wv = threadIdx.x >> 6;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int o = __shfl_up(v, off);
-    if (lane >= off) v += o;
-  }
+  v = row_inclusive_scan(v);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);
   if (lane == 63) wave_tot[wv] = v;
   __syncthreads();
   if (wv == 0) {
+    static_assert(kPermThreads / 64 <= 16, "the wave totals fit one row");
     int t = lane < (kPermThreads / 64) ? wave_tot[lane] : 0;
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) {
-      const int o = __shfl_up(t, off);
-      if (lane >= off) t += o;
-    }
+    t = row_inclusive_scan(t);
     if (lane < (kPermThreads / 64)) wave_tot[lane] = t;
   }
   __syncthreads();
