@@ -243,8 +243,36 @@ __global__ __launch_bounds__(256) void router_select_kernel(const float* __restr
                          w2 ? w2 + o : nullptr);
 }
 
+// Rows of the logits product as one expert segment of the grouped GEMM:
+// position p holds token p (p < T) or the pad id T, offsets {0, cap}.
+__global__ __launch_bounds__(256) void router_rows_kernel(int T, int cap, int32_t* __restrict__ ids,
+                                                          int32_t* __restrict__ offs) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < cap) ids[i] = i < T ? i : T;
+  if (i == 0) {
+    offs[0] = 0;
+    offs[1] = cap;
+  }
+}
+
 namespace {
 constexpr int kRouterSplitMaxT = 64;  // the two-launch form up to this many tokens
+#ifndef MOE_ROUTER_GEMM_MIN_TE
+#define MOE_ROUTER_GEMM_MIN_TE (1L << 20)
+#endif
+// Many tokens times many experts: the logits as a plain GEMM on the tiled
+// bf16 kernel (128-token tiles, every workgroup reading its weight tile once
+// per K step), then the gate on them.  The single kernel below makes each
+// 16-token workgroup read the whole router matrix, which a large E·H makes
+// bound by one CU's read rate (307 µs on 8192 tokens x 256 experts x 7168).
+bool router_as_gemm(int T, int E) {
+  return T > kRouterSplitMaxT && E % 8 == 0 && static_cast<long>(T) * E >= MOE_ROUTER_GEMM_MIN_TE;
+}
+size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+size_t router_gemm_cap(int T) {
+  const int bm = bf16_tiled_block_m();
+  return static_cast<size_t>((T + bm - 1) / bm) * bm;
+}
 // K slices of the split router: enough workgroups to spread the router matrix
 // over the CUs, slices of at least 128 elements, at most 32 of them.
 int router_ks(int T, int H, int E) {
@@ -256,6 +284,8 @@ int router_ks(int T, int H, int E) {
 }  // namespace
 
 size_t router_workspace_bytes(int T, int H, int E) {
+  if (router_as_gemm(T, E))  // row ids, segment offsets, logits
+    return align256(router_gemm_cap(T) * sizeof(int32_t)) + 256 + align256(static_cast<size_t>(T) * E * sizeof(float));
   if (T > kRouterSplitMaxT) return 0;
   return static_cast<size_t>(router_ks(T, H, E)) * T * E * sizeof(float);
 }
@@ -264,6 +294,37 @@ hipError_t launch_router_gate(const uint16_t* hidden, const uint16_t* wr, int T,
                               int renorm, float scale, const float* bias, float* logits_out, int32_t* ids,
                               float* w, int32_t* ids2, float* w2, void* ws, hipStream_t s) {
   const int epl = (E + 63) / 64;
+  if (router_as_gemm(T, E)) {
+    const size_t cap = router_gemm_cap(T);
+    int32_t* rows = static_cast<int32_t*>(ws);
+    int32_t* offs = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + align256(cap * sizeof(int32_t)));
+    float* lg = reinterpret_cast<float*>(reinterpret_cast<char*>(offs) + 256);
+    // the product's y stores are 16-byte: a caller's logits buffer is written
+    // directly when it is 16-byte aligned, else the gate reads the workspace
+    // copy and it is copied out after
+    const bool direct = logits_out && reinterpret_cast<uintptr_t>(logits_out) % 16 == 0;
+    hipLaunchKernelGGL(router_rows_kernel, dim3(static_cast<unsigned>((cap + 255) / 256)), dim3(256), 0, s, T,
+                       static_cast<int>(cap), rows, offs);
+    GroupedGemm g{};
+    g.x = hidden;  // unread by the second product
+    g.sorted_ids = rows;
+    g.offsets = offs;
+    g.T = T;
+    g.H = E;  // output columns: the experts
+    g.E = 1;  // one segment: every token against the whole router matrix
+    g.I = H;  // K
+    g.top_k = 1;
+    g.n_routed = T;
+    g.max_rows = static_cast<int>(cap);
+    g.w2 = wr;
+    g.inter = const_cast<uint16_t*>(hidden);  // A rows: the hidden rows in order (pad rows are never read)
+    g.y = direct ? logits_out : lg;
+    hipError_t err = launch_gemm2_bf16_tiled(g, s);
+    if (err != hipSuccess) return err;
+    err = launch_gate_topk(direct ? logits_out : lg, bias, T, E, k, mode, renorm, scale, ids, w, ids2, w2, s);
+    if (err != hipSuccess || !logits_out || direct) return err;
+    return hipMemcpyAsync(logits_out, lg, static_cast<size_t>(T) * E * sizeof(float), hipMemcpyDeviceToDevice, s);
+  }
   if (T > kRouterSplitMaxT) {
     // KS slices of K per column-tile group, U K-steps of 32 loaded ahead per
     // stage; the partial logits of all slices fit in LDS.  H % 128 == 0, so

@@ -156,6 +156,13 @@ def test_gate_and_permute_validation():
     assert R(FAKE, FAKE, 4, 256, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, FAKE + 4, BIG, None) == 4
     need = L.moe_router_workspace_bytes(4, 256, 8)
     assert need > 0 and L.moe_router_workspace_bytes(4, 200, 8) == 0
+    # many tokens x many experts: row ids (padded to 128 rows), offsets and
+    # the logits of the GEMM form; fewer: the single kernel needs none
+    al = lambda b: (b + 255) // 256 * 256  # noqa: E731
+    assert L.moe_router_workspace_bytes(8192, 7168, 256) == al(8192 * 4) + 256 + al(8192 * 256 * 4)
+    assert L.moe_router_workspace_bytes(4100, 512, 256) == al(4224 * 4) + 256 + al(4100 * 256 * 4)
+    assert L.moe_router_workspace_bytes(4096, 4096, 64) == 0
+    assert L.moe_router_workspace_bytes(8192, 512, 100) == 0   # E % 8 != 0: the single kernel
     assert R(FAKE, FAKE, 4, 256, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, FAKE, need - 1, None) == 5
     assert R(FAKE, FAKE, 4, 256, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, None, BIG, None) == 5
     assert R(None, None, 0, 256, 8, 2, 0, 1, 1.0, None, None, None, None, None, 0, None) == 0

@@ -58,12 +58,33 @@ def _check_router(dev, cfg, sample=None):
 
 
 @pytest.mark.parametrize("T,H,E,k", [(1, 128, 8, 2), (16, 4096, 64, 6), (37, 512, 100, 7),
-                                     (77, 256, 16, 4), (300, 1024, 300, 8), (20, 384, 1024, 32)])
+                                     (77, 256, 16, 4), (300, 1024, 300, 8), (20, 384, 1024, 32),
+                                     (4100, 512, 256, 8)])
 @pytest.mark.parametrize("n", [2, 4])
 def test_router_gate_shapes(dev, T, H, E, k, n):
     # n = 2: softmax renormalised; n = 4: sigmoid + selection bias x 2.5 (rank
     # selection up to 64 experts, arg-max rounds above)
     _check_router(dev, synth.tiny_config(n, T=T, H=H, E=E, top_k=k))
+
+
+def test_router_gemm_route_unaligned_logits(dev):
+    # many tokens x many experts take the logits product on the tiled GEMM
+    # (4100 tokens: a ragged last 128-row tile); a logits buffer that is only
+    # 4-byte aligned gets the same values through the workspace copy
+    cfg = synth.tiny_config(4, T=4100, H=512, E=256, top_k=8)
+    r = synth.make_routing_inputs(cfg)
+    wr = _bf16(synth.make_router_weights(cfg), dev)
+    hid = _bf16(r["hidden"], dev)
+    bias = torch.from_numpy(r["sel_bias"]).to(dev)
+    a = torch.empty((cfg.T, cfg.E), dtype=torch.float32, device=dev)
+    buf = torch.empty(cfg.T * cfg.E + 1, dtype=torch.float32, device=dev)
+    b = buf[1:].view(cfg.T, cfg.E)
+    assert b.data_ptr() % 16 != 0
+    args = (cfg.top_k, cfg.mode, cfg.renormalize, cfg.routed_scale)
+    ia, wa = moe.moe_router_gate_topk(hid, wr, *args, sel_bias=bias, logits=a)
+    ib, wb = moe.moe_router_gate_topk(hid, wr, *args, sel_bias=bias, logits=b)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b) and torch.equal(ia, ib) and torch.equal(wa, wb)
 
 
 def test_router_gate_workload_shapes(dev):
@@ -73,9 +94,11 @@ def test_router_gate_workload_shapes(dev):
     _check_router(dev, synth.config(4))
 
 
-@pytest.mark.parametrize("n,T", [(2, 16), (1, 300), (4, 200), (6, 16)])
-def test_forward_with_router(dev, n, T):
-    cfg = synth.tiny_config(n, T=T)
+@pytest.mark.parametrize("n,T,over", [(2, 16, {}), (1, 300, {}), (4, 200, {}), (6, 16, {}),
+                                      (2, 4096, dict(H=256, E=256, I=128))])
+def test_forward_with_router(dev, n, T, over):
+    # the last case's logits come from the tiled GEMM (4096 tokens x 256 experts)
+    cfg = synth.tiny_config(n, T=T, **over)
     print(f"forward with router {cfg}", flush=True)
     inp = synth.make_inputs(cfg)
     wr = synth.make_router_weights(cfg)
