@@ -27,7 +27,8 @@ def test_two_streams_match_sequential():
     require_gpu()
     cfgs = [synth.tiny_config(4, T=600, H=512, I=1024, E=16, top_k=4),   # fp8, tiled
             synth.tiny_config(3, T=900, H=384, I=256, E=12, top_k=3),    # bf16, tiled
-            synth.tiny_config(2, T=12, H=1024, I=512, E=24, top_k=4)]    # bf16, streamed decode
+            synth.tiny_config(2, T=12, H=1024, I=512, E=24, top_k=4),    # bf16, streamed decode
+            synth.tiny_config(5, T=12, H=1024, I=512, E=12, top_k=4)]    # int4, streamed decode
     layers = []
     for cfg in cfgs:
         print(f"concurrency layer {cfg}", flush=True)
