@@ -153,13 +153,13 @@ moe_status moe_gate_topk(const float* logits, const float* sel_bias, int T, int 
  * Router GEMM in front of the gate (the step before the MoE Gate node,
  * Fig. 1): logits[t,e] = sum_h hidden[t,h] * w_router[e,h], bf16 products
  * accumulated in fp32, then exactly the selection and weights of
- * moe_gate_topk on those fp32 logits.  Two launches: the logits GEMM in K
- * slices over many workgroups (partial logits in ws), then one wavefront
- * per token that sums the slices in slice order and selects (up to 64
- * tokens); above 64 tokens, where T * E >= 2^20 and E % 8 == 0, the logits
- * as a plain GEMM over 128-token tiles (row ids, offsets and logits in ws)
- * and then the gate; otherwise one kernel per 16-token tile, and no
- * scratch.
+ * moe_gate_topk on those fp32 logits.  Where T * E >= 2^20 (E % 8 == 0
+ * and T > 64): the logits as a plain GEMM over 128-token tiles (row ids,
+ * offsets and logits in ws), then the gate.  Otherwise up to 1024 tokens two
+ * launches: the logits GEMM in K slices over many workgroups (partial
+ * logits in ws; 16-token tiles up to 64 tokens, 64-token tiles above), then
+ * one wavefront per token that sums the slices in slice order and selects;
+ * above 1024 tokens one kernel per 16-token tile, and no scratch.
  *   hidden    device bf16 bits [T,H], 16-byte aligned; H % 128 == 0, H <= 65536
  *   w_router  device bf16 bits [E,H], 16-byte aligned
  *   logits    device fp32 [T,E] or NULL: receives the logits the selection used

@@ -256,7 +256,7 @@ __global__ __launch_bounds__(256) void router_rows_kernel(int T, int cap, int32_
 }
 
 namespace {
-constexpr int kRouterSplitMaxT = 64;  // the two-launch form up to this many tokens
+constexpr int kRouterSplitMaxT = 64;  // the two-launch form's 16-token tiles up to this many tokens
 #ifndef MOE_ROUTER_GEMM_MIN_TE
 #define MOE_ROUTER_GEMM_MIN_TE (1L << 20)
 #endif
@@ -275,8 +275,18 @@ size_t router_gemm_cap(int T) {
 }
 // K slices of the split router: enough workgroups to spread the router matrix
 // over the CUs, slices of at least 128 elements, at most 32 of them.
+// From 65 to kRouterMidMaxT tokens the two-launch form takes 64-token tiles
+// (four 16-token tiles per workgroup, each weight fragment used four times):
+// there the single kernel has too few 16-token workgroups to fill the device
+// (router stage, two-launch / single kernel: 18.6 / 38.6 us at 256 tokens and
+// 64 experts, 32.7 / 57.5 at 512 and 128, 30.6 / 42.4 at 1024 and 64;
+// at 2048 tokens the single kernel is ahead).
+constexpr int kRouterMidMaxT = 1024;
+constexpr int kMidTT = 4;
+bool router_split(int T) { return T <= kRouterMidMaxT; }
 int router_ks(int T, int H, int E) {
-  const long tiles = static_cast<long>((T + 15) / 16) * ((E + 63) / 64);
+  const int tt = T > kRouterSplitMaxT ? kMidTT : 1;
+  const long tiles = static_cast<long>((T + 16 * tt - 1) / (16 * tt)) * ((E + 63) / 64);
   int ks = 1;
   while (ks < kRouterMaxKS && tiles * ks < 256 && H % (64 * ks) == 0 && H / (2 * ks) >= 128) ks *= 2;
   return ks;
@@ -286,7 +296,7 @@ int router_ks(int T, int H, int E) {
 size_t router_workspace_bytes(int T, int H, int E) {
   if (router_as_gemm(T, E))  // row ids, segment offsets, logits
     return align256(router_gemm_cap(T) * sizeof(int32_t)) + 256 + align256(static_cast<size_t>(T) * E * sizeof(float));
-  if (T > kRouterSplitMaxT) return 0;
+  if (!router_split(T)) return 0;
   return static_cast<size_t>(router_ks(T, H, E)) * T * E * sizeof(float);
 }
 
@@ -325,7 +335,7 @@ hipError_t launch_router_gate(const uint16_t* hidden, const uint16_t* wr, int T,
     if (err != hipSuccess || !logits_out || direct) return err;
     return hipMemcpyAsync(logits_out, lg, static_cast<size_t>(T) * E * sizeof(float), hipMemcpyDeviceToDevice, s);
   }
-  if (T > kRouterSplitMaxT) {
+  if (!router_split(T)) {
     // KS slices of K per column-tile group, U K-steps of 32 loaded ahead per
     // stage; the partial logits of all slices fit in LDS.  H % 128 == 0, so
     // every slice is whole K-steps.  16-token tiles keep the most CUs busy
@@ -344,10 +354,15 @@ hipError_t launch_router_gate(const uint16_t* hidden, const uint16_t* wr, int T,
   }
   const int KS = router_ks(T, H, E), hs = H / KS;
   float* part = static_cast<float*>(ws);
-  const dim3 g1((T + 15) / 16, (E + 63) / 64, KS);
-  // all of a short slice's K steps in flight at once
-  if (hs <= 128) hipLaunchKernelGGL((router_partial_kernel<1, 4>), g1, dim3(256), 0, s, hidden, wr, T, H, E, hs, part);
-  else hipLaunchKernelGGL((router_partial_kernel<1, 8>), g1, dim3(256), 0, s, hidden, wr, T, H, E, hs, part);
+  if (T > kRouterSplitMaxT) {
+    const dim3 gm((T + 16 * kMidTT - 1) / (16 * kMidTT), (E + 63) / 64, KS);
+    hipLaunchKernelGGL((router_partial_kernel<kMidTT, 4>), gm, dim3(256), 0, s, hidden, wr, T, H, E, hs, part);
+  } else {
+    const dim3 g1((T + 15) / 16, (E + 63) / 64, KS);
+    // all of a short slice's K steps in flight at once
+    if (hs <= 128) hipLaunchKernelGGL((router_partial_kernel<1, 4>), g1, dim3(256), 0, s, hidden, wr, T, H, E, hs, part);
+    else hipLaunchKernelGGL((router_partial_kernel<1, 8>), g1, dim3(256), 0, s, hidden, wr, T, H, E, hs, part);
+  }
   const dim3 g2((T + 3) / 4);
 #define MOE_ROUTER_SEL(N)                                                                                  \
   hipLaunchKernelGGL(router_select_kernel<N>, g2, dim3(256), 0, s, part, KS, T, E, k, mode, renorm, scale, \

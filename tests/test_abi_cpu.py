@@ -162,6 +162,8 @@ def test_gate_and_permute_validation():
     assert L.moe_router_workspace_bytes(8192, 7168, 256) == al(8192 * 4) + 256 + al(8192 * 256 * 4)
     assert L.moe_router_workspace_bytes(4100, 512, 256) == al(4224 * 4) + 256 + al(4100 * 256 * 4)
     assert L.moe_router_workspace_bytes(4096, 4096, 64) == 0
+    assert L.moe_router_workspace_bytes(300, 1024, 300) > 0    # 64-token tiles in K slices up to 1024 tokens
+    assert L.moe_router_workspace_bytes(1025, 1024, 300) == 0
     assert L.moe_router_workspace_bytes(8192, 512, 100) == 0   # E % 8 != 0: the single kernel
     assert R(FAKE, FAKE, 4, 256, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, FAKE, need - 1, None) == 5
     assert R(FAKE, FAKE, 4, 256, 8, 2, 0, 1, 1.0, None, None, FAKE, FAKE, None, BIG, None) == 5
