@@ -129,7 +129,7 @@ class HipEvents:
 
 
 def measure_peaks(moe, torch) -> dict:
-    """Achievable peaks of this machine, from the library's probes (see
+    """Achievable peaks of this device, from the library's probes (see
     include/moe_peaks.h), each timed with HIP events over three launches on
     torch's current stream: MFMA-only loops in bf16 and fp8 (TFLOP/s), a
     2 GiB streaming read and a 2 GiB streaming copy (read + write bytes),
