@@ -288,6 +288,15 @@ def test_int4_decode_zero_and_wide_scales(dev):
     _check(cfg, inp=out)
 
 
+@pytest.mark.parametrize("shape", [dict(T=8, H=512, I=512, E=1, top_k=1),     # one expert, both K minimal
+                                   dict(T=1, H=4096, I=4096, E=4, top_k=1),    # one token, the largest K
+                                   dict(T=3, H=2048, I=512, E=64, top_k=2)])   # most experts empty
+def test_int4_decode_edges(dev, shape):
+    cfg = synth.tiny_config(5, **shape)
+    assert _int4_decode_layout(cfg) == 16
+    _check(cfg)
+
+
 def test_int4_decode_scales_beyond_tiled_range(dev):
     # group scales alternating by 2^+-36 along every weight row: ratios of
     # 2^72 between neighbouring groups, past the 64-row kernels' 2^64 limit;
