@@ -264,7 +264,7 @@ constexpr int kRouterSplitMaxT = 64;  // the two-launch form's 16-token tiles up
 // bf16 kernel (128-token tiles, every workgroup reading its weight tile once
 // per K step), then the gate on them.  The single kernel below makes each
 // 16-token workgroup read the whole router matrix, which a large E·H makes
-// bound by one CU's read rate (307 µs on 8192 tokens x 256 experts x 7168).
+// bound by one CU's read rate (307 us on 8192 tokens x 256 experts x 7168).
 bool router_as_gemm(int T, int E) {
   return T > kRouterSplitMaxT && E % 8 == 0 && static_cast<long>(T) * E >= MOE_ROUTER_GEMM_MIN_TE;
 }
@@ -273,8 +273,6 @@ size_t router_gemm_cap(int T) {
   const int bm = bf16_tiled_block_m();
   return static_cast<size_t>((T + bm - 1) / bm) * bm;
 }
-// K slices of the split router: enough workgroups to spread the router matrix
-// over the CUs, slices of at least 128 elements, at most 32 of them.
 // From 65 to kRouterMidMaxT tokens the two-launch form takes 64-token tiles
 // (four 16-token tiles per workgroup, each weight fragment used four times):
 // there the single kernel has too few 16-token workgroups to fill the device
@@ -284,6 +282,8 @@ size_t router_gemm_cap(int T) {
 constexpr int kRouterMidMaxT = 1024;
 constexpr int kMidTT = 4;
 bool router_split(int T) { return T <= kRouterMidMaxT; }
+// K slices of the split router: enough workgroups to spread the router matrix
+// over the CUs, slices of at least 128 elements, at most 32 of them.
 int router_ks(int T, int H, int E) {
   const int tt = T > kRouterSplitMaxT ? kMidTT : 1;
   const long tiles = static_cast<long>((T + 16 * tt - 1) / (16 * tt)) * ((E + 63) / 64);
